@@ -1,0 +1,157 @@
+"""Throughput of the coupled + routed path (with gradient) on one MI355X.
+
+One step = one saki_couple call with fused routing and an fp32 gradient over
+the whole 'large' workload: 64 sequences x 1024 positions = 65,536 rows of
+V = 151,936 bf16 student and teacher logits, resident in HBM.  Prints one
+JSON line.  --gpus N with N > 1 exits: this build runs on one GPU.
+"""
+import argparse
+import json
+import multiprocessing as mp
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
+
+
+def _oracle_rows(args):
+    """CPU oracle on a batch of rows (runs in a worker process)."""
+    os.environ.setdefault("OMP_NUM_THREADS", "1")
+    import numpy as np
+    from oracle import coupling, routing
+    s, t, eps, seed, offsets = args
+    t0 = time.perf_counter()
+    for i in range(s.shape[0]):
+        ev = coupling.couple_rows(s[i:i + 1], t[i:i + 1], eps, seed, int(offsets[i]))
+        routing.couple_and_route(ev, s[i:i + 1], None, 1.0, want_grad=True)
+    return time.perf_counter() - t0
+
+
+def cpu_baseline(s, t, eps, seed, n_sample, workers):
+    """The float64 oracle (as it stands) on a bounded sample of the same rows."""
+    import numpy as np
+    import torch
+    n = s.shape[0]
+    rows = np.linspace(0, n - 1, n_sample).astype(np.int64)
+    idx = torch.as_tensor(rows, device=s.device)
+    S = s[idx].float().cpu().numpy().astype(np.float64)
+    T = t[idx].float().cpu().numpy().astype(np.float64)
+    parts = np.array_split(np.arange(n_sample), workers)
+    jobs = [(S[p], T[p], eps, seed, rows[p]) for p in parts if len(p)]
+    ctx = mp.get_context("spawn")
+    with ctx.Pool(len(jobs)) as pool:
+        pool.map(_noop, range(len(jobs)))  # start the workers before timing
+        t0 = time.perf_counter()
+        busy = pool.map(_oracle_rows, jobs)
+        wall = time.perf_counter() - t0
+    return dict(value=n_sample / wall, unit="positions/s", cores=len(jobs), kind="oracle",
+                sample=f"{n_sample} rows of the same workload (evenly spaced), coupling + routed "
+                       f"loss + gradient, {len(jobs)} single-threaded worker processes; "
+                       f"{sum(busy):.1f} s of CPU work in {wall:.1f} s wall")
+
+
+def _noop(x):
+    return x
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--eps", type=float, default=0.2)
+    ap.add_argument("--rows", type=int, default=None, help="override the row count (debug)")
+    ap.add_argument("--cpu-sample", type=int, default=64)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(rows shard across GPUs without communication; see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_36601_amd as saki
+    from paper_2609_36601_amd import workloads
+
+    saki.load()
+    dev = torch.device("cuda:0")
+    cfg = workloads.CONFIGS["large"]
+    n = args.rows or cfg["rows"]
+    V = cfg["V"]
+    seed = workloads.coupling_seed("large")
+    print(f"# generating {n} x {V} bf16 student/teacher rows", file=sys.stderr, flush=True)
+    s = torch.empty(n, V, dtype=torch.bfloat16, device=dev)
+    t = torch.empty_like(s)
+    workloads.fill("large", s, t)
+    grad = torch.empty(n, V, dtype=torch.float32, device=dev)
+    out = saki.alloc_couple_out(n, dev)
+    route = dict(valid_mask=None, grad_scale=1.0 / n,
+                 row_loss=torch.empty(n, dtype=torch.float32, device=dev),
+                 loss_sum=torch.empty(1, dtype=torch.float64, device=dev), grad=grad)
+    ws = torch.empty(max(saki.workspace_bytes(saki.SAKI_OP_COUPLE, n, V), 8), dtype=torch.uint8,
+                     device=dev)
+    torch.cuda.synchronize()
+
+    def step():
+        saki.saki_couple(s, t, args.eps, seed, 0, out, route, ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    t_wall = time.perf_counter()
+    ev[0].record(stream)
+    for i in range(args.steps):
+        step()
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+    ms = sum(per) / len(per)
+    print(f"# per-step ms: {[round(x, 3) for x in per]} (wall {wall:.3f} s)", file=sys.stderr, flush=True)
+
+    bytes_per_row = 2 * V * 2 + V * 4  # s + t read once (bf16), fp32 gradient written once
+    achieved = n * bytes_per_row / (ms * 1e-3) / 1e9
+    corr_rate = float(out["corrected"].float().mean())
+    mean_tv = float(out["tv"].mean())
+    mean_lam = float(out["lambda"].mean())
+    print(f"# correction rate {corr_rate:.4f}, mean TV {mean_tv:.4f}, mean lambda {mean_lam:.4f}",
+          file=sys.stderr, flush=True)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        workers = max(1, min(16, os.cpu_count() or 1))
+        cpu = cpu_baseline(s, t, args.eps, seed, args.cpu_sample, workers)
+
+    line = {
+        "metric": "coupled+routed positions/sec at V=151,936 bf16; % of MI355X peak HBM GB/s",
+        "value": n / (ms * 1e-3),
+        "unit": "positions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 in, f32/f64 accumulation, f32 gradient",
+        "data": "synthetic",
+        "config": {"workload": "large: 64 seq x 1024 pos = 65,536 rows, V=151,936 bf16, "
+                               "rho~U(0.3,0.95), coupling + routed loss + fp32 grad",
+                   "rows": n, "vocab": V, "eps": args.eps, "grad_dtype": "f32"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None},
+        "cpu_baseline": cpu,
+        "stats": {"correction_rate": corr_rate, "mean_tv": mean_tv, "mean_lambda": mean_lam},
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,189 @@
+/*
+ * saki.h -- C ABI of the SAKI coupling-and-routing library for AMD MI355X (gfx950).
+ *
+ * Per position (one row of [positions x vocab] logits) the library
+ *   1. forms the student p = softmax(s) and teacher pi = softmax(t);
+ *   2. finds the trust-region bridge coefficient lambda*, the largest lambda in
+ *      [0, 1] with KL(q_lambda || p) <= eps, where q_lambda is proportional to
+ *      p^(1-lambda) * pi^lambda                     (SAKI Sec. 3.2, Eq. bridge,
+ *                                                    Eq. trust_region, App. A);
+ *   3. realises q = q_lambda* by maximal coupling with p: z ~ p, accept with
+ *      probability min(1, q(z)/p(z)), else draw a correction from the normalised
+ *      positive residual [q - p]_+                (Sec. 3.3, Eq. accept, Eq. residual);
+ *   4. routes the loss: sampled-token reverse KL at accepted rows, the teacher
+ *      argmax cross-entropy at corrections, and writes its gradient with respect
+ *      to the student logits                      (Sec. 3.4, Eq. general_objective, App. H);
+ *   5. for speculative blocks of k drafted tokens, commits the longest accepted
+ *      prefix and draws the correction at the first rejection
+ *                                                 (Sec. 3.5, App. F, App. I).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory.     Every array argument is DEVICE memory owned by the caller.  The
+ *             library never allocates, frees or synchronises; scratch space is
+ *             the caller's workspace, sized by saki_workspace_bytes().
+ * Streams.    Every call only enqueues work on `stream` (a hipStream_t; NULL is
+ *             the default stream) and returns without waiting for it.
+ * Layout.     Logit rows are row-major, contiguous in the vocabulary:
+ *             element (r, v) is at base[r * row_stride + v].  The base pointer
+ *             must be 16-byte aligned and row_stride * sizeof(element) a
+ *             multiple of 16.  1 <= vocab <= SAKI_MAX_VOCAB, row_stride >= vocab.
+ * Randomness. Draws come from Philox-4x32-10 (Salmon et al., SC'11) keyed by
+ *             (seed, stream id, global row g = row_offset + r), so results are
+ *             a deterministic function of (input bits, eps, seed, g) and do not
+ *             depend on launch geometry or on how rows are split into calls.
+ * Errors.     Argument errors are found on the host before anything is
+ *             enqueued and return a SAKI_E_* code (details: saki_last_error()).
+ *             Data errors found on the device never abort: the row gets a
+ *             non-zero row_status, NaN in its float outputs and -1 in its index
+ *             outputs, and other rows are unaffected.  No C++ exception crosses
+ *             this interface.  n_rows == 0 returns SAKI_OK and enqueues nothing.
+ */
+#ifndef SAKI_H
+#define SAKI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SAKI_MAX_VOCAB (1 << 21) /* 2,097,152 entries per row */
+#define SAKI_CHUNK 1024          /* vocab entries per race chunk (sampler definition) */
+#define SAKI_MAX_BLOCK_K 64      /* largest speculative block length */
+
+typedef void *saki_stream_t; /* a hipStream_t; NULL = the default stream */
+
+typedef enum { SAKI_F32 = 0, SAKI_BF16 = 1 } saki_dtype;
+
+typedef enum {
+  SAKI_OK = 0,
+  SAKI_E_NULLPTR = 1,   /* a required pointer is NULL */
+  SAKI_E_SHAPE = 2,     /* n_rows < 0, vocab outside [1, SAKI_MAX_VOCAB], row_stride < vocab, bad k */
+  SAKI_E_VALUE = 3,     /* eps < 0 or NaN, grad_scale not finite, row_offset < 0 */
+  SAKI_E_DTYPE = 4,     /* unknown saki_dtype */
+  SAKI_E_ALIGN = 5,     /* base pointer or row pitch not 16-byte aligned */
+  SAKI_E_WORKSPACE = 6, /* workspace NULL or smaller than saki_workspace_bytes() */
+  SAKI_E_DEVICE = 7,    /* no usable HIP device, or a HIP call failed */
+  SAKI_E_LAUNCH = 8     /* a kernel launch failed */
+} saki_status;
+
+/* Row status codes written to saki_couple_out.row_status. */
+#define SAKI_ROW_OK 0
+#define SAKI_ROW_NONFINITE 1 /* a student or teacher logit is NaN or infinite */
+#define SAKI_ROW_BAD_DRAFT 2 /* a draft token id is outside [0, vocab) */
+#define SAKI_ROW_SKIPPED 3   /* verify: position after the end of the committed prefix */
+
+/* Student and teacher logits for n_rows positions (Sec. 3.1: p at prefix h_t and
+ * pi_T at the same prefix).  Both arrays have the same dtype, shape and stride. */
+typedef struct {
+  const void *student; /* [n_rows, row_stride]; p = softmax(student row)            */
+  const void *teacher; /* [n_rows, row_stride]; pi = softmax(teacher row)           */
+  int32_t dtype;       /* saki_dtype of both arrays                                */
+  int32_t reserved;    /* must be 0                                                */
+  int64_t n_rows;      /* number of positions, >= 0                                */
+  int64_t vocab;       /* entries per row used, 1 .. SAKI_MAX_VOCAB                */
+  int64_t row_stride;  /* elements between consecutive rows, >= vocab              */
+  int64_t row_offset;  /* global index of row 0 (keys the random draws), >= 0      */
+} saki_rows;
+
+/* Per-row outputs of the coupling (token-aligned metadata, Sec. 3.5 and App. I).
+ * Every pointer may be NULL, in which case that output is not written. Arrays
+ * have n_rows entries. */
+typedef struct {
+  float *lambda;          /* lambda*                                                   */
+  float *kl;              /* KL(q_lambda* || p)                                         */
+  float *tv;              /* TV(p, q) = sum_v [q(v) - p(v)]_+ = Pr(correction) (Prop. 1)  */
+  float *accept_prob;     /* alpha = min(1, q(z)/p(z)) at the proposal z                */
+  float *margin;          /* |u - alpha|, distance of the accept decision from a tie    */
+  float *logp_token;      /* log p(y) of the committed token y                          */
+  float *logt_token;      /* log pi_T(y)                                                 */
+  float *logq_token;      /* log q(y)                                                    */
+  int32_t *proposal;      /* z, the student proposal                                    */
+  int32_t *token;         /* y, the committed token (z if accepted, else the correction) */
+  int32_t *teacher_argmax;/* v* = argmax_v t_v, lowest index on ties                    */
+  uint8_t *corrected;     /* C: 1 if the proposal was rejected                          */
+  uint8_t *row_status;    /* SAKI_ROW_*                                                  */
+} saki_couple_out;
+
+/* Routing arguments (Eq. general_objective).  row loss
+ *   l_r = M_r * [ (1 - C_r) * (-A_r) * log p(y_r) + C_r * (-log p(v*_r)) ],
+ *   A_r = log pi_T(y_r) - log p(y_r)   (detached advantage, Eq. k1_advantage_token),
+ * gradient  g[r, j] = grad_scale * M_r * d l_r / d s[r, j]
+ *         = grad_scale * M_r * [ (1 - C_r) * (-A_r) * (1[j = y_r] - p_j) + C_r * (p_j - 1[j = v*_r]) ]. */
+typedef struct {
+  const uint8_t *valid_mask; /* M, [n_rows] (0 / non-zero); NULL = every row valid        */
+  float grad_scale;          /* the caller's 1 / N_valid over the WHOLE batch (App. H)    */
+  int32_t grad_dtype;        /* saki_dtype of grad                                        */
+  float *row_loss;           /* [n_rows] unscaled l_r, or NULL                            */
+  double *loss_sum;          /* one double: OVERWRITTEN with sum_r grad_scale * l_r, or NULL */
+  void *grad;                /* [n_rows, grad_stride] gradient, or NULL (loss only)       */
+  int64_t grad_stride;       /* elements between gradient rows, >= vocab                  */
+} saki_route_args;
+
+/* Operation codes for saki_workspace_bytes. */
+#define SAKI_OP_COUPLE 0
+#define SAKI_OP_ROUTE 1
+#define SAKI_OP_VERIFY 2
+
+/* Bytes of caller workspace that one call of `op` on n_rows rows of `vocab`
+ * entries needs (device memory, any contents, 256-byte aligned).  For
+ * SAKI_OP_VERIFY n_rows is the number of blocks times k. */
+size_t saki_workspace_bytes(int op, int64_t n_rows, int64_t vocab);
+
+/* Coupling for every row (Sec. 3.2-3.3) and, when route != NULL, the routed
+ * loss and gradient fused into the same pass (Sec. 3.4).
+ *   in     rows of student / teacher logits
+ *   eps    trust-region radius, eps >= 0 (eps = 0 gives q = p and no corrections)
+ *   seed   64-bit Philox key
+ *   out    per-row outputs (any field may be NULL); out itself may not be NULL
+ *   route  NULL for coupling only
+ *   ws     workspace of ws_bytes >= saki_workspace_bytes(SAKI_OP_COUPLE, ...) */
+saki_status saki_couple(const saki_rows *in, double eps, uint64_t seed, const saki_couple_out *out,
+                        const saki_route_args *route, void *ws, size_t ws_bytes,
+                        saki_stream_t stream);
+
+/* Routed loss and gradient from given events (Sec. 3.4), for callers that
+ * already hold the coupling results.  student: [n_rows, row_stride] logits of
+ * pi_theta (= p).  token y, corrected C, teacher_argmax v* and advantage A
+ * (= log pi_T(y) - log p(y), read only at rows with C = 0) are [n_rows] device
+ * arrays.  A token or v* outside [0, vocab) at a valid row gives that row a NaN
+ * loss and a NaN gradient row. */
+saki_status saki_route_loss(const void *student, int32_t dtype, int64_t n_rows, int64_t vocab,
+                            int64_t row_stride, const int32_t *token, const uint8_t *corrected,
+                            const int32_t *teacher_argmax, const float *advantage,
+                            const saki_route_args *route, void *ws, size_t ws_bytes,
+                            saki_stream_t stream);
+
+/* Speculative block verification (Sec. 3.5, App. F, App. I).  Rows are
+ * block-major: row b*k + j holds position j of block b, whose student draft is
+ * draft[b*k + j].  Positions are examined in order; position j is accepted iff
+ * u_j < alpha_j(draft_j) with u_j the ACCEPT uniform of its global row; the
+ * block commits the accepted prefix of length n and, if n < k, the correction
+ * drawn from [q_n - p_n]_+ at position n.  With eos_id >= 0 an accepted draft
+ * equal to eos_id at position j ends the block: n = j + 1, no correction.  A
+ * position with bad data (non-finite logits, draft outside the vocabulary) ends
+ * the block before it with no correction.
+ *   accepted_len [n_blocks]  n
+ *   correction   [n_blocks]  the correction token, or -1
+ *   per_pos      optional per-position outputs ([n_rows], fields may be NULL):
+ *                positions after the end of the committed prefix get NaN / -1
+ *                and row_status SAKI_ROW_SKIPPED; proposal = the draft, token =
+ *                the committed token. */
+saki_status saki_spec_verify(const saki_rows *in, int32_t k, const int32_t *draft, double eps,
+                             uint64_t seed, int32_t eos_id, int32_t *accepted_len,
+                             int32_t *correction, const saki_couple_out *per_pos, void *ws,
+                             size_t ws_bytes, saki_stream_t stream);
+
+/* Static description of a status code. */
+const char *saki_status_str(saki_status s);
+
+/* Detail of the last non-OK status returned on the calling thread ("" if none). */
+const char *saki_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SAKI_H */

@@ -1,0 +1,255 @@
+"""ctypes binding of libsaki.so (include/saki.h).
+
+Argument marshalling only: every step of the path runs in the HIP library.
+Tensors are torch device tensors; the library sees their data pointers and the
+current torch stream.  If the built library is missing the binding raises; it
+has no fallback.
+"""
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsaki.so")
+
+SAKI_F32, SAKI_BF16 = 0, 1
+SAKI_OP_COUPLE, SAKI_OP_ROUTE, SAKI_OP_VERIFY = 0, 1, 2
+SAKI_MAX_VOCAB = 1 << 21
+SAKI_CHUNK = 1024
+ROW_OK, ROW_NONFINITE, ROW_BAD_DRAFT, ROW_SKIPPED = 0, 1, 2, 3
+
+STATUS = {0: "SAKI_OK", 1: "SAKI_E_NULLPTR", 2: "SAKI_E_SHAPE", 3: "SAKI_E_VALUE",
+          4: "SAKI_E_DTYPE", 5: "SAKI_E_ALIGN", 6: "SAKI_E_WORKSPACE", 7: "SAKI_E_DEVICE",
+          8: "SAKI_E_LAUNCH"}
+
+EXPORTED = ["saki_workspace_bytes", "saki_couple", "saki_route_loss", "saki_spec_verify",
+            "saki_status_str", "saki_last_error"]
+
+
+class SakiRows(ctypes.Structure):
+    _fields_ = [("student", ctypes.c_void_p), ("teacher", ctypes.c_void_p),
+                ("dtype", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("n_rows", ctypes.c_int64), ("vocab", ctypes.c_int64),
+                ("row_stride", ctypes.c_int64), ("row_offset", ctypes.c_int64)]
+
+
+COUPLE_FLOAT_FIELDS = ["lambda", "kl", "tv", "accept_prob", "margin", "logp_token",
+                       "logt_token", "logq_token"]
+COUPLE_INT_FIELDS = ["proposal", "token", "teacher_argmax"]
+COUPLE_U8_FIELDS = ["corrected", "row_status"]
+COUPLE_FIELDS = COUPLE_FLOAT_FIELDS + COUPLE_INT_FIELDS + COUPLE_U8_FIELDS
+
+
+class SakiCoupleOut(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in COUPLE_FIELDS]
+
+
+class SakiRouteArgs(ctypes.Structure):
+    _fields_ = [("valid_mask", ctypes.c_void_p), ("grad_scale", ctypes.c_float),
+                ("grad_dtype", ctypes.c_int32), ("row_loss", ctypes.c_void_p),
+                ("loss_sum", ctypes.c_void_p), ("grad", ctypes.c_void_p),
+                ("grad_stride", ctypes.c_int64)]
+
+
+class SakiError(RuntimeError):
+    def __init__(self, status, detail):
+        super().__init__(f"{STATUS.get(status, status)}: {detail}")
+        self.status = status
+
+
+_lib = None
+
+
+def load(path=LIB_PATH):
+    """Load libsaki.so once and declare its C signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"libsaki.so not built at {path}; run __graft_entry__.build()")
+    lib = ctypes.CDLL(path)
+    lib.saki_workspace_bytes.restype = ctypes.c_size_t
+    lib.saki_workspace_bytes.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_int64]
+    lib.saki_couple.restype = ctypes.c_int
+    lib.saki_couple.argtypes = [ctypes.POINTER(SakiRows), ctypes.c_double, ctypes.c_uint64,
+                                ctypes.POINTER(SakiCoupleOut), ctypes.POINTER(SakiRouteArgs),
+                                ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    lib.saki_route_loss.restype = ctypes.c_int
+    lib.saki_route_loss.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64,
+                                    ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                    ctypes.c_void_p, ctypes.c_void_p,
+                                    ctypes.POINTER(SakiRouteArgs), ctypes.c_void_p,
+                                    ctypes.c_size_t, ctypes.c_void_p]
+    lib.saki_spec_verify.restype = ctypes.c_int
+    lib.saki_spec_verify.argtypes = [ctypes.POINTER(SakiRows), ctypes.c_int32, ctypes.c_void_p,
+                                     ctypes.c_double, ctypes.c_uint64, ctypes.c_int32,
+                                     ctypes.c_void_p, ctypes.c_void_p,
+                                     ctypes.POINTER(SakiCoupleOut), ctypes.c_void_p,
+                                     ctypes.c_size_t, ctypes.c_void_p]
+    lib.saki_status_str.restype = ctypes.c_char_p
+    lib.saki_status_str.argtypes = [ctypes.c_int]
+    lib.saki_last_error.restype = ctypes.c_char_p
+    lib.saki_last_error.argtypes = []
+    _lib = lib
+    return lib
+
+
+def _check(status):
+    if status != 0:
+        raise SakiError(status, _lib.saki_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dtype_code(dt):
+    if dt == torch.float32:
+        return SAKI_F32
+    if dt == torch.bfloat16:
+        return SAKI_BF16
+    raise ValueError(f"unsupported dtype {dt}")
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _rows(student, teacher, row_offset):
+    assert student.dim() == 2 and student.shape == teacher.shape
+    assert student.dtype == teacher.dtype and student.stride() == teacher.stride()
+    assert student.stride(1) == 1
+    return SakiRows(_ptr(student), _ptr(teacher), _dtype_code(student.dtype), 0,
+                    student.shape[0], student.shape[1], student.stride(0), row_offset)
+
+
+def workspace_bytes(op, n_rows, vocab):
+    load()
+    return int(_lib.saki_workspace_bytes(op, n_rows, vocab))
+
+
+def alloc_couple_out(n_rows, device, fields=COUPLE_FIELDS):
+    out = {}
+    for f in fields:
+        if f in COUPLE_FLOAT_FIELDS:
+            out[f] = torch.empty(n_rows, dtype=torch.float32, device=device)
+        elif f in COUPLE_INT_FIELDS:
+            out[f] = torch.empty(n_rows, dtype=torch.int32, device=device)
+        else:
+            out[f] = torch.empty(n_rows, dtype=torch.uint8, device=device)
+    return out
+
+
+def _couple_struct(out):
+    return SakiCoupleOut(*[_ptr(out.get(f)) for f in COUPLE_FIELDS])
+
+
+def _route_struct(valid_mask, grad_scale, row_loss, loss_sum, grad):
+    gdt = _dtype_code(grad.dtype) if grad is not None else SAKI_F32
+    gstride = grad.stride(0) if grad is not None else 0
+    return SakiRouteArgs(_ptr(valid_mask), float(grad_scale), gdt, _ptr(row_loss),
+                         _ptr(loss_sum), _ptr(grad), gstride)
+
+
+def saki_couple(student, teacher, eps, seed, row_offset=0, out=None, route=None,
+                workspace=None, stream=None):
+    """Call saki_couple on preallocated buffers.
+
+    out:   dict field -> tensor (missing fields are not written)
+    route: None, or dict with optional keys valid_mask, grad_scale, row_loss,
+           loss_sum (float64 tensor of 1), grad (2-D float32/bfloat16 tensor).
+    """
+    load()
+    rows = _rows(student, teacher, row_offset)
+    co = _couple_struct(out or {})
+    rt = None
+    if route is not None:
+        rt = _route_struct(route.get("valid_mask"), route.get("grad_scale", 1.0),
+                           route.get("row_loss"), route.get("loss_sum"), route.get("grad"))
+    ws_b = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = _lib.saki_couple(ctypes.byref(rows), float(eps), int(seed) & (2**64 - 1),
+                          ctypes.byref(co), ctypes.byref(rt) if rt is not None else None,
+                          _ptr(workspace), ws_b, _stream(stream))
+    _check(st)
+
+
+def saki_route_loss(student, token, corrected, teacher_argmax, advantage, valid_mask=None,
+                    grad_scale=1.0, row_loss=None, loss_sum=None, grad=None, workspace=None,
+                    stream=None):
+    load()
+    rt = _route_struct(valid_mask, grad_scale, row_loss, loss_sum, grad)
+    ws_b = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = _lib.saki_route_loss(_ptr(student), _dtype_code(student.dtype), student.shape[0],
+                              student.shape[1], student.stride(0), _ptr(token), _ptr(corrected),
+                              _ptr(teacher_argmax), _ptr(advantage), ctypes.byref(rt),
+                              _ptr(workspace), ws_b, _stream(stream))
+    _check(st)
+
+
+def saki_spec_verify(student, teacher, k, draft, eps, seed, row_offset=0, eos_id=-1,
+                     accepted_len=None, correction=None, per_pos=None, workspace=None,
+                     stream=None):
+    load()
+    rows = _rows(student, teacher, row_offset)
+    pp = _couple_struct(per_pos) if per_pos is not None else None
+    ws_b = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = _lib.saki_spec_verify(ctypes.byref(rows), int(k), _ptr(draft), float(eps),
+                               int(seed) & (2**64 - 1), int(eos_id), _ptr(accepted_len),
+                               _ptr(correction), ctypes.byref(pp) if pp is not None else None,
+                               _ptr(workspace), ws_b, _stream(stream))
+    _check(st)
+
+
+# ---------------------------------------------------------------------------
+# Convenience wrappers that allocate their outputs (tests, examples).
+# ---------------------------------------------------------------------------
+def couple(student, teacher, eps, seed, row_offset=0, route=False, grad_dtype=None,
+           valid_mask=None, grad_scale=1.0, stream=None):
+    n, V = student.shape
+    dev = student.device
+    out = alloc_couple_out(n, dev)
+    rargs = None
+    ws = None
+    if route:
+        rargs = dict(valid_mask=valid_mask, grad_scale=grad_scale,
+                     row_loss=torch.empty(n, dtype=torch.float32, device=dev),
+                     loss_sum=torch.empty(1, dtype=torch.float64, device=dev))
+        if grad_dtype is not None:
+            rargs["grad"] = torch.empty(n, V, dtype=grad_dtype, device=dev)
+        nb = workspace_bytes(SAKI_OP_COUPLE, n, V)
+        ws = torch.empty(max(nb, 8), dtype=torch.uint8, device=dev)
+    saki_couple(student, teacher, eps, seed, row_offset, out, rargs, ws, stream)
+    if rargs is not None:
+        out.update({k: v for k, v in rargs.items() if k in ("row_loss", "loss_sum", "grad")})
+    return out
+
+
+def route_loss(student, token, corrected, teacher_argmax, advantage, valid_mask=None,
+               grad_scale=1.0, grad_dtype=torch.float32, stream=None):
+    n, V = student.shape
+    dev = student.device
+    row_loss = torch.empty(n, dtype=torch.float32, device=dev)
+    loss_sum = torch.empty(1, dtype=torch.float64, device=dev)
+    grad = torch.empty(n, V, dtype=grad_dtype, device=dev) if grad_dtype is not None else None
+    ws = torch.empty(max(workspace_bytes(SAKI_OP_ROUTE, n, V), 8), dtype=torch.uint8, device=dev)
+    saki_route_loss(student, token, corrected, teacher_argmax, advantage, valid_mask, grad_scale,
+                    row_loss, loss_sum, grad, ws, stream)
+    return dict(row_loss=row_loss, loss_sum=loss_sum, grad=grad)
+
+
+def spec_verify(student, teacher, k, draft, eps, seed, row_offset=0, eos_id=-1, per_pos=True,
+                stream=None):
+    n, V = student.shape
+    dev = student.device
+    nb = n // k
+    acc = torch.empty(nb, dtype=torch.int32, device=dev)
+    corr = torch.empty(nb, dtype=torch.int32, device=dev)
+    pp = alloc_couple_out(n, dev) if per_pos else None
+    saki_spec_verify(student, teacher, k, draft, eps, seed, row_offset, eos_id, acc, corr, pp,
+                     None, stream)
+    out = dict(accepted_len=acc, correction=corr)
+    if pp is not None:
+        out["per_pos"] = pp
+    return out

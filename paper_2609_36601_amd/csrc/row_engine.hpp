@@ -1,0 +1,563 @@
+// Per-row passes of the SAKI coupling path.  One workgroup of NT threads owns
+// one row at a time; chunk c of the row (1024 entries) belongs to wave c % NW.
+//
+//  stats sweep   : max / log-sum-exp of s and t, teacher argmax, p-moments of
+//                  d = t - s, min/max of d, per-chunk proposal masses.
+//  lambda sweeps : sums over the row at one or two candidate lambdas, giving
+//                  A(lambda) = log sum_v p_v exp(lambda x_v) (x = d - c), its
+//                  first two derivatives, KL(q_lambda || p) = lambda A' - A and
+//                  KL' = lambda A''.  A safeguarded Newton iteration on
+//                  log KL(lambda) = log eps picks the next candidate.
+//  final sweep   : TV(p, q) = sum_v p_v [q_v/p_v - 1]_+, residual chunk
+//                  masses, and (optionally) the gradient row.
+// (SAKI Sec. 3.2 Eq. bridge / Eq. trust_region; Sec. 3.3; Sec. 3.4; App. E.)
+#pragma once
+
+#include "device_util.hpp"
+
+namespace saki {
+
+template <int NT>
+struct RowShared {
+  static constexpr int NW = NT / WAVE;
+  float chunk_a[MAX_CHUNKS];  // proposal: chunk max of s | residual: chunk mass
+  float chunk_b[MAX_CHUNKS];  // proposal: chunk sum of exp(s - chunk max)
+  double red_d[NW][8];
+  float red_f[NW][4];
+  int red_i[NW][4];
+};
+
+// Row-uniform results of the stats sweep.
+struct RowStats {
+  float ms, mt;        // max s, max t
+  double lse_s, lse_t; // log-sum-exp of s and t
+  double sum_s;        // sum exp(s - ms)
+  float c;             // centring constant: E_p[d] rounded to float
+  double var;          // Var_p[d] (starting point of the lambda search)
+  float dmin, dmax;    // range of d = t - s
+  float tmax;          // max t
+  int vstar;           // argmax t, lowest index on ties
+  bool finite;
+};
+
+// Result of one lambda evaluation.
+struct LamEval {
+  float lam;
+  double A, Eq, Var, KL, KLp;
+};
+
+template <int NT>
+struct Block {
+  static constexpr int NW = NT / WAVE;
+  int tid, lane, wave;
+  RowShared<NT>& sh;
+  __device__ Block(RowShared<NT>& s) : sh(s) {
+    tid = threadIdx.x;
+    lane = tid & (WAVE - 1);
+    wave = tid / WAVE;
+  }
+
+  // Sums N doubles over the block; every thread gets the same bits.
+  template <int N>
+  __device__ void sum(double (&v)[N]) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = wave_sum(v[i]);
+    if (lane == 0) {
+#pragma unroll
+      for (int i = 0; i < N; ++i) sh.red_d[wave][i] = v[i];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      double acc = 0.0;
+      for (int w = 0; w < NW; ++w) acc += sh.red_d[w][i];
+      v[i] = acc;
+    }
+    __syncthreads();
+  }
+
+  __device__ float max(float v) {
+    v = wave_max(v);
+    if (lane == 0) sh.red_f[wave][0] = v;
+    __syncthreads();
+    float m = -finf();
+    for (int w = 0; w < NW; ++w) m = fmaxf(m, sh.red_f[w][0]);
+    __syncthreads();
+    return m;
+  }
+
+  __device__ float min(float v) { return -max(-v); }
+
+  template <typename K>
+  __device__ void argmin(K& key, int& idx) {
+    wave_argmin(key, idx);
+    if (lane == 0) {
+      sh.red_d[wave][0] = static_cast<double>(key);
+      sh.red_i[wave][0] = idx;
+    }
+    __syncthreads();
+    double bk = sh.red_d[0][0];
+    int bi = sh.red_i[0][0];
+    for (int w = 1; w < NW; ++w) {
+      const double k2 = sh.red_d[w][0];
+      const int i2 = sh.red_i[w][0];
+      if (k2 < bk || (k2 == bk && i2 < bi)) { bk = k2; bi = i2; }
+    }
+    __syncthreads();
+    key = static_cast<K>(bk);
+    idx = bi;
+  }
+
+  __device__ void argmax(float& val, int& idx) {
+    wave_argmax(val, idx);
+    if (lane == 0) {
+      sh.red_f[wave][0] = val;
+      sh.red_i[wave][0] = idx;
+    }
+    __syncthreads();
+    float bv = sh.red_f[0][0];
+    int bi = sh.red_i[0][0];
+    for (int w = 1; w < NW; ++w) {
+      const float v2 = sh.red_f[w][0];
+      const int i2 = sh.red_i[w][0];
+      if (v2 > bv || (v2 == bv && i2 < bi)) { bv = v2; bi = i2; }
+    }
+    __syncthreads();
+    val = bv;
+    idx = bi;
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Stats sweep.
+// ---------------------------------------------------------------------------
+template <typename T, int NT, bool TAIL>
+__device__ __forceinline__ void stats_chunk(const T* srow, const T* trow, int V, int c, int lane,
+                                            bool keep_chunks, RowShared<NT>& sh, float& Ms,
+                                            float& Mt, double& Ss, double& S1, double& S2,
+                                            double& St, double& T1, float& tbest, int& tidx,
+                                            float& dmin, float& dmax) {
+  float s[EPL], t[EPL];
+  uint32_t vm;
+  load_lane<T, TAIL>(srow, c, lane, V, s, &vm);
+  load_lane<T, TAIL>(trow, c, lane, V, t, &vm);
+  float ls = -finf(), lt = -finf();
+#pragma unroll
+  for (int e = 0; e < EPL; ++e) {
+    if (!TAIL || ((vm >> e) & 1u)) {
+      ls = fmaxf(ls, s[e]);
+      lt = fmaxf(lt, t[e]);
+    }
+  }
+  const float cms = wave_max(ls), cmt = wave_max(lt);
+  const float ks = cms * LOG2E, kt = cmt * LOG2E;
+  float ps = 0.f, pt = 0.f, p1 = 0.f, p2 = 0.f, t1 = 0.f;
+  const int base = c * CHUNK;
+#pragma unroll
+  for (int e = 0; e < EPL; ++e) {
+    if (!TAIL || ((vm >> e) & 1u)) {
+      const float es = fexp2(fmaf(s[e], LOG2E, -ks));
+      const float et = fexp2(fmaf(t[e], LOG2E, -kt));
+      const float d = t[e] - s[e];
+      ps += es;
+      pt += et;
+      const float ed = es * d;
+      p1 += ed;
+      p2 = fmaf(ed, d, p2);
+      t1 = fmaf(et, d, t1);
+      if (t[e] > tbest) {
+        tbest = t[e];
+        tidx = base + elem_offset(lane, e);
+      }
+      dmin = fminf(dmin, d);
+      dmax = fmaxf(dmax, d);
+    }
+  }
+  if (keep_chunks) {
+    const float csum = wave_sum(ps);
+    if (lane == 0) {
+      sh.chunk_a[c] = cms;
+      sh.chunk_b[c] = csum;
+    }
+  }
+  // fold this chunk into the wave's running sums (all lanes share Ms, Mt)
+  if (cms > Ms) {
+    const float f = fexp2((Ms - cms) * LOG2E);
+    Ss *= f; S1 *= f; S2 *= f;
+    Ms = cms;
+  }
+  if (cmt > Mt) {
+    const float f = fexp2((Mt - cmt) * LOG2E);
+    St *= f; T1 *= f;
+    Mt = cmt;
+  }
+  const float gs = fexp2((cms - Ms) * LOG2E);
+  const float gt = fexp2((cmt - Mt) * LOG2E);
+  Ss += static_cast<double>(ps * gs);
+  S1 += static_cast<double>(p1 * gs);
+  S2 += static_cast<double>(p2 * gs);
+  St += static_cast<double>(pt * gt);
+  T1 += static_cast<double>(t1 * gt);
+}
+
+template <typename T, int NT>
+__device__ RowStats stats_sweep(Block<NT>& B, const T* srow, const T* trow, int V, bool keep_chunks) {
+  constexpr int NW = NT / WAVE;
+  const int nchunks = (V + CHUNK - 1) / CHUNK;
+  const bool ragged = (V % CHUNK) != 0;
+  float Ms = -finf(), Mt = -finf();
+  double Ss = 0, S1 = 0, S2 = 0, St = 0, T1 = 0;
+  float tbest = -finf();
+  int tidx = 0x7fffffff;
+  float dmin = finf(), dmax = -finf();
+  for (int c = B.wave; c < nchunks; c += NW) {
+    if (ragged && c == nchunks - 1)
+      stats_chunk<T, NT, true>(srow, trow, V, c, B.lane, keep_chunks, B.sh, Ms, Mt, Ss, S1, S2, St,
+                               T1, tbest, tidx, dmin, dmax);
+    else
+      stats_chunk<T, NT, false>(srow, trow, V, c, B.lane, keep_chunks, B.sh, Ms, Mt, Ss, S1, S2,
+                                St, T1, tbest, tidx, dmin, dmax);
+  }
+  RowStats R;
+  R.ms = B.max(Ms);
+  R.mt = B.max(Mt);
+  // rescale each wave's sums to the row maxima, then add in a fixed order
+  const float gs = (Ms == -finf()) ? 0.f : fexp2((Ms - R.ms) * LOG2E);
+  const float gt = (Mt == -finf()) ? 0.f : fexp2((Mt - R.mt) * LOG2E);
+  double v[5] = {Ss * gs, S1 * gs, S2 * gs, St * gt, T1 * gt};
+  B.sum(v);
+  B.argmax(tbest, tidx);
+  R.dmin = B.min(dmin);
+  R.dmax = B.max(dmax);
+  R.tmax = tbest;
+  R.vstar = tidx;
+  R.sum_s = v[0];
+  R.lse_s = static_cast<double>(R.ms) + log(v[0]);
+  R.lse_t = static_cast<double>(R.mt) + log(v[3]);
+  const double Ed = v[1] / v[0];
+  R.var = fmax(v[2] / v[0] - Ed * Ed, 0.0);
+  R.c = static_cast<float>(Ed);
+  R.finite = isfinite(R.lse_s) && isfinite(R.lse_t) && isfinite(Ed) && isfinite(v[2]) &&
+             isfinite(v[4]) && isfinite(R.dmin) && isfinite(R.dmax) && isfinite(R.ms) &&
+             isfinite(R.mt);
+  return R;
+}
+
+// ---------------------------------------------------------------------------
+// Lambda sweep: sums at NC candidate lambdas.  For candidate j the weights are
+// w_v = p~_v * exp(lam_j x_v - sig_j), p~_v = exp(s_v - ms), x_v = d_v - c.
+// With sig_j = 0 the sum of (w - p~) is kept instead of the sum of w, so that
+// A(lam) = log1p(sum(w - p~) / sum p~) keeps its relative precision when lam
+// is small.  sig_j > 0 only when lam_j * (dmax - c) could overflow float.
+// ---------------------------------------------------------------------------
+template <typename T, int NT, int NC, bool TAIL>
+__device__ __forceinline__ void lam_chunk(const T* srow, const T* trow, int V, int c, int lane,
+                                          float ksl, float cf, const float* lam, const float* sigl,
+                                          double& B0, double (&W)[NC], double (&S1)[NC],
+                                          double (&S2)[NC]) {
+  float s[EPL], t[EPL];
+  uint32_t vm;
+  load_lane<T, TAIL>(srow, c, lane, V, s, &vm);
+  load_lane<T, TAIL>(trow, c, lane, V, t, &vm);
+  float b0 = 0.f, w0[NC], s1[NC], s2[NC];
+#pragma unroll
+  for (int j = 0; j < NC; ++j) { w0[j] = 0.f; s1[j] = 0.f; s2[j] = 0.f; }
+#pragma unroll
+  for (int e = 0; e < EPL; ++e) {
+    if (!TAIL || ((vm >> e) & 1u)) {
+      const float a = fmaf(s[e], LOG2E, -ksl);
+      const float pt = fexp2(a);
+      const float x = (t[e] - s[e]) - cf;
+      const float xl = x * LOG2E;
+      b0 += pt;
+#pragma unroll
+      for (int j = 0; j < NC; ++j) {
+        const float w = fexp2(fmaf(lam[j], xl, a) - sigl[j]);
+        w0[j] += (sigl[j] == 0.f) ? (w - pt) : w;
+        const float wx = w * x;
+        s1[j] += wx;
+        s2[j] = fmaf(wx, x, s2[j]);
+      }
+    }
+  }
+  B0 += static_cast<double>(b0);
+#pragma unroll
+  for (int j = 0; j < NC; ++j) {
+    W[j] += static_cast<double>(w0[j]);
+    S1[j] += static_cast<double>(s1[j]);
+    S2[j] += static_cast<double>(s2[j]);
+  }
+}
+
+template <typename T, int NT, int NC>
+__device__ void lam_sweep(Block<NT>& B, const T* srow, const T* trow, int V, const RowStats& R,
+                          const float (&lam)[NC], LamEval (&out)[NC]) {
+  constexpr int NW = NT / WAVE;
+  const int nchunks = (V + CHUNK - 1) / CHUNK;
+  const bool ragged = (V % CHUNK) != 0;
+  // overflow guard: keep lam * x - sig <= 60 (natural units) for every entry;
+  // sigl is the shift in log2 units
+  float sigl[NC];
+#pragma unroll
+  for (int j = 0; j < NC; ++j) {
+    const double top = static_cast<double>(lam[j]) * (static_cast<double>(R.dmax) - R.c);
+    sigl[j] = top > 60.0 ? static_cast<float>((top - 60.0) * static_cast<double>(LOG2E)) : 0.0f;
+  }
+  const float ksl = R.ms * LOG2E;
+  double B0 = 0, W[NC], S1[NC], S2[NC];
+#pragma unroll
+  for (int j = 0; j < NC; ++j) { W[j] = 0; S1[j] = 0; S2[j] = 0; }
+  for (int c = B.wave; c < nchunks; c += NW) {
+    if (ragged && c == nchunks - 1)
+      lam_chunk<T, NT, NC, true>(srow, trow, V, c, B.lane, ksl, R.c, lam, sigl, B0, W, S1, S2);
+    else
+      lam_chunk<T, NT, NC, false>(srow, trow, V, c, B.lane, ksl, R.c, lam, sigl, B0, W, S1, S2);
+  }
+  double v[1 + 3 * NC];
+  v[0] = B0;
+#pragma unroll
+  for (int j = 0; j < NC; ++j) { v[1 + 3 * j] = W[j]; v[2 + 3 * j] = S1[j]; v[3 + 3 * j] = S2[j]; }
+  B.sum(v);
+#pragma unroll
+  for (int j = 0; j < NC; ++j) {
+    const double b0 = v[0], w = v[1 + 3 * j], s1 = v[2 + 3 * j], s2 = v[3 + 3 * j];
+    // sigl is in log2 units: the shift in natural units is sigl * ln 2
+    const double sh = static_cast<double>(sigl[j]) * LN2_D;
+    LamEval& E = out[j];
+    E.lam = lam[j];
+    double S0;
+    if (sigl[j] == 0.f) {
+      S0 = b0 + w;
+      E.A = log1p(w / b0);
+    } else {
+      S0 = w;
+      E.A = sh + log(w / b0);
+    }
+    E.Eq = s1 / S0;
+    E.Var = fmax(s2 / S0 - E.Eq * E.Eq, 0.0);
+    const double l = static_cast<double>(lam[j]);
+    E.KL = l * E.Eq - E.A;
+    E.KLp = l * E.Var;
+  }
+}
+
+// Result of the lambda search.
+struct LamResult {
+  float lam;   // lambda*
+  double A;    // A(lambda*) = log sum_v p_v exp(lambda* x_v), x = d - c
+  double KL;   // KL(q_lambda* || p)
+  float c;     // centring constant used by A (may differ from RowStats::c)
+};
+
+// Largest lambda in [0, 1] with KL(q_lambda || p) <= eps (Eq. trust_region).
+template <typename T, int NT>
+__device__ LamResult lambda_search(Block<NT>& B, const T* srow, const T* trow, int V,
+                                   const RowStats& R0, double eps) {
+  LamResult out;
+  RowStats R = R0;
+  if (R.dmin == R.dmax) {
+    // t - s constant: p = pi, KL = 0 for every lambda, lambda* = 1, q = p
+    out.lam = 1.0f; out.A = 0.0; out.KL = 0.0; out.c = R.dmin;
+    return out;
+  }
+  out.c = R.c;
+  if (eps == 0.0) {
+    out.lam = 0.0f; out.A = 0.0; out.KL = 0.0;
+    return out;
+  }
+  // first sweep: the teacher endpoint and a small-lambda start,
+  // KL(lam) ~ lam^2 Var_p(d) / 2  =>  lam0 = sqrt(2 eps / Var)
+  double l0 = R.var > 0 ? sqrt(2.0 * eps / R.var) : 0.5;
+  l0 = fmin(fmax(l0, 1e-6), 0.999);
+  LamEval E2[2];
+  {
+    const float cand[2] = {static_cast<float>(l0), 1.0f};
+    lam_sweep<T, NT, 2>(B, srow, trow, V, R, cand, E2);
+  }
+  if (E2[1].KL <= eps) {
+    out.lam = 1.0f; out.A = E2[1].A; out.KL = E2[1].KL;
+    return out;
+  }
+  double lo = 0.0, hi = 1.0;
+  LamEval cur = E2[0];
+  const double leps = log(eps);
+  for (int it = 0; it < 24; ++it) {
+    const double l = cur.lam;
+    if (cur.KL <= eps) lo = fmax(lo, l); else hi = fmin(hi, l);
+    double nl;
+    bool newton_ok = cur.KL > 0 && cur.KLp > 0 && isfinite(cur.KL);
+    double step = 0;
+    if (newton_ok) {
+      // Newton on log KL(lam) - log eps
+      step = -(log(cur.KL) - leps) * cur.KL / cur.KLp;
+      nl = l + step;
+      if (!(nl > lo && nl < hi)) newton_ok = false;
+    }
+    if (!newton_ok) nl = (lo > 0) ? sqrt(lo * hi) : 0.25 * hi;
+    const float nlf = static_cast<float>(nl);
+    if (newton_ok && (fabs(step) <= 2e-8 * l || nlf == cur.lam)) {
+      // converged: extrapolate A and KL from the last evaluation to lambda*
+      const double dl = static_cast<double>(nlf) - l;
+      out.lam = nlf;
+      out.A = cur.A + cur.Eq * dl + 0.5 * cur.Var * dl * dl;
+      out.KL = cur.KL + cur.KLp * dl;
+      return out;
+    }
+    LamEval E1[1];
+    const float cand[1] = {nlf};
+    lam_sweep<T, NT, 1>(B, srow, trow, V, R, cand, E1);
+    cur = E1[0];
+  }
+  out.lam = cur.lam; out.A = cur.A; out.KL = cur.KL;
+  return out;
+}
+
+// ---------------------------------------------------------------------------
+// Final sweep at lambda*: TV, residual chunk masses, gradient row.
+//   p_v = p~_v / sum_s,  q_v / p_v = exp(lam* x_v - A*),
+//   w_v = p_v [q_v/p_v - 1]_+ ;  grad_v = coef * (p_v - 1[v = hot]).
+// ---------------------------------------------------------------------------
+// Residual weight [q_v - p_v]_+ and p_v of one entry; the residual race uses
+// the same function so that its weights are bit-identical to the chunk masses.
+__device__ __forceinline__ float res_weight(float s, float t, float ksl, float invS, float cf,
+                                            float laml, float Al, float* p_out) {
+  const float p = fexp2(fmaf(s, LOG2E, -ksl)) * invS;
+  const float x = (t - s) - cf;
+  const float r = fexp2(fmaf(laml, x, -Al));
+  *p_out = p;
+  return p * fmaxf(r - 1.0f, 0.0f);
+}
+
+template <typename T, typename G, int NT, bool TAIL, bool GRAD>
+__device__ __forceinline__ void final_chunk(const T* srow, const T* trow, G* grow, int V, int c,
+                                            int lane, float ksl, float invS, float cf, float laml,
+                                            float Al, bool keep_res, float coef, int hot,
+                                            RowShared<NT>& sh, double& TV) {
+  float s[EPL], t[EPL];
+  uint32_t vm;
+  load_lane<T, TAIL>(srow, c, lane, V, s, &vm);
+  load_lane<T, TAIL>(trow, c, lane, V, t, &vm);
+  float tv = 0.f;
+  float g[EPL];
+  const int base = c * CHUNK;
+#pragma unroll
+  for (int e = 0; e < EPL; ++e) {
+    float p;
+    const float w = res_weight(s[e], t[e], ksl, invS, cf, laml, Al, &p);
+    if (!TAIL || ((vm >> e) & 1u)) tv += w;
+    if (GRAD) g[e] = coef * (p - ((base + elem_offset(lane, e) == hot) ? 1.0f : 0.0f));
+  }
+  if (keep_res) {
+    const float m = wave_sum(tv);
+    if (lane == 0) sh.chunk_a[c] = m;
+  }
+  TV += static_cast<double>(tv);
+  if (GRAD) store_lane<G, TAIL>(grow, c, lane, V, g);
+}
+
+template <typename T, typename G, int NT, bool GRAD>
+__device__ double final_sweep(Block<NT>& B, const T* srow, const T* trow, G* grow, int V,
+                              const RowStats& R, const LamResult& L, bool keep_res, float coef,
+                              int hot) {
+  constexpr int NW = NT / WAVE;
+  const int nchunks = (V + CHUNK - 1) / CHUNK;
+  const bool ragged = (V % CHUNK) != 0;
+  const float ksl = R.ms * LOG2E;
+  const float invS = static_cast<float>(1.0 / R.sum_s);
+  const float laml = L.lam * LOG2E;
+  const float Al = static_cast<float>(L.A * static_cast<double>(LOG2E));
+  double TV = 0;
+  for (int c = B.wave; c < nchunks; c += NW) {
+    if (ragged && c == nchunks - 1)
+      final_chunk<T, G, NT, true, GRAD>(srow, trow, grow, V, c, B.lane, ksl, invS, L.c, laml, Al,
+                                        keep_res, coef, hot, B.sh, TV);
+    else
+      final_chunk<T, G, NT, false, GRAD>(srow, trow, grow, V, c, B.lane, ksl, invS, L.c, laml, Al,
+                                         keep_res, coef, hot, B.sh, TV);
+  }
+  double v[1] = {TV};
+  B.sum(v);
+  return v[0];
+}
+
+// Gradient-only sweep for rows that carry no coupling (non-finite rows, or
+// the standalone routed loss): grad_v = coef * (p_v - 1[v = hot]).
+template <typename T, typename G, int NT, bool TAIL>
+__device__ __forceinline__ void grad_chunk(const T* srow, G* grow, int V, int c, int lane, float ksl,
+                                           float invS, float coef, int hot, bool nan_row) {
+  float s[EPL];
+  uint32_t vm;
+  load_lane<T, TAIL>(srow, c, lane, V, s, &vm);
+  float g[EPL];
+  const int base = c * CHUNK;
+#pragma unroll
+  for (int e = 0; e < EPL; ++e) {
+    const float p = fexp2(fmaf(s[e], LOG2E, -ksl)) * invS;
+    g[e] = nan_row ? __builtin_nanf("") : coef * (p - ((base + elem_offset(lane, e) == hot) ? 1.0f : 0.0f));
+  }
+  store_lane<G, TAIL>(grow, c, lane, V, g);
+}
+
+template <typename T, typename G, int NT>
+__device__ void grad_sweep(Block<NT>& B, const T* srow, G* grow, int V, float ms, double sum_s,
+                           float coef, int hot, bool nan_row) {
+  constexpr int NW = NT / WAVE;
+  const int nchunks = (V + CHUNK - 1) / CHUNK;
+  const bool ragged = (V % CHUNK) != 0;
+  const float ksl = ms * LOG2E;
+  const float invS = static_cast<float>(1.0 / sum_s);
+  for (int c = B.wave; c < nchunks; c += NW) {
+    if (ragged && c == nchunks - 1)
+      grad_chunk<T, G, NT, true>(srow, grow, V, c, B.lane, ksl, invS, coef, hot, nan_row);
+    else
+      grad_chunk<T, G, NT, false>(srow, grow, V, c, B.lane, ksl, invS, coef, hot, nan_row);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Two-level exponential races (the sampler this library fixes for z ~ p and
+// c ~ [q - p]_+): the chunk with the smallest E_c / W_c wins, then the entry
+// of that chunk with the smallest E_v / w_v; ties to the lowest index.  Keys
+// are compared as ln E - ln w.
+// ---------------------------------------------------------------------------
+
+// Chunk level.  logw(c) returns ln W_c up to a row constant, or -inf.
+template <int NT, typename F>
+__device__ int chunk_race(Block<NT>& B, int nchunks, uint64_t seed, uint32_t stream, uint64_t g,
+                          F logw) {
+  double best = __builtin_huge_val();
+  int bi = 0x7fffffff;
+  for (int c = B.tid; c < nchunks; c += NT) {
+    const double lw = logw(c);
+    if (lw > -__builtin_huge_val()) {
+      const double u = static_cast<double>(philox_uniform(seed, stream, g, static_cast<uint32_t>(c)));
+      const double key = log(-log(u)) - lw;
+      if (key < best) { best = key; bi = c; }
+    }
+  }
+  B.argmin(best, bi);
+  return bi;
+}
+
+// Entry level inside chunk c.  logw(v) returns ln w_v up to a row constant, or -inf.
+template <int NT, typename F>
+__device__ int elem_race(Block<NT>& B, int c, int V, uint64_t seed, uint32_t stream, uint64_t g,
+                         F logw) {
+  float best = finf();
+  int bi = 0x7fffffff;
+  const int lo = c * CHUNK;
+  const int hi = min(V, lo + CHUNK);
+  for (int v = lo + B.tid; v < hi; v += NT) {
+    const float lw = logw(v);
+    if (lw > -finf()) {
+      const float u = philox_uniform(seed, stream, g, static_cast<uint32_t>(v));
+      const float E = -flog2(u) * LN2;
+      const float key = flog2(E) * LN2 - lw;
+      if (key < best) { best = key; bi = v; }
+    }
+  }
+  B.argmin(best, bi);
+  return bi;
+}
+
+}  // namespace saki

@@ -1,0 +1,710 @@
+// SAKI coupling-and-routing kernels for gfx950 and the C ABI of include/saki.h.
+//
+// One workgroup of NT = 512 threads (8 waves) owns one row at a time and
+// walks the grid's rows persistently; the row engine (row_engine.hpp) runs the
+// stats sweep, the lambda sweeps and the final sweep over that row.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+#include <stdio.h>
+
+#include <mutex>
+#include <string>
+
+#include "../../include/saki.h"
+#include "row_engine.hpp"
+
+namespace saki {
+
+constexpr int NT = 512;
+constexpr int WG_PER_CU = 1;
+
+struct CoupleParams {
+  const void* s;
+  const void* t;
+  int64_t n_rows;
+  int64_t stride;
+  int64_t row_offset;
+  int V;
+  double eps;
+  uint64_t seed;
+  saki_couple_out out;
+  // routing
+  const uint8_t* valid;
+  float grad_scale;
+  float* row_loss;
+  double* scaled_loss;  // workspace [n_rows] or NULL
+  void* grad;
+  int64_t grad_stride;
+};
+
+__device__ __forceinline__ float nanf_() { return __builtin_nanf(""); }
+
+template <typename T, typename G, bool ROUTE, bool GRAD>
+__global__ __launch_bounds__(NT) void couple_kernel(CoupleParams P) {
+  __shared__ RowShared<NT> sh;
+  Block<NT> B(sh);
+  const int V = P.V;
+  const int nch = (V + CHUNK - 1) / CHUNK;
+  for (int64_t r = blockIdx.x; r < P.n_rows; r += gridDim.x) {
+    const T* srow = static_cast<const T*>(P.s) + r * P.stride;
+    const T* trow = static_cast<const T*>(P.t) + r * P.stride;
+    G* grow = GRAD ? static_cast<G*>(P.grad) + r * P.grad_stride : nullptr;
+    const uint64_t g = static_cast<uint64_t>(P.row_offset + r);
+    const float M = (ROUTE && P.valid) ? (P.valid[r] ? 1.0f : 0.0f) : 1.0f;
+
+    const RowStats R = stats_sweep<T, NT>(B, srow, trow, V, true);
+    if (!R.finite) {
+      if (GRAD) grad_sweep<T, G, NT>(B, srow, grow, V, 0.0f, 1.0, 0.0f, -1, M != 0.0f);
+      if (B.tid == 0) {
+        const saki_couple_out& o = P.out;
+        if (o.lambda) o.lambda[r] = nanf_();
+        if (o.kl) o.kl[r] = nanf_();
+        if (o.tv) o.tv[r] = nanf_();
+        if (o.accept_prob) o.accept_prob[r] = nanf_();
+        if (o.margin) o.margin[r] = nanf_();
+        if (o.logp_token) o.logp_token[r] = nanf_();
+        if (o.logt_token) o.logt_token[r] = nanf_();
+        if (o.logq_token) o.logq_token[r] = nanf_();
+        if (o.proposal) o.proposal[r] = -1;
+        if (o.token) o.token[r] = -1;
+        if (o.teacher_argmax) o.teacher_argmax[r] = -1;
+        if (o.corrected) o.corrected[r] = 0;
+        if (o.row_status) o.row_status[r] = SAKI_ROW_NONFINITE;
+        if (ROUTE) {
+          const float l = (M != 0.0f) ? nanf_() : 0.0f;
+          if (P.row_loss) P.row_loss[r] = l;
+          if (P.scaled_loss) P.scaled_loss[r] = static_cast<double>(l);
+        }
+      }
+      continue;
+    }
+
+    // z ~ p by the two-level race (chunk masses from the stats sweep)
+    const int c0 = chunk_race<NT>(B, nch, P.seed, PROP_CHUNK, g, [&](int c) {
+      return static_cast<double>(sh.chunk_a[c]) + log(static_cast<double>(sh.chunk_b[c]));
+    });
+    int z = elem_race<NT>(B, c0 < nch ? c0 : 0, V, P.seed, PROP_ELEM, g,
+                          [&](int v) { return Loader<T>::load1(srow + v); });
+    if (z >= V) z = R.vstar;  // unreachable for finite rows: every chunk has a winner
+
+    const LamResult L = lambda_search<T, NT>(B, srow, trow, V, R, P.eps);
+
+    // accept test, Eq. accept in the log form exp(min(0, log q(z) - log p(z)))
+    const float sz = Loader<T>::load1(srow + z), tz = Loader<T>::load1(trow + z);
+    const double xz = (static_cast<double>(tz) - static_cast<double>(sz)) - static_cast<double>(L.c);
+    const double alpha = exp(fmin(0.0, static_cast<double>(L.lam) * xz - L.A));
+    const double u = static_cast<double>(philox_uniform(P.seed, ACCEPT, g, 0));
+    const bool C = !(u < alpha);
+
+    const double logp_z = static_cast<double>(sz) - R.lse_s;
+    const double logt_z = static_cast<double>(tz) - R.lse_t;
+    const double adv = logt_z - logp_z;
+    const float coef = ROUTE ? static_cast<float>(static_cast<double>(P.grad_scale) * M * (C ? 1.0 : adv)) : 0.0f;
+    const int hot = C ? R.vstar : z;
+
+    const double TV = final_sweep<T, G, NT, GRAD>(B, srow, trow, grow, V, R, L, C, coef, hot);
+
+    int y = z;
+    if (C) {
+      const int c1 = chunk_race<NT>(B, nch, P.seed, RES_CHUNK, g, [&](int c) {
+        const float m = sh.chunk_a[c];
+        return m > 0.0f ? log(static_cast<double>(m)) : -__builtin_huge_val();
+      });
+      const float ksl = R.ms * LOG2E;
+      const float invS = static_cast<float>(1.0 / R.sum_s);
+      const float laml = L.lam * LOG2E;
+      const float Al = static_cast<float>(L.A * static_cast<double>(LOG2E));
+      // a residual that rounds to zero everywhere in float (lambda* x within
+      // rounding of A*) leaves no chunk with mass; the proposal is kept then
+      if (c1 < nch) {
+        const int yc = elem_race<NT>(B, c1, V, P.seed, RES_ELEM, g, [&](int v) {
+          float p;
+          const float w = res_weight(Loader<T>::load1(srow + v), Loader<T>::load1(trow + v), ksl,
+                                     invS, L.c, laml, Al, &p);
+          return w > 0.0f ? flog2(w) * LN2 : -finf();
+        });
+        if (yc < V) y = yc;
+      }
+    }
+
+    if (B.tid == 0) {
+      const float sy = Loader<T>::load1(srow + y), ty = Loader<T>::load1(trow + y);
+      const double logp_y = static_cast<double>(sy) - R.lse_s;
+      const double logt_y = static_cast<double>(ty) - R.lse_t;
+      const double xy = (static_cast<double>(ty) - static_cast<double>(sy)) - static_cast<double>(L.c);
+      const double logq_y = logp_y + static_cast<double>(L.lam) * xy - L.A;
+      const saki_couple_out& o = P.out;
+      if (o.lambda) o.lambda[r] = L.lam;
+      if (o.kl) o.kl[r] = static_cast<float>(L.KL);
+      if (o.tv) o.tv[r] = static_cast<float>(TV);
+      if (o.accept_prob) o.accept_prob[r] = static_cast<float>(alpha);
+      if (o.margin) o.margin[r] = static_cast<float>(fabs(u - alpha));
+      if (o.logp_token) o.logp_token[r] = static_cast<float>(logp_y);
+      if (o.logt_token) o.logt_token[r] = static_cast<float>(logt_y);
+      if (o.logq_token) o.logq_token[r] = static_cast<float>(logq_y);
+      if (o.proposal) o.proposal[r] = z;
+      if (o.token) o.token[r] = y;
+      if (o.teacher_argmax) o.teacher_argmax[r] = R.vstar;
+      if (o.corrected) o.corrected[r] = C ? 1 : 0;
+      if (o.row_status) o.row_status[r] = SAKI_ROW_OK;
+      if (ROUTE) {
+        double l = 0.0;
+        if (M != 0.0f) {
+          if (C) {
+            const double logp_v = static_cast<double>(Loader<T>::load1(srow + R.vstar)) - R.lse_s;
+            l = -logp_v;
+          } else {
+            l = -adv * logp_z;
+          }
+        }
+        if (P.row_loss) P.row_loss[r] = static_cast<float>(l);
+        if (P.scaled_loss) P.scaled_loss[r] = static_cast<double>(P.grad_scale) * l;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Speculative verification: one workgroup per block, positions in order.
+// ---------------------------------------------------------------------------
+struct VerifyParams {
+  const void* s;
+  const void* t;
+  int64_t n_blocks;
+  int64_t stride;
+  int64_t row_offset;
+  int V;
+  int k;
+  const int32_t* draft;
+  double eps;
+  uint64_t seed;
+  int eos;
+  int32_t* accepted_len;
+  int32_t* correction;
+  saki_couple_out pp;  // per-position outputs (fields may be NULL)
+  int has_pp;
+};
+
+__device__ void write_skipped(const saki_couple_out& o, int64_t r, int32_t draft, uint8_t status) {
+  if (o.lambda) o.lambda[r] = nanf_();
+  if (o.kl) o.kl[r] = nanf_();
+  if (o.tv) o.tv[r] = nanf_();
+  if (o.accept_prob) o.accept_prob[r] = nanf_();
+  if (o.margin) o.margin[r] = nanf_();
+  if (o.logp_token) o.logp_token[r] = nanf_();
+  if (o.logt_token) o.logt_token[r] = nanf_();
+  if (o.logq_token) o.logq_token[r] = nanf_();
+  if (o.proposal) o.proposal[r] = draft;
+  if (o.token) o.token[r] = -1;
+  if (o.teacher_argmax) o.teacher_argmax[r] = -1;
+  if (o.corrected) o.corrected[r] = 0;
+  if (o.row_status) o.row_status[r] = status;
+}
+
+template <typename T>
+__global__ __launch_bounds__(NT) void verify_kernel(VerifyParams P) {
+  __shared__ RowShared<NT> sh;
+  Block<NT> B(sh);
+  const int V = P.V;
+  const int nch = (V + CHUNK - 1) / CHUNK;
+  const saki_couple_out& o = P.pp;
+  const bool need_tv = P.has_pp && o.tv != nullptr;
+  for (int64_t b = blockIdx.x; b < P.n_blocks; b += gridDim.x) {
+    int n = P.k;
+    int corr = -1;
+    int next_unwritten = P.k;  // first position whose per-position outputs are not yet written
+    for (int j = 0; j < P.k; ++j) {
+      const int64_t r = b * P.k + j;
+      const T* srow = static_cast<const T*>(P.s) + r * P.stride;
+      const T* trow = static_cast<const T*>(P.t) + r * P.stride;
+      const uint64_t g = static_cast<uint64_t>(P.row_offset + r);
+      const int z = P.draft[r];
+      if (z < 0 || z >= V) {
+        if (P.has_pp && B.tid == 0) write_skipped(o, r, z, SAKI_ROW_BAD_DRAFT);
+        n = j;
+        next_unwritten = j + 1;
+        break;
+      }
+      const RowStats R = stats_sweep<T, NT>(B, srow, trow, V, false);
+      if (!R.finite) {
+        if (P.has_pp && B.tid == 0) write_skipped(o, r, z, SAKI_ROW_NONFINITE);
+        n = j;
+        next_unwritten = j + 1;
+        break;
+      }
+      const LamResult L = lambda_search<T, NT>(B, srow, trow, V, R, P.eps);
+      const float sz = Loader<T>::load1(srow + z), tz = Loader<T>::load1(trow + z);
+      const double xz = (static_cast<double>(tz) - static_cast<double>(sz)) - static_cast<double>(L.c);
+      const double alpha = exp(fmin(0.0, static_cast<double>(L.lam) * xz - L.A));
+      const double u = static_cast<double>(philox_uniform(P.seed, ACCEPT, g, 0));
+      const bool accept = u < alpha;
+      double TV = __builtin_nan("");
+      if (need_tv || !accept)
+        TV = final_sweep<T, float, NT, false>(B, srow, trow, nullptr, V, R, L, !accept, 0.0f, -1);
+      int y = z;
+      if (!accept) {
+        const int c1 = chunk_race<NT>(B, nch, P.seed, RES_CHUNK, g, [&](int c) {
+          const float m = sh.chunk_a[c];
+          return m > 0.0f ? log(static_cast<double>(m)) : -__builtin_huge_val();
+        });
+        const float ksl = R.ms * LOG2E;
+        const float invS = static_cast<float>(1.0 / R.sum_s);
+        const float laml = L.lam * LOG2E;
+        const float Al = static_cast<float>(L.A * static_cast<double>(LOG2E));
+        if (c1 < nch) {
+          const int yc = elem_race<NT>(B, c1, V, P.seed, RES_ELEM, g, [&](int v) {
+            float p;
+            const float w = res_weight(Loader<T>::load1(srow + v), Loader<T>::load1(trow + v), ksl,
+                                       invS, L.c, laml, Al, &p);
+            return w > 0.0f ? flog2(w) * LN2 : -finf();
+          });
+          if (yc < V) y = yc;
+        }
+      }
+      if (P.has_pp && B.tid == 0) {
+        const float sy = Loader<T>::load1(srow + y), ty = Loader<T>::load1(trow + y);
+        const double logp_y = static_cast<double>(sy) - R.lse_s;
+        const double logt_y = static_cast<double>(ty) - R.lse_t;
+        const double xy = (static_cast<double>(ty) - static_cast<double>(sy)) - static_cast<double>(L.c);
+        if (o.lambda) o.lambda[r] = L.lam;
+        if (o.kl) o.kl[r] = static_cast<float>(L.KL);
+        if (o.tv) o.tv[r] = static_cast<float>(TV);
+        if (o.accept_prob) o.accept_prob[r] = static_cast<float>(alpha);
+        if (o.margin) o.margin[r] = static_cast<float>(fabs(u - alpha));
+        if (o.logp_token) o.logp_token[r] = static_cast<float>(logp_y);
+        if (o.logt_token) o.logt_token[r] = static_cast<float>(logt_y);
+        if (o.logq_token) o.logq_token[r] = static_cast<float>(logp_y + static_cast<double>(L.lam) * xy - L.A);
+        if (o.proposal) o.proposal[r] = z;
+        if (o.token) o.token[r] = y;
+        if (o.teacher_argmax) o.teacher_argmax[r] = R.vstar;
+        if (o.corrected) o.corrected[r] = accept ? 0 : 1;
+        if (o.row_status) o.row_status[r] = SAKI_ROW_OK;
+      }
+      if (!accept) {
+        n = j;
+        corr = y;
+        next_unwritten = j + 1;
+        break;
+      }
+      if (P.eos >= 0 && z == P.eos) {
+        n = j + 1;
+        next_unwritten = j + 1;
+        break;
+      }
+    }
+    if (B.tid == 0) {
+      P.accepted_len[b] = n;
+      P.correction[b] = corr;
+      if (P.has_pp) {
+        // positions after the end of the block's committed prefix
+        for (int jj = next_unwritten; jj < P.k; ++jj) {
+          const int64_t r = b * P.k + jj;
+          write_skipped(o, r, P.draft[r], SAKI_ROW_SKIPPED);
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Standalone routed loss and gradient from given events.
+// ---------------------------------------------------------------------------
+struct RouteParams {
+  const void* s;
+  int64_t n_rows;
+  int64_t stride;
+  int V;
+  const int32_t* token;
+  const uint8_t* corrected;
+  const int32_t* vstar;
+  const float* advantage;
+  const uint8_t* valid;
+  float grad_scale;
+  float* row_loss;
+  double* scaled_loss;
+  void* grad;
+  int64_t grad_stride;
+};
+
+template <typename T, bool TAIL>
+__device__ __forceinline__ void lse_chunk(const T* srow, int V, int c, int lane, float& Ms, double& Ss) {
+  float s[EPL];
+  uint32_t vm;
+  load_lane<T, TAIL>(srow, c, lane, V, s, &vm);
+  float ls = -finf();
+#pragma unroll
+  for (int e = 0; e < EPL; ++e)
+    if (!TAIL || ((vm >> e) & 1u)) ls = fmaxf(ls, s[e]);
+  const float cms = wave_max(ls);
+  const float ks = cms * LOG2E;
+  float ps = 0.f;
+#pragma unroll
+  for (int e = 0; e < EPL; ++e)
+    if (!TAIL || ((vm >> e) & 1u)) ps += fexp2(fmaf(s[e], LOG2E, -ks));
+  if (cms > Ms) {
+    Ss *= fexp2((Ms - cms) * LOG2E);
+    Ms = cms;
+  }
+  Ss += static_cast<double>(ps * fexp2((cms - Ms) * LOG2E));
+}
+
+template <typename T, typename G, bool GRAD>
+__global__ __launch_bounds__(NT) void route_kernel(RouteParams P) {
+  __shared__ RowShared<NT> sh;
+  Block<NT> B(sh);
+  constexpr int NW = NT / WAVE;
+  const int V = P.V;
+  const int nch = (V + CHUNK - 1) / CHUNK;
+  const bool ragged = (V % CHUNK) != 0;
+  for (int64_t r = blockIdx.x; r < P.n_rows; r += gridDim.x) {
+    const T* srow = static_cast<const T*>(P.s) + r * P.stride;
+    G* grow = GRAD ? static_cast<G*>(P.grad) + r * P.grad_stride : nullptr;
+    float Ms = -finf();
+    double Ss = 0.0;
+    for (int c = B.wave; c < nch; c += NW) {
+      if (ragged && c == nch - 1) lse_chunk<T, true>(srow, V, c, B.lane, Ms, Ss);
+      else lse_chunk<T, false>(srow, V, c, B.lane, Ms, Ss);
+    }
+    const float ms = B.max(Ms);
+    double v[1] = {(Ms == -finf()) ? 0.0 : Ss * fexp2((Ms - ms) * LOG2E)};
+    B.sum(v);
+    const double lse = static_cast<double>(ms) + log(v[0]);
+    const bool M = P.valid ? (P.valid[r] != 0) : true;
+    const bool C = P.corrected[r] != 0;
+    const int hot = C ? P.vstar[r] : P.token[r];
+    const bool bad = M && (hot < 0 || hot >= V || !isfinite(lse));
+    const double A = C ? 0.0 : static_cast<double>(P.advantage[r]);
+    float coef = 0.0f;
+    if (M && !bad) coef = static_cast<float>(static_cast<double>(P.grad_scale) * (C ? 1.0 : A));
+    if (GRAD) grad_sweep<T, G, NT>(B, srow, grow, V, ms, v[0], coef, bad ? -1 : hot, bad);
+    if (B.tid == 0) {
+      double l = 0.0;
+      if (bad) {
+        l = __builtin_nan("");
+      } else if (M) {
+        const double logp_h = static_cast<double>(Loader<T>::load1(srow + hot)) - lse;
+        l = C ? -logp_h : -A * logp_h;
+      }
+      if (P.row_loss) P.row_loss[r] = static_cast<float>(l);
+      if (P.scaled_loss) P.scaled_loss[r] = static_cast<double>(P.grad_scale) * l;
+    }
+  }
+}
+
+// Deterministic sum of the scaled row losses: fixed per-thread strides, then a
+// fixed-order block tree.
+__global__ __launch_bounds__(1024) void loss_sum_kernel(const double* x, int64_t n, double* out) {
+  __shared__ double part[1024];
+  double acc = 0.0;
+  for (int64_t i = threadIdx.x; i < n; i += 1024) acc += x[i];
+  part[threadIdx.x] = acc;
+  __syncthreads();
+  for (int w = 512; w > 0; w >>= 1) {
+    if (static_cast<int>(threadIdx.x) < w) part[threadIdx.x] += part[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *out = part[0];
+}
+
+}  // namespace saki
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+namespace {
+
+thread_local std::string g_last_error;
+
+saki_status fail(saki_status st, const std::string& msg) {
+  g_last_error = msg;
+  return st;
+}
+
+saki_status ok() {
+  g_last_error.clear();
+  return SAKI_OK;
+}
+
+int elem_size(int32_t dt) { return dt == SAKI_BF16 ? 2 : 4; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+saki_status device_cus(int* cus) {
+  static std::mutex mu;
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return fail(SAKI_E_DEVICE, "hipGetDevice failed");
+  std::lock_guard<std::mutex> lock(mu);
+  if (dev < 64 && cache[dev] > 0) {
+    *cus = cache[dev];
+    return SAKI_OK;
+  }
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+    return fail(SAKI_E_DEVICE, "hipDeviceGetAttribute(MultiprocessorCount) failed");
+  if (dev < 64) cache[dev] = n;
+  *cus = n;
+  return SAKI_OK;
+}
+
+saki_status check_rows(const saki_rows* in) {
+  if (!in) return fail(SAKI_E_NULLPTR, "rows descriptor is NULL");
+  if (in->dtype != SAKI_F32 && in->dtype != SAKI_BF16) return fail(SAKI_E_DTYPE, "unknown logits dtype");
+  if (in->reserved != 0) return fail(SAKI_E_VALUE, "saki_rows.reserved must be 0");
+  if (in->n_rows < 0) return fail(SAKI_E_SHAPE, "n_rows < 0");
+  if (in->vocab < 1 || in->vocab > SAKI_MAX_VOCAB) return fail(SAKI_E_SHAPE, "vocab outside [1, SAKI_MAX_VOCAB]");
+  if (in->row_stride < in->vocab) return fail(SAKI_E_SHAPE, "row_stride < vocab");
+  if (in->row_offset < 0) return fail(SAKI_E_VALUE, "row_offset < 0");
+  if (in->n_rows == 0) return SAKI_OK;
+  if (!in->student || !in->teacher) return fail(SAKI_E_NULLPTR, "student or teacher pointer is NULL");
+  if (!aligned16(in->student) || !aligned16(in->teacher) ||
+      (in->row_stride * elem_size(in->dtype)) % 16 != 0)
+    return fail(SAKI_E_ALIGN, "logit base pointers and row pitch must be 16-byte aligned");
+  return SAKI_OK;
+}
+
+saki_status check_route(const saki_route_args* rt, int64_t vocab, bool* want_loss_sum) {
+  *want_loss_sum = false;
+  if (!rt) return SAKI_OK;
+  if (!isfinite(rt->grad_scale)) return fail(SAKI_E_VALUE, "grad_scale is not finite");
+  if (rt->grad) {
+    if (rt->grad_dtype != SAKI_F32 && rt->grad_dtype != SAKI_BF16) return fail(SAKI_E_DTYPE, "unknown grad dtype");
+    if (rt->grad_stride < vocab) return fail(SAKI_E_SHAPE, "grad_stride < vocab");
+    if (!aligned16(rt->grad) || (rt->grad_stride * elem_size(rt->grad_dtype)) % 16 != 0)
+      return fail(SAKI_E_ALIGN, "grad base pointer and row pitch must be 16-byte aligned");
+  }
+  *want_loss_sum = rt->loss_sum != nullptr;
+  return SAKI_OK;
+}
+
+size_t loss_ws_bytes(int64_t n_rows) {
+  const size_t b = static_cast<size_t>(n_rows) * sizeof(double);
+  return (b + 255) & ~static_cast<size_t>(255);
+}
+
+saki_status launched(const char* what) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(SAKI_E_LAUNCH, std::string(what) + ": " + hipGetErrorString(e));
+  return SAKI_OK;
+}
+
+template <typename T, typename G, bool ROUTE, bool GRAD>
+saki_status launch_couple(const saki::CoupleParams& P, int grid, hipStream_t st) {
+  hipLaunchKernelGGL((saki::couple_kernel<T, G, ROUTE, GRAD>), dim3(grid), dim3(saki::NT), 0, st, P);
+  return launched("couple_kernel");
+}
+
+template <typename T>
+saki_status dispatch_couple(const saki::CoupleParams& P, bool route, bool grad, int32_t gdt, int grid,
+                            hipStream_t st) {
+  if (!route) return launch_couple<T, float, false, false>(P, grid, st);
+  if (!grad) return launch_couple<T, float, true, false>(P, grid, st);
+  if (gdt == SAKI_BF16) return launch_couple<T, uint16_t, true, true>(P, grid, st);
+  return launch_couple<T, float, true, true>(P, grid, st);
+}
+
+template <typename T, typename G, bool GRAD>
+saki_status launch_route(const saki::RouteParams& P, int grid, hipStream_t st) {
+  hipLaunchKernelGGL((saki::route_kernel<T, G, GRAD>), dim3(grid), dim3(saki::NT), 0, st, P);
+  return launched("route_kernel");
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t saki_workspace_bytes(int op, int64_t n_rows, int64_t vocab) {
+  (void)vocab;
+  if (n_rows <= 0) return 0;
+  switch (op) {
+    case SAKI_OP_COUPLE:
+    case SAKI_OP_ROUTE:
+      return loss_ws_bytes(n_rows);
+    case SAKI_OP_VERIFY:
+      return 0;
+    default:
+      return 0;
+  }
+}
+
+saki_status saki_couple(const saki_rows* in, double eps, uint64_t seed, const saki_couple_out* out,
+                        const saki_route_args* route, void* ws, size_t ws_bytes, saki_stream_t stream) {
+  saki_status st = check_rows(in);
+  if (st != SAKI_OK) return st;
+  if (!out) return fail(SAKI_E_NULLPTR, "out is NULL");
+  if (!(eps >= 0.0) || !isfinite(eps)) return fail(SAKI_E_VALUE, "eps must be finite and >= 0");
+  bool want_sum = false;
+  st = check_route(route, in->vocab, &want_sum);
+  if (st != SAKI_OK) return st;
+  if (want_sum) {
+    if (!ws) return fail(SAKI_E_WORKSPACE, "workspace is NULL but loss_sum is requested");
+    if (ws_bytes < loss_ws_bytes(in->n_rows)) return fail(SAKI_E_WORKSPACE, "workspace too small");
+    if ((reinterpret_cast<uintptr_t>(ws) & 7u) != 0) return fail(SAKI_E_ALIGN, "workspace must be 8-byte aligned");
+  }
+  if (in->n_rows == 0) return ok();
+  int cus = 0;
+  st = device_cus(&cus);
+  if (st != SAKI_OK) return st;
+  saki::CoupleParams P{};
+  P.s = in->student;
+  P.t = in->teacher;
+  P.n_rows = in->n_rows;
+  P.stride = in->row_stride;
+  P.row_offset = in->row_offset;
+  P.V = static_cast<int>(in->vocab);
+  P.eps = eps;
+  P.seed = seed;
+  P.out = *out;
+  if (route) {
+    P.valid = route->valid_mask;
+    P.grad_scale = route->grad_scale;
+    P.row_loss = route->row_loss;
+    P.scaled_loss = want_sum ? static_cast<double*>(ws) : nullptr;
+    P.grad = route->grad;
+    P.grad_stride = route->grad_stride;
+  }
+  const int grid = static_cast<int>(std::min<int64_t>(in->n_rows, static_cast<int64_t>(cus) * saki::WG_PER_CU));
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  const bool grad = route && route->grad;
+  st = (in->dtype == SAKI_BF16)
+           ? dispatch_couple<uint16_t>(P, route != nullptr, grad, route ? route->grad_dtype : 0, grid, hs)
+           : dispatch_couple<float>(P, route != nullptr, grad, route ? route->grad_dtype : 0, grid, hs);
+  if (st != SAKI_OK) return st;
+  if (want_sum) {
+    hipLaunchKernelGGL(saki::loss_sum_kernel, dim3(1), dim3(1024), 0, hs,
+                       static_cast<const double*>(ws), in->n_rows, route->loss_sum);
+    st = launched("loss_sum_kernel");
+    if (st != SAKI_OK) return st;
+  }
+  return ok();
+}
+
+saki_status saki_route_loss(const void* student, int32_t dtype, int64_t n_rows, int64_t vocab,
+                            int64_t row_stride, const int32_t* token, const uint8_t* corrected,
+                            const int32_t* teacher_argmax, const float* advantage,
+                            const saki_route_args* route, void* ws, size_t ws_bytes,
+                            saki_stream_t stream) {
+  if (dtype != SAKI_F32 && dtype != SAKI_BF16) return fail(SAKI_E_DTYPE, "unknown logits dtype");
+  if (n_rows < 0) return fail(SAKI_E_SHAPE, "n_rows < 0");
+  if (vocab < 1 || vocab > SAKI_MAX_VOCAB) return fail(SAKI_E_SHAPE, "vocab outside [1, SAKI_MAX_VOCAB]");
+  if (row_stride < vocab) return fail(SAKI_E_SHAPE, "row_stride < vocab");
+  if (!route) return fail(SAKI_E_NULLPTR, "route is NULL");
+  bool want_sum = false;
+  saki_status st = check_route(route, vocab, &want_sum);
+  if (st != SAKI_OK) return st;
+  if (want_sum) {
+    if (!ws) return fail(SAKI_E_WORKSPACE, "workspace is NULL but loss_sum is requested");
+    if (ws_bytes < loss_ws_bytes(n_rows)) return fail(SAKI_E_WORKSPACE, "workspace too small");
+    if ((reinterpret_cast<uintptr_t>(ws) & 7u) != 0) return fail(SAKI_E_ALIGN, "workspace must be 8-byte aligned");
+  }
+  if (n_rows == 0) return ok();
+  if (!student || !token || !corrected || !teacher_argmax || !advantage)
+    return fail(SAKI_E_NULLPTR, "student, token, corrected, teacher_argmax and advantage are required");
+  if (!aligned16(student) || (row_stride * elem_size(dtype)) % 16 != 0)
+    return fail(SAKI_E_ALIGN, "student base pointer and row pitch must be 16-byte aligned");
+  int cus = 0;
+  st = device_cus(&cus);
+  if (st != SAKI_OK) return st;
+  saki::RouteParams P{};
+  P.s = student;
+  P.n_rows = n_rows;
+  P.stride = row_stride;
+  P.V = static_cast<int>(vocab);
+  P.token = token;
+  P.corrected = corrected;
+  P.vstar = teacher_argmax;
+  P.advantage = advantage;
+  P.valid = route->valid_mask;
+  P.grad_scale = route->grad_scale;
+  P.row_loss = route->row_loss;
+  P.scaled_loss = want_sum ? static_cast<double*>(ws) : nullptr;
+  P.grad = route->grad;
+  P.grad_stride = route->grad_stride;
+  const int grid = static_cast<int>(std::min<int64_t>(n_rows, static_cast<int64_t>(cus) * saki::WG_PER_CU));
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  const bool grad = route->grad != nullptr;
+  const bool gbf = route->grad_dtype == SAKI_BF16;
+  if (dtype == SAKI_BF16) {
+    st = !grad ? launch_route<uint16_t, float, false>(P, grid, hs)
+         : gbf ? launch_route<uint16_t, uint16_t, true>(P, grid, hs)
+               : launch_route<uint16_t, float, true>(P, grid, hs);
+  } else {
+    st = !grad ? launch_route<float, float, false>(P, grid, hs)
+         : gbf ? launch_route<float, uint16_t, true>(P, grid, hs)
+               : launch_route<float, float, true>(P, grid, hs);
+  }
+  if (st != SAKI_OK) return st;
+  if (want_sum) {
+    hipLaunchKernelGGL(saki::loss_sum_kernel, dim3(1), dim3(1024), 0, hs,
+                       static_cast<const double*>(ws), n_rows, route->loss_sum);
+    st = launched("loss_sum_kernel");
+    if (st != SAKI_OK) return st;
+  }
+  return ok();
+}
+
+saki_status saki_spec_verify(const saki_rows* in, int32_t k, const int32_t* draft, double eps,
+                             uint64_t seed, int32_t eos_id, int32_t* accepted_len,
+                             int32_t* correction, const saki_couple_out* per_pos, void* ws,
+                             size_t ws_bytes, saki_stream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  saki_status st = check_rows(in);
+  if (st != SAKI_OK) return st;
+  if (k < 1 || k > SAKI_MAX_BLOCK_K) return fail(SAKI_E_SHAPE, "k outside [1, SAKI_MAX_BLOCK_K]");
+  if (in->n_rows % k != 0) return fail(SAKI_E_SHAPE, "n_rows is not a multiple of k");
+  if (!(eps >= 0.0) || !isfinite(eps)) return fail(SAKI_E_VALUE, "eps must be finite and >= 0");
+  if (in->n_rows == 0) return ok();
+  if (!draft || !accepted_len || !correction)
+    return fail(SAKI_E_NULLPTR, "draft, accepted_len and correction are required");
+  int cus = 0;
+  st = device_cus(&cus);
+  if (st != SAKI_OK) return st;
+  saki::VerifyParams P{};
+  P.s = in->student;
+  P.t = in->teacher;
+  P.n_blocks = in->n_rows / k;
+  P.stride = in->row_stride;
+  P.row_offset = in->row_offset;
+  P.V = static_cast<int>(in->vocab);
+  P.k = k;
+  P.draft = draft;
+  P.eps = eps;
+  P.seed = seed;
+  P.eos = eos_id;
+  P.accepted_len = accepted_len;
+  P.correction = correction;
+  if (per_pos) {
+    P.pp = *per_pos;
+    P.has_pp = 1;
+  }
+  const int grid = static_cast<int>(std::min<int64_t>(P.n_blocks, static_cast<int64_t>(cus) * saki::WG_PER_CU));
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (in->dtype == SAKI_BF16)
+    hipLaunchKernelGGL(saki::verify_kernel<uint16_t>, dim3(grid), dim3(saki::NT), 0, hs, P);
+  else
+    hipLaunchKernelGGL(saki::verify_kernel<float>, dim3(grid), dim3(saki::NT), 0, hs, P);
+  st = launched("verify_kernel");
+  if (st != SAKI_OK) return st;
+  return ok();
+}
+
+const char* saki_status_str(saki_status s) {
+  switch (s) {
+    case SAKI_OK: return "ok";
+    case SAKI_E_NULLPTR: return "a required pointer is NULL";
+    case SAKI_E_SHAPE: return "invalid shape";
+    case SAKI_E_VALUE: return "invalid value";
+    case SAKI_E_DTYPE: return "unknown dtype";
+    case SAKI_E_ALIGN: return "pointer or pitch not 16-byte aligned";
+    case SAKI_E_WORKSPACE: return "workspace missing or too small";
+    case SAKI_E_DEVICE: return "HIP device error";
+    case SAKI_E_LAUNCH: return "kernel launch failed";
+  }
+  return "unknown status";
+}
+
+const char* saki_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,104 @@
+"""Host-side checks of the C ABI: the library loads, exports every symbol the
+header declares, and rejects bad arguments before touching a device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_36601_amd as saki
+from paper_2609_36601_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "saki.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2609_36601_amd import build
+        build.build()
+    return saki.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:[\w\s\*]+?)\b(saki_\w+)\s*\(", text, re.M)))
+
+
+def test_header_and_exports_agree(lib):
+    names = declared_functions()
+    assert set(names) == set(binding.EXPORTED)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    for code in range(9):
+        assert lib.saki_status_str(code)
+    assert lib.saki_last_error() is not None
+
+
+def _rows(**kw):
+    r = dict(student=16, teacher=32, dtype=binding.SAKI_BF16, reserved=0, n_rows=4, vocab=64,
+             row_stride=64, row_offset=0)
+    r.update(kw)
+    return binding.SakiRows(**r)
+
+
+def _couple(lib, rows, eps=0.1, out=True, route=None, ws=None, ws_bytes=0):
+    co = binding.SakiCoupleOut()
+    return lib.saki_couple(ctypes.byref(rows) if rows is not None else None, eps, 1,
+                           ctypes.byref(co) if out else None,
+                           ctypes.byref(route) if route is not None else None,
+                           ws, ws_bytes, None)
+
+
+def test_argument_errors_without_launch(lib):
+    assert _couple(lib, None) == 1                                   # NULL rows
+    assert _couple(lib, _rows(), out=False) == 1                     # NULL out
+    assert _couple(lib, _rows(vocab=0)) == 2                         # vocab < 1
+    assert _couple(lib, _rows(vocab=(1 << 21) + 1, row_stride=(1 << 21) + 8)) == 2
+    assert _couple(lib, _rows(row_stride=32)) == 2                   # stride < vocab
+    assert _couple(lib, _rows(n_rows=-1)) == 2
+    assert _couple(lib, _rows(), eps=-0.1) == 3
+    assert _couple(lib, _rows(), eps=float("nan")) == 3
+    assert _couple(lib, _rows(row_offset=-5)) == 3
+    assert _couple(lib, _rows(dtype=7)) == 4
+    assert _couple(lib, _rows(student=17)) == 5                      # misaligned base
+    assert _couple(lib, _rows(row_stride=68)) == 5                   # pitch 136 B
+    assert _couple(lib, _rows(student=0)) == 1
+    rt = binding.SakiRouteArgs(None, 1.0, 0, None, 64, None, 0)     # loss_sum, no workspace
+    assert _couple(lib, _rows(), route=rt) == 6
+    assert _couple(lib, _rows(), route=rt, ws=256, ws_bytes=8) == 6  # too small
+    rt = binding.SakiRouteArgs(None, float("inf"), 0, None, None, None, 0)
+    assert _couple(lib, _rows(), route=rt) == 3
+    rt = binding.SakiRouteArgs(None, 1.0, 0, None, None, 48, 32)    # grad stride < vocab
+    assert _couple(lib, _rows(), route=rt) == 2
+    assert b"vocab" in lib.saki_last_error() or lib.saki_last_error()
+
+
+def test_zero_rows_returns_ok_without_device(lib):
+    assert _couple(lib, _rows(n_rows=0, student=0, teacher=0)) == 0
+    assert lib.saki_last_error() == b""
+
+
+def test_verify_and_route_argument_errors(lib):
+    rows = _rows(n_rows=6)
+    acc = ctypes.c_void_p(64)
+    bad_k = lib.saki_spec_verify(ctypes.byref(rows), 0, 64, 0.1, 1, -1, acc, acc, None, None, 0, None)
+    assert bad_k == 2
+    not_multiple = lib.saki_spec_verify(ctypes.byref(rows), 4, 64, 0.1, 1, -1, acc, acc, None, None, 0, None)
+    assert not_multiple == 2
+    no_draft = lib.saki_spec_verify(ctypes.byref(rows), 3, None, 0.1, 1, -1, acc, acc, None, None, 0, None)
+    assert no_draft == 1
+    rt = binding.SakiRouteArgs(None, 1.0, 0, None, None, None, 0)
+    assert lib.saki_route_loss(16, 9, 4, 64, 64, 64, 64, 64, 64, ctypes.byref(rt), None, 0, None) == 4
+    assert lib.saki_route_loss(16, 1, 4, 64, 64, None, 64, 64, 64, ctypes.byref(rt), None, 0, None) == 1
+    assert lib.saki_route_loss(16, 1, 4, 64, 64, 64, 64, 64, 64, None, None, 0, None) == 1
+
+
+def test_workspace_sizes(lib):
+    assert saki.workspace_bytes(saki.SAKI_OP_COUPLE, 0, 10) == 0
+    assert saki.workspace_bytes(saki.SAKI_OP_COUPLE, 1000, 10) >= 8000
+    assert saki.workspace_bytes(saki.SAKI_OP_ROUTE, 33, 10) % 256 == 0
