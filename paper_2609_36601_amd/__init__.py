@@ -5,5 +5,5 @@ include/saki.h); this package is its thin Python binding.
 """
 from .binding import (  # noqa: F401
     COUPLE_FIELDS, EXPORTED, SAKI_BF16, SAKI_CHUNK, SAKI_F32, SAKI_MAX_VOCAB, SAKI_OP_COUPLE,
-    SAKI_OP_ROUTE, SAKI_OP_VERIFY, SakiError, alloc_couple_out, couple, load, route_loss,
+    SAKI_OP_ROUTE, SAKI_OP_VERIFY, SakiError, alloc_couple_out, alloc_rows, couple, load, route_loss,
     saki_couple, saki_route_loss, saki_spec_verify, spec_verify, workspace_bytes)

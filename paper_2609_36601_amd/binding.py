@@ -130,6 +130,13 @@ def workspace_bytes(op, n_rows, vocab):
     return int(_lib.saki_workspace_bytes(op, n_rows, vocab))
 
 
+def alloc_rows(n_rows, vocab, dtype, device):
+    """[n_rows, vocab] tensor whose row pitch is a multiple of 16 bytes (the ABI's layout rule)."""
+    per = 16 // torch.tensor([], dtype=dtype).element_size()
+    pitch = (vocab + per - 1) // per * per
+    return torch.empty(n_rows, pitch, dtype=dtype, device=device)[:, :vocab]
+
+
 def alloc_couple_out(n_rows, device, fields=COUPLE_FIELDS):
     out = {}
     for f in fields:
@@ -217,7 +224,7 @@ def couple(student, teacher, eps, seed, row_offset=0, route=False, grad_dtype=No
                      row_loss=torch.empty(n, dtype=torch.float32, device=dev),
                      loss_sum=torch.empty(1, dtype=torch.float64, device=dev))
         if grad_dtype is not None:
-            rargs["grad"] = torch.empty(n, V, dtype=grad_dtype, device=dev)
+            rargs["grad"] = alloc_rows(n, V, grad_dtype, dev)
         nb = workspace_bytes(SAKI_OP_COUPLE, n, V)
         ws = torch.empty(max(nb, 8), dtype=torch.uint8, device=dev)
     saki_couple(student, teacher, eps, seed, row_offset, out, rargs, ws, stream)
@@ -232,7 +239,7 @@ def route_loss(student, token, corrected, teacher_argmax, advantage, valid_mask=
     dev = student.device
     row_loss = torch.empty(n, dtype=torch.float32, device=dev)
     loss_sum = torch.empty(1, dtype=torch.float64, device=dev)
-    grad = torch.empty(n, V, dtype=grad_dtype, device=dev) if grad_dtype is not None else None
+    grad = alloc_rows(n, V, grad_dtype, dev) if grad_dtype is not None else None
     ws = torch.empty(max(workspace_bytes(SAKI_OP_ROUTE, n, V), 8), dtype=torch.uint8, device=dev)
     saki_route_loss(student, token, corrected, teacher_argmax, advantage, valid_mask, grad_scale,
                     row_loss, loss_sum, grad, ws, stream)

@@ -135,7 +135,7 @@ template <typename T, int NT, bool TAIL>
 __device__ __forceinline__ void stats_chunk(const T* srow, const T* trow, int V, int c, int lane,
                                             bool keep_chunks, RowShared<NT>& sh, float& Ms,
                                             float& Mt, double& Ss, double& S1, double& S2,
-                                            double& St, double& T1, float& tbest, int& tidx,
+                                            double& St, float& tbest, int& tidx,
                                             float& dmin, float& dmax) {
   float s[EPL], t[EPL];
   uint32_t vm;
@@ -150,21 +150,24 @@ __device__ __forceinline__ void stats_chunk(const T* srow, const T* trow, int V,
     }
   }
   const float cms = wave_max(ls), cmt = wave_max(lt);
-  const float ks = cms * LOG2E, kt = cmt * LOG2E;
-  float ps = 0.f, pt = 0.f, p1 = 0.f, p2 = 0.f, t1 = 0.f;
+  // exponent arguments as (x - max) * log2(e): the subtraction is exact, so
+  // the largest terms carry no rounding from the shift
+  double ps = 0.0, pt = 0.0;
+  float p1 = 0.f, p2 = 0.f;
   const int base = c * CHUNK;
 #pragma unroll
   for (int e = 0; e < EPL; ++e) {
     if (!TAIL || ((vm >> e) & 1u)) {
-      const float es = fexp2(fmaf(s[e], LOG2E, -ks));
-      const float et = fexp2(fmaf(t[e], LOG2E, -kt));
+      const float es = fexp2((s[e] - cms) * LOG2E);
+      const float et = fexp2((t[e] - cmt) * LOG2E);
       const float d = t[e] - s[e];
-      ps += es;
-      pt += et;
+      // the normalisers are summed in double per entry: next to an entry of
+      // weight ~1 a float partial sum would lose the small remaining mass
+      ps += static_cast<double>(es);
+      pt += static_cast<double>(et);
       const float ed = es * d;
       p1 += ed;
       p2 = fmaf(ed, d, p2);
-      t1 = fmaf(et, d, t1);
       if (t[e] > tbest) {
         tbest = t[e];
         tidx = base + elem_offset(lane, e);
@@ -174,7 +177,7 @@ __device__ __forceinline__ void stats_chunk(const T* srow, const T* trow, int V,
     }
   }
   if (keep_chunks) {
-    const float csum = wave_sum(ps);
+    const float csum = static_cast<float>(wave_sum(ps));
     if (lane == 0) {
       sh.chunk_a[c] = cms;
       sh.chunk_b[c] = csum;
@@ -182,22 +185,22 @@ __device__ __forceinline__ void stats_chunk(const T* srow, const T* trow, int V,
   }
   // fold this chunk into the wave's running sums (all lanes share Ms, Mt)
   if (cms > Ms) {
-    const float f = fexp2((Ms - cms) * LOG2E);
+    const double f = static_cast<double>(fexp2((Ms - cms) * LOG2E));
     Ss *= f; S1 *= f; S2 *= f;
     Ms = cms;
   }
   if (cmt > Mt) {
-    const float f = fexp2((Mt - cmt) * LOG2E);
-    St *= f; T1 *= f;
+    St *= static_cast<double>(fexp2((Mt - cmt) * LOG2E));
     Mt = cmt;
   }
-  const float gs = fexp2((cms - Ms) * LOG2E);
-  const float gt = fexp2((cmt - Mt) * LOG2E);
-  Ss += static_cast<double>(ps * gs);
-  S1 += static_cast<double>(p1 * gs);
-  S2 += static_cast<double>(p2 * gs);
-  St += static_cast<double>(pt * gt);
-  T1 += static_cast<double>(t1 * gt);
+  // chunks below the running maximum are rescaled; the chunk holding the
+  // maximum is added unscaled (factor exactly 1)
+  const double gs = (cms == Ms) ? 1.0 : static_cast<double>(fexp2((cms - Ms) * LOG2E));
+  const double gt = (cmt == Mt) ? 1.0 : static_cast<double>(fexp2((cmt - Mt) * LOG2E));
+  Ss += ps * gs;
+  S1 += static_cast<double>(p1) * gs;
+  S2 += static_cast<double>(p2) * gs;
+  St += pt * gt;
 }
 
 template <typename T, int NT>
@@ -206,25 +209,25 @@ __device__ RowStats stats_sweep(Block<NT>& B, const T* srow, const T* trow, int 
   const int nchunks = (V + CHUNK - 1) / CHUNK;
   const bool ragged = (V % CHUNK) != 0;
   float Ms = -finf(), Mt = -finf();
-  double Ss = 0, S1 = 0, S2 = 0, St = 0, T1 = 0;
+  double Ss = 0, S1 = 0, S2 = 0, St = 0;
   float tbest = -finf();
   int tidx = 0x7fffffff;
   float dmin = finf(), dmax = -finf();
   for (int c = B.wave; c < nchunks; c += NW) {
     if (ragged && c == nchunks - 1)
       stats_chunk<T, NT, true>(srow, trow, V, c, B.lane, keep_chunks, B.sh, Ms, Mt, Ss, S1, S2, St,
-                               T1, tbest, tidx, dmin, dmax);
+                               tbest, tidx, dmin, dmax);
     else
       stats_chunk<T, NT, false>(srow, trow, V, c, B.lane, keep_chunks, B.sh, Ms, Mt, Ss, S1, S2,
-                                St, T1, tbest, tidx, dmin, dmax);
+                                St, tbest, tidx, dmin, dmax);
   }
   RowStats R;
   R.ms = B.max(Ms);
   R.mt = B.max(Mt);
   // rescale each wave's sums to the row maxima, then add in a fixed order
-  const float gs = (Ms == -finf()) ? 0.f : fexp2((Ms - R.ms) * LOG2E);
-  const float gt = (Mt == -finf()) ? 0.f : fexp2((Mt - R.mt) * LOG2E);
-  double v[5] = {Ss * gs, S1 * gs, S2 * gs, St * gt, T1 * gt};
+  const double gs = (Ms == -finf()) ? 0.0 : (Ms == R.ms) ? 1.0 : static_cast<double>(fexp2((Ms - R.ms) * LOG2E));
+  const double gt = (Mt == -finf()) ? 0.0 : (Mt == R.mt) ? 1.0 : static_cast<double>(fexp2((Mt - R.mt) * LOG2E));
+  double v[4] = {Ss * gs, S1 * gs, S2 * gs, St * gt};
   B.sum(v);
   B.argmax(tbest, tidx);
   R.dmin = B.min(dmin);
@@ -238,7 +241,7 @@ __device__ RowStats stats_sweep(Block<NT>& B, const T* srow, const T* trow, int 
   R.var = fmax(v[2] / v[0] - Ed * Ed, 0.0);
   R.c = static_cast<float>(Ed);
   R.finite = isfinite(R.lse_s) && isfinite(R.lse_t) && isfinite(Ed) && isfinite(v[2]) &&
-             isfinite(v[4]) && isfinite(R.dmin) && isfinite(R.dmax) && isfinite(R.ms) &&
+             isfinite(R.dmin) && isfinite(R.dmax) && isfinite(R.ms) &&
              isfinite(R.mt);
   return R;
 }
@@ -250,9 +253,15 @@ __device__ RowStats stats_sweep(Block<NT>& B, const T* srow, const T* trow, int 
 // A(lam) = log1p(sum(w - p~) / sum p~) keeps its relative precision when lam
 // is small.  sig_j > 0 only when lam_j * (dmax - c) could overflow float.
 // ---------------------------------------------------------------------------
-template <typename T, int NT, int NC, bool TAIL>
+// exp(y) - 1 for |y| < 1/16 to ~1e-7 relative: the Taylor polynomial through
+// y^4 / 24 (the next term is below y^5 / 120).
+__device__ __forceinline__ float expm1_small(float y) {
+  return y * fmaf(y, fmaf(y, fmaf(y, 1.0f / 24.0f, 1.0f / 6.0f), 0.5f), 1.0f);
+}
+
+template <typename T, int NT, int NC, bool TAIL, bool ACC>
 __device__ __forceinline__ void lam_chunk(const T* srow, const T* trow, int V, int c, int lane,
-                                          float ksl, float cf, const float* lam, const float* sigl,
+                                          float ms, float cf, const float* lam, const float* sigl,
                                           double& B0, double (&W)[NC], double (&S1)[NC],
                                           double (&S2)[NC]) {
   float s[EPL], t[EPL];
@@ -265,18 +274,31 @@ __device__ __forceinline__ void lam_chunk(const T* srow, const T* trow, int V, i
 #pragma unroll
   for (int e = 0; e < EPL; ++e) {
     if (!TAIL || ((vm >> e) & 1u)) {
-      const float a = fmaf(s[e], LOG2E, -ksl);
+      const float a = (s[e] - ms) * LOG2E;
       const float pt = fexp2(a);
       const float x = (t[e] - s[e]) - cf;
       const float xl = x * LOG2E;
       b0 += pt;
 #pragma unroll
       for (int j = 0; j < NC; ++j) {
-        const float w = fexp2(fmaf(lam[j], xl, a) - sigl[j]);
-        w0[j] += (sigl[j] == 0.f) ? (w - pt) : w;
-        const float wx = w * x;
-        s1[j] += wx;
-        s2[j] = fmaf(wx, x, s2[j]);
+        if (ACC) {
+          // w - p~ = p~ * expm1(lam x), with expm1 accurate for small |lam x|
+          // (used when the KL being resolved is small; requires sig = 0)
+          const float y = lam[j] * x;
+          const float e = fexp2(y * LOG2E);
+          const float em1 = (fabsf(y) < 0.0625f) ? expm1_small(y) : (e - 1.0f);
+          const float w = pt * e;
+          w0[j] = fmaf(pt, em1, w0[j]);
+          const float wx = w * x;
+          s1[j] += wx;
+          s2[j] = fmaf(wx, x, s2[j]);
+        } else {
+          const float w = fexp2(fmaf(lam[j], xl, a) - sigl[j]);
+          w0[j] += (sigl[j] == 0.f) ? (w - pt) : w;
+          const float wx = w * x;
+          s1[j] += wx;
+          s2[j] = fmaf(wx, x, s2[j]);
+        }
       }
     }
   }
@@ -289,7 +311,7 @@ __device__ __forceinline__ void lam_chunk(const T* srow, const T* trow, int V, i
   }
 }
 
-template <typename T, int NT, int NC>
+template <typename T, int NT, int NC, bool ACC = false>
 __device__ void lam_sweep(Block<NT>& B, const T* srow, const T* trow, int V, const RowStats& R,
                           const float (&lam)[NC], LamEval (&out)[NC]) {
   constexpr int NW = NT / WAVE;
@@ -301,17 +323,16 @@ __device__ void lam_sweep(Block<NT>& B, const T* srow, const T* trow, int V, con
 #pragma unroll
   for (int j = 0; j < NC; ++j) {
     const double top = static_cast<double>(lam[j]) * (static_cast<double>(R.dmax) - R.c);
-    sigl[j] = top > 60.0 ? static_cast<float>((top - 60.0) * static_cast<double>(LOG2E)) : 0.0f;
+    sigl[j] = (!ACC && top > 60.0) ? static_cast<float>((top - 60.0) * static_cast<double>(LOG2E)) : 0.0f;
   }
-  const float ksl = R.ms * LOG2E;
   double B0 = 0, W[NC], S1[NC], S2[NC];
 #pragma unroll
   for (int j = 0; j < NC; ++j) { W[j] = 0; S1[j] = 0; S2[j] = 0; }
   for (int c = B.wave; c < nchunks; c += NW) {
     if (ragged && c == nchunks - 1)
-      lam_chunk<T, NT, NC, true>(srow, trow, V, c, B.lane, ksl, R.c, lam, sigl, B0, W, S1, S2);
+      lam_chunk<T, NT, NC, true, ACC>(srow, trow, V, c, B.lane, R.ms, R.c, lam, sigl, B0, W, S1, S2);
     else
-      lam_chunk<T, NT, NC, false>(srow, trow, V, c, B.lane, ksl, R.c, lam, sigl, B0, W, S1, S2);
+      lam_chunk<T, NT, NC, false, ACC>(srow, trow, V, c, B.lane, R.ms, R.c, lam, sigl, B0, W, S1, S2);
   }
   double v[1 + 3 * NC];
   v[0] = B0;
@@ -336,10 +357,14 @@ __device__ void lam_sweep(Block<NT>& B, const T* srow, const T* trow, int V, con
     E.Eq = s1 / S0;
     E.Var = fmax(s2 / S0 - E.Eq * E.Eq, 0.0);
     const double l = static_cast<double>(lam[j]);
-    E.KL = l * E.Eq - E.A;
+    E.KL = fmax(l * E.Eq - E.A, 0.0);  // non-negative; rounding can give -1e-16 when p ~ pi
     E.KLp = l * E.Var;
   }
 }
+
+// Rows whose KL (the radius, or KL(pi||p) at the teacher endpoint) is below
+// this use the expm1 forms of the sweeps.
+constexpr double KL_ACCURATE = 0.01;
 
 // Result of the lambda search.
 struct LamResult {
@@ -374,12 +399,31 @@ __device__ LamResult lambda_search(Block<NT>& B, const T* srow, const T* trow, i
     const float cand[2] = {static_cast<float>(l0), 1.0f};
     lam_sweep<T, NT, 2>(B, srow, trow, V, R, cand, E2);
   }
+  // A KL below KL_ACCURATE is resolved with the expm1 form of the sweep: the
+  // plain form carries ~2^-24 absolute error per weight, too much next to a
+  // KL of that size.  Its overflow guard needs lam * (dmax - c) <= 60.
+  const bool acc_ok = (static_cast<double>(R.dmax) - R.c) <= 60.0;
   if (E2[1].KL <= eps) {
     out.lam = 1.0f; out.A = E2[1].A; out.KL = E2[1].KL;
-    return out;
+    if (E2[1].KL < KL_ACCURATE && acc_ok) {
+      LamEval E1[1];
+      const float one[1] = {1.0f};
+      lam_sweep<T, NT, 1, true>(B, srow, trow, V, R, one, E1);
+      if (E1[0].KL <= eps) { out.A = E1[0].A; out.KL = E1[0].KL; return out; }
+      E2[1] = E1[0];  // the accurate value says the endpoint is infeasible
+    } else {
+      return out;
+    }
   }
+  const bool acc = eps < KL_ACCURATE && acc_ok;
   double lo = 0.0, hi = 1.0;
   LamEval cur = E2[0];
+  if (acc) {
+    LamEval E1[1];
+    const float c0[1] = {E2[0].lam};
+    lam_sweep<T, NT, 1, true>(B, srow, trow, V, R, c0, E1);
+    cur = E1[0];
+  }
   const double leps = log(eps);
   for (int it = 0; it < 24; ++it) {
     const double l = cur.lam;
@@ -405,7 +449,8 @@ __device__ LamResult lambda_search(Block<NT>& B, const T* srow, const T* trow, i
     }
     LamEval E1[1];
     const float cand[1] = {nlf};
-    lam_sweep<T, NT, 1>(B, srow, trow, V, R, cand, E1);
+    if (acc) lam_sweep<T, NT, 1, true>(B, srow, trow, V, R, cand, E1);
+    else lam_sweep<T, NT, 1>(B, srow, trow, V, R, cand, E1);
     cur = E1[0];
   }
   out.lam = cur.lam; out.A = cur.A; out.KL = cur.KL;
@@ -419,18 +464,26 @@ __device__ LamResult lambda_search(Block<NT>& B, const T* srow, const T* trow, i
 // ---------------------------------------------------------------------------
 // Residual weight [q_v - p_v]_+ and p_v of one entry; the residual race uses
 // the same function so that its weights are bit-identical to the chunk masses.
-__device__ __forceinline__ float res_weight(float s, float t, float ksl, float invS, float cf,
+// With ACC the ratio minus one, q/p - 1 = expm1(lam x - A), uses the small-
+// argument polynomial near zero (rows whose KL, and so every q/p - 1, is small).
+template <bool ACC>
+__device__ __forceinline__ float res_weight(float s, float t, float ms, float invS, float cf,
                                             float laml, float Al, float* p_out) {
-  const float p = fexp2(fmaf(s, LOG2E, -ksl)) * invS;
+  const float p = fexp2((s - ms) * LOG2E) * invS;
   const float x = (t - s) - cf;
-  const float r = fexp2(fmaf(laml, x, -Al));
+  const float y2 = fmaf(laml, x, -Al);  // log2 of q/p
   *p_out = p;
-  return p * fmaxf(r - 1.0f, 0.0f);
+  if (ACC) {
+    const float y = y2 * LN2;
+    const float em1 = (fabsf(y) < 0.0625f) ? expm1_small(y) : (fexp2(y2) - 1.0f);
+    return p * fmaxf(em1, 0.0f);
+  }
+  return p * fmaxf(fexp2(y2) - 1.0f, 0.0f);
 }
 
-template <typename T, typename G, int NT, bool TAIL, bool GRAD>
+template <typename T, typename G, int NT, bool TAIL, bool GRAD, bool ACC>
 __device__ __forceinline__ void final_chunk(const T* srow, const T* trow, G* grow, int V, int c,
-                                            int lane, float ksl, float invS, float cf, float laml,
+                                            int lane, float ms, float invS, float cf, float laml,
                                             float Al, bool keep_res, float coef, int hot,
                                             RowShared<NT>& sh, double& TV) {
   float s[EPL], t[EPL];
@@ -443,7 +496,7 @@ __device__ __forceinline__ void final_chunk(const T* srow, const T* trow, G* gro
 #pragma unroll
   for (int e = 0; e < EPL; ++e) {
     float p;
-    const float w = res_weight(s[e], t[e], ksl, invS, cf, laml, Al, &p);
+    const float w = res_weight<ACC>(s[e], t[e], ms, invS, cf, laml, Al, &p);
     if (!TAIL || ((vm >> e) & 1u)) tv += w;
     if (GRAD) g[e] = coef * (p - ((base + elem_offset(lane, e) == hot) ? 1.0f : 0.0f));
   }
@@ -455,25 +508,24 @@ __device__ __forceinline__ void final_chunk(const T* srow, const T* trow, G* gro
   if (GRAD) store_lane<G, TAIL>(grow, c, lane, V, g);
 }
 
-template <typename T, typename G, int NT, bool GRAD>
+template <typename T, typename G, int NT, bool GRAD, bool ACC>
 __device__ double final_sweep(Block<NT>& B, const T* srow, const T* trow, G* grow, int V,
                               const RowStats& R, const LamResult& L, bool keep_res, float coef,
                               int hot) {
   constexpr int NW = NT / WAVE;
   const int nchunks = (V + CHUNK - 1) / CHUNK;
   const bool ragged = (V % CHUNK) != 0;
-  const float ksl = R.ms * LOG2E;
   const float invS = static_cast<float>(1.0 / R.sum_s);
   const float laml = L.lam * LOG2E;
   const float Al = static_cast<float>(L.A * static_cast<double>(LOG2E));
   double TV = 0;
   for (int c = B.wave; c < nchunks; c += NW) {
     if (ragged && c == nchunks - 1)
-      final_chunk<T, G, NT, true, GRAD>(srow, trow, grow, V, c, B.lane, ksl, invS, L.c, laml, Al,
-                                        keep_res, coef, hot, B.sh, TV);
+      final_chunk<T, G, NT, true, GRAD, ACC>(srow, trow, grow, V, c, B.lane, R.ms, invS, L.c, laml,
+                                             Al, keep_res, coef, hot, B.sh, TV);
     else
-      final_chunk<T, G, NT, false, GRAD>(srow, trow, grow, V, c, B.lane, ksl, invS, L.c, laml, Al,
-                                         keep_res, coef, hot, B.sh, TV);
+      final_chunk<T, G, NT, false, GRAD, ACC>(srow, trow, grow, V, c, B.lane, R.ms, invS, L.c, laml,
+                                              Al, keep_res, coef, hot, B.sh, TV);
   }
   double v[1] = {TV};
   B.sum(v);
@@ -483,7 +535,7 @@ __device__ double final_sweep(Block<NT>& B, const T* srow, const T* trow, G* gro
 // Gradient-only sweep for rows that carry no coupling (non-finite rows, or
 // the standalone routed loss): grad_v = coef * (p_v - 1[v = hot]).
 template <typename T, typename G, int NT, bool TAIL>
-__device__ __forceinline__ void grad_chunk(const T* srow, G* grow, int V, int c, int lane, float ksl,
+__device__ __forceinline__ void grad_chunk(const T* srow, G* grow, int V, int c, int lane, float ms,
                                            float invS, float coef, int hot, bool nan_row) {
   float s[EPL];
   uint32_t vm;
@@ -492,7 +544,7 @@ __device__ __forceinline__ void grad_chunk(const T* srow, G* grow, int V, int c,
   const int base = c * CHUNK;
 #pragma unroll
   for (int e = 0; e < EPL; ++e) {
-    const float p = fexp2(fmaf(s[e], LOG2E, -ksl)) * invS;
+    const float p = fexp2((s[e] - ms) * LOG2E) * invS;
     g[e] = nan_row ? __builtin_nanf("") : coef * (p - ((base + elem_offset(lane, e) == hot) ? 1.0f : 0.0f));
   }
   store_lane<G, TAIL>(grow, c, lane, V, g);
@@ -504,13 +556,12 @@ __device__ void grad_sweep(Block<NT>& B, const T* srow, G* grow, int V, float ms
   constexpr int NW = NT / WAVE;
   const int nchunks = (V + CHUNK - 1) / CHUNK;
   const bool ragged = (V % CHUNK) != 0;
-  const float ksl = ms * LOG2E;
   const float invS = static_cast<float>(1.0 / sum_s);
   for (int c = B.wave; c < nchunks; c += NW) {
     if (ragged && c == nchunks - 1)
-      grad_chunk<T, G, NT, true>(srow, grow, V, c, B.lane, ksl, invS, coef, hot, nan_row);
+      grad_chunk<T, G, NT, true>(srow, grow, V, c, B.lane, ms, invS, coef, hot, nan_row);
     else
-      grad_chunk<T, G, NT, false>(srow, grow, V, c, B.lane, ksl, invS, coef, hot, nan_row);
+      grad_chunk<T, G, NT, false>(srow, grow, V, c, B.lane, ms, invS, coef, hot, nan_row);
   }
 }
 

@@ -103,7 +103,9 @@ __global__ __launch_bounds__(NT) void couple_kernel(CoupleParams P) {
     const float coef = ROUTE ? static_cast<float>(static_cast<double>(P.grad_scale) * M * (C ? 1.0 : adv)) : 0.0f;
     const int hot = C ? R.vstar : z;
 
-    const double TV = final_sweep<T, G, NT, GRAD>(B, srow, trow, grow, V, R, L, C, coef, hot);
+    const bool acc = L.KL < KL_ACCURATE;
+    const double TV = acc ? final_sweep<T, G, NT, GRAD, true>(B, srow, trow, grow, V, R, L, C, coef, hot)
+                          : final_sweep<T, G, NT, GRAD, false>(B, srow, trow, grow, V, R, L, C, coef, hot);
 
     int y = z;
     if (C) {
@@ -111,7 +113,6 @@ __global__ __launch_bounds__(NT) void couple_kernel(CoupleParams P) {
         const float m = sh.chunk_a[c];
         return m > 0.0f ? log(static_cast<double>(m)) : -__builtin_huge_val();
       });
-      const float ksl = R.ms * LOG2E;
       const float invS = static_cast<float>(1.0 / R.sum_s);
       const float laml = L.lam * LOG2E;
       const float Al = static_cast<float>(L.A * static_cast<double>(LOG2E));
@@ -120,8 +121,9 @@ __global__ __launch_bounds__(NT) void couple_kernel(CoupleParams P) {
       if (c1 < nch) {
         const int yc = elem_race<NT>(B, c1, V, P.seed, RES_ELEM, g, [&](int v) {
           float p;
-          const float w = res_weight(Loader<T>::load1(srow + v), Loader<T>::load1(trow + v), ksl,
-                                     invS, L.c, laml, Al, &p);
+          const float sv = Loader<T>::load1(srow + v), tv = Loader<T>::load1(trow + v);
+          const float w = acc ? res_weight<true>(sv, tv, R.ms, invS, L.c, laml, Al, &p)
+                              : res_weight<false>(sv, tv, R.ms, invS, L.c, laml, Al, &p);
           return w > 0.0f ? flog2(w) * LN2 : -finf();
         });
         if (yc < V) y = yc;
@@ -240,23 +242,25 @@ __global__ __launch_bounds__(NT) void verify_kernel(VerifyParams P) {
       const double u = static_cast<double>(philox_uniform(P.seed, ACCEPT, g, 0));
       const bool accept = u < alpha;
       double TV = __builtin_nan("");
+      const bool acc = L.KL < KL_ACCURATE;
       if (need_tv || !accept)
-        TV = final_sweep<T, float, NT, false>(B, srow, trow, nullptr, V, R, L, !accept, 0.0f, -1);
+        TV = acc ? final_sweep<T, float, NT, false, true>(B, srow, trow, nullptr, V, R, L, !accept, 0.0f, -1)
+                 : final_sweep<T, float, NT, false, false>(B, srow, trow, nullptr, V, R, L, !accept, 0.0f, -1);
       int y = z;
       if (!accept) {
         const int c1 = chunk_race<NT>(B, nch, P.seed, RES_CHUNK, g, [&](int c) {
           const float m = sh.chunk_a[c];
           return m > 0.0f ? log(static_cast<double>(m)) : -__builtin_huge_val();
         });
-        const float ksl = R.ms * LOG2E;
         const float invS = static_cast<float>(1.0 / R.sum_s);
         const float laml = L.lam * LOG2E;
         const float Al = static_cast<float>(L.A * static_cast<double>(LOG2E));
         if (c1 < nch) {
           const int yc = elem_race<NT>(B, c1, V, P.seed, RES_ELEM, g, [&](int v) {
             float p;
-            const float w = res_weight(Loader<T>::load1(srow + v), Loader<T>::load1(trow + v), ksl,
-                                       invS, L.c, laml, Al, &p);
+            const float sv = Loader<T>::load1(srow + v), tv = Loader<T>::load1(trow + v);
+          const float w = acc ? res_weight<true>(sv, tv, R.ms, invS, L.c, laml, Al, &p)
+                              : res_weight<false>(sv, tv, R.ms, invS, L.c, laml, Al, &p);
             return w > 0.0f ? flog2(w) * LN2 : -finf();
           });
           if (yc < V) y = yc;
@@ -337,16 +341,15 @@ __device__ __forceinline__ void lse_chunk(const T* srow, int V, int c, int lane,
   for (int e = 0; e < EPL; ++e)
     if (!TAIL || ((vm >> e) & 1u)) ls = fmaxf(ls, s[e]);
   const float cms = wave_max(ls);
-  const float ks = cms * LOG2E;
-  float ps = 0.f;
+  double ps = 0.0;
 #pragma unroll
   for (int e = 0; e < EPL; ++e)
-    if (!TAIL || ((vm >> e) & 1u)) ps += fexp2(fmaf(s[e], LOG2E, -ks));
+    if (!TAIL || ((vm >> e) & 1u)) ps += static_cast<double>(fexp2((s[e] - cms) * LOG2E));
   if (cms > Ms) {
-    Ss *= fexp2((Ms - cms) * LOG2E);
+    Ss *= static_cast<double>(fexp2((Ms - cms) * LOG2E));
     Ms = cms;
   }
-  Ss += static_cast<double>(ps * fexp2((cms - Ms) * LOG2E));
+  Ss += ps * ((cms == Ms) ? 1.0 : static_cast<double>(fexp2((cms - Ms) * LOG2E)));
 }
 
 template <typename T, typename G, bool GRAD>
@@ -367,7 +370,7 @@ __global__ __launch_bounds__(NT) void route_kernel(RouteParams P) {
       else lse_chunk<T, false>(srow, V, c, B.lane, Ms, Ss);
     }
     const float ms = B.max(Ms);
-    double v[1] = {(Ms == -finf()) ? 0.0 : Ss * fexp2((Ms - ms) * LOG2E)};
+    double v[1] = {(Ms == -finf()) ? 0.0 : (Ms == ms) ? Ss : Ss * static_cast<double>(fexp2((Ms - ms) * LOG2E))};
     B.sum(v);
     const double lse = static_cast<double>(ms) + log(v[0]);
     const bool M = P.valid ? (P.valid[r] != 0) : true;

@@ -74,6 +74,7 @@ def _row_properties(o, eps, grad=None):
     assert np.all(np.abs(o["kl"][interior] - eps) <= 2e-5 * eps)
     assert np.all(o["kl"] <= eps * (1 + 2e-5))
     # Cor. 1 (Pinsker) and Prop. 1 (correction rate = TV, on average)
+    assert np.all(o["kl"] >= 0)
     assert np.all(o["tv"] <= np.sqrt(o["kl"] / 2) * (1 + 1e-5) + 1e-7)
     n = len(lam)
     rate, mean_tv = o["corrected"].mean(), o["tv"].mean()
