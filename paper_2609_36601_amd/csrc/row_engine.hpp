@@ -17,12 +17,14 @@
 
 namespace saki {
 
+constexpr int RED_MAX = 12;  // widest block reduction (doubles per thread)
+
 template <int NT>
 struct RowShared {
   static constexpr int NW = NT / WAVE;
   float chunk_a[MAX_CHUNKS];  // proposal: chunk max of s | residual: chunk mass
   float chunk_b[MAX_CHUNKS];  // proposal: chunk sum of exp(s - chunk max)
-  double red_d[NW][8];
+  double red_d[NW][RED_MAX];
   float red_f[NW][4];
   int red_i[NW][4];
 };
@@ -33,7 +35,9 @@ struct RowStats {
   double lse_s, lse_t; // log-sum-exp of s and t
   double sum_s;        // sum exp(s - ms)
   float c;             // centring constant: E_p[d] rounded to float
-  double var;          // Var_p[d] (starting point of the lambda search)
+  double var;          // Var_p[d] = kappa_2 (starting point of the lambda search)
+  double k3, k4;       // third and fourth cumulants of d under p
+  double kl1_est;      // KL(pi || p) = E_pi[d] - (lse_t - lse_s), a first estimate
   float dmin, dmax;    // range of d = t - s
   float tmax;          // max t
   int vstar;           // argmax t, lowest index on ties
@@ -60,6 +64,7 @@ struct Block {
   // Sums N doubles over the block; every thread gets the same bits.
   template <int N>
   __device__ void sum(double (&v)[N]) {
+    static_assert(N <= RED_MAX, "block reduction wider than the LDS buffer");
 #pragma unroll
     for (int i = 0; i < N; ++i) v[i] = wave_sum(v[i]);
     if (lane == 0) {
@@ -135,7 +140,8 @@ template <typename T, int NT, bool TAIL>
 __device__ __forceinline__ void stats_chunk(const T* srow, const T* trow, int V, int c, int lane,
                                             bool keep_chunks, RowShared<NT>& sh, float& Ms,
                                             float& Mt, double& Ss, double& S1, double& S2,
-                                            double& St, float& tbest, int& tidx,
+                                            double& S3, double& S4, double& St, double& T1,
+                                            float& tbest, int& tidx,
                                             float& dmin, float& dmax) {
   float s[EPL], t[EPL];
   uint32_t vm;
@@ -153,7 +159,7 @@ __device__ __forceinline__ void stats_chunk(const T* srow, const T* trow, int V,
   // exponent arguments as (x - max) * log2(e): the subtraction is exact, so
   // the largest terms carry no rounding from the shift
   double ps = 0.0, pt = 0.0;
-  float p1 = 0.f, p2 = 0.f;
+  float p1 = 0.f, p2 = 0.f, p3 = 0.f, p4 = 0.f, t1 = 0.f;
   const int base = c * CHUNK;
 #pragma unroll
   for (int e = 0; e < EPL; ++e) {
@@ -166,8 +172,13 @@ __device__ __forceinline__ void stats_chunk(const T* srow, const T* trow, int V,
       ps += static_cast<double>(es);
       pt += static_cast<double>(et);
       const float ed = es * d;
+      const float ed2 = ed * d;
+      const float ed3 = ed2 * d;
       p1 += ed;
-      p2 = fmaf(ed, d, p2);
+      p2 += ed2;
+      p3 += ed3;
+      p4 = fmaf(ed3, d, p4);
+      t1 = fmaf(et, d, t1);
       if (t[e] > tbest) {
         tbest = t[e];
         tidx = base + elem_offset(lane, e);
@@ -186,11 +197,12 @@ __device__ __forceinline__ void stats_chunk(const T* srow, const T* trow, int V,
   // fold this chunk into the wave's running sums (all lanes share Ms, Mt)
   if (cms > Ms) {
     const double f = static_cast<double>(fexp2((Ms - cms) * LOG2E));
-    Ss *= f; S1 *= f; S2 *= f;
+    Ss *= f; S1 *= f; S2 *= f; S3 *= f; S4 *= f;
     Ms = cms;
   }
   if (cmt > Mt) {
-    St *= static_cast<double>(fexp2((Mt - cmt) * LOG2E));
+    const double f = static_cast<double>(fexp2((Mt - cmt) * LOG2E));
+    St *= f; T1 *= f;
     Mt = cmt;
   }
   // chunks below the running maximum are rescaled; the chunk holding the
@@ -200,7 +212,10 @@ __device__ __forceinline__ void stats_chunk(const T* srow, const T* trow, int V,
   Ss += ps * gs;
   S1 += static_cast<double>(p1) * gs;
   S2 += static_cast<double>(p2) * gs;
+  S3 += static_cast<double>(p3) * gs;
+  S4 += static_cast<double>(p4) * gs;
   St += pt * gt;
+  T1 += static_cast<double>(t1) * gt;
 }
 
 template <typename T, int NT>
@@ -209,17 +224,17 @@ __device__ RowStats stats_sweep(Block<NT>& B, const T* srow, const T* trow, int 
   const int nchunks = (V + CHUNK - 1) / CHUNK;
   const bool ragged = (V % CHUNK) != 0;
   float Ms = -finf(), Mt = -finf();
-  double Ss = 0, S1 = 0, S2 = 0, St = 0;
+  double Ss = 0, S1 = 0, S2 = 0, S3 = 0, S4 = 0, St = 0, T1 = 0;
   float tbest = -finf();
   int tidx = 0x7fffffff;
   float dmin = finf(), dmax = -finf();
   for (int c = B.wave; c < nchunks; c += NW) {
     if (ragged && c == nchunks - 1)
-      stats_chunk<T, NT, true>(srow, trow, V, c, B.lane, keep_chunks, B.sh, Ms, Mt, Ss, S1, S2, St,
-                               tbest, tidx, dmin, dmax);
+      stats_chunk<T, NT, true>(srow, trow, V, c, B.lane, keep_chunks, B.sh, Ms, Mt, Ss, S1, S2, S3,
+                               S4, St, T1, tbest, tidx, dmin, dmax);
     else
-      stats_chunk<T, NT, false>(srow, trow, V, c, B.lane, keep_chunks, B.sh, Ms, Mt, Ss, S1, S2,
-                                St, tbest, tidx, dmin, dmax);
+      stats_chunk<T, NT, false>(srow, trow, V, c, B.lane, keep_chunks, B.sh, Ms, Mt, Ss, S1, S2, S3,
+                                S4, St, T1, tbest, tidx, dmin, dmax);
   }
   RowStats R;
   R.ms = B.max(Ms);
@@ -227,7 +242,7 @@ __device__ RowStats stats_sweep(Block<NT>& B, const T* srow, const T* trow, int 
   // rescale each wave's sums to the row maxima, then add in a fixed order
   const double gs = (Ms == -finf()) ? 0.0 : (Ms == R.ms) ? 1.0 : static_cast<double>(fexp2((Ms - R.ms) * LOG2E));
   const double gt = (Mt == -finf()) ? 0.0 : (Mt == R.mt) ? 1.0 : static_cast<double>(fexp2((Mt - R.mt) * LOG2E));
-  double v[4] = {Ss * gs, S1 * gs, S2 * gs, St * gt};
+  double v[7] = {Ss * gs, S1 * gs, S2 * gs, S3 * gs, S4 * gs, St * gt, T1 * gt};
   B.sum(v);
   B.argmax(tbest, tidx);
   R.dmin = B.min(dmin);
@@ -236,9 +251,12 @@ __device__ RowStats stats_sweep(Block<NT>& B, const T* srow, const T* trow, int 
   R.vstar = tidx;
   R.sum_s = v[0];
   R.lse_s = static_cast<double>(R.ms) + log(v[0]);
-  R.lse_t = static_cast<double>(R.mt) + log(v[3]);
-  const double Ed = v[1] / v[0];
-  R.var = fmax(v[2] / v[0] - Ed * Ed, 0.0);
+  R.lse_t = static_cast<double>(R.mt) + log(v[5]);
+  const double Ed = v[1] / v[0], E2 = v[2] / v[0], E3 = v[3] / v[0], E4 = v[4] / v[0];
+  R.var = fmax(E2 - Ed * Ed, 0.0);
+  R.k3 = E3 - 3.0 * Ed * E2 + 2.0 * Ed * Ed * Ed;
+  R.k4 = (E4 - 4.0 * Ed * E3 + 6.0 * Ed * Ed * E2 - 3.0 * Ed * Ed * Ed * Ed) - 3.0 * R.var * R.var;
+  R.kl1_est = v[6] / v[5] - (R.lse_t - R.lse_s);
   R.c = static_cast<float>(Ed);
   R.finite = isfinite(R.lse_s) && isfinite(R.lse_t) && isfinite(Ed) && isfinite(v[2]) &&
              isfinite(R.dmin) && isfinite(R.dmax) && isfinite(R.ms) &&
@@ -374,12 +392,95 @@ struct LamResult {
   float c;     // centring constant used by A (may differ from RowStats::c)
 };
 
+// Degree-8 Hermite interpolant of A(lambda) through three nodes carrying
+// A, A' and A'' (Newton divided differences with each node repeated three
+// times).  KL(lambda) = lambda A'(lambda) - A(lambda) on the interpolant.
+struct Hermite3 {
+  double z[9], a[9];
+  __device__ void build(const LamEval (&E)[3]) {
+    // in-place divided differences; order 1 and 2 differences over a repeated
+    // node are A' and A'' / 2 at that node
+    for (int i = 0; i < 9; ++i) {
+      z[i] = E[i / 3].lam;
+      a[i] = E[i / 3].A;
+    }
+    for (int j = 1; j < 9; ++j) {
+      for (int i = 8; i >= j; --i) {
+        if (z[i] == z[i - j]) {
+          a[i] = (j == 1) ? E[i / 3].Eq : 0.5 * E[i / 3].Var;
+        } else {
+          a[i] = (a[i] - a[i - 1]) / (z[i] - z[i - j]);
+        }
+      }
+    }
+  }
+  // A, A', A'' at l
+  __device__ void eval(double l, double& p0, double& p1, double& p2) const {
+    double p = a[8], dp = 0.0, ddp = 0.0;
+    for (int j = 7; j >= 0; --j) {
+      const double h = l - z[j];
+      ddp = ddp * h + 2.0 * dp;
+      dp = dp * h + p;
+      p = p * h + a[j];
+    }
+    p0 = p; p1 = dp; p2 = ddp;
+  }
+  // |d/dl (l * T'(l) - T(l))|-style size of the top Newton term T, an
+  // estimate of the interpolant's truncation error in KL at l
+  __device__ double top_term(double l) const {
+    double prod = a[8], dprod = 0.0;
+    for (int j = 0; j < 8; ++j) {
+      const double h = l - z[j];
+      dprod = dprod * h + prod;
+      prod = prod * h;
+    }
+    return fabs(l * dprod - prod);
+  }
+  // root of lambda A' - A = eps in [lo, hi], where KL(lo) <= eps < KL(hi)
+  __device__ double solve(double eps, double lo, double hi) const {
+    double l = 0.5 * (lo + hi);
+    for (int it = 0; it < 60; ++it) {
+      double A0, A1, A2;
+      eval(l, A0, A1, A2);
+      const double f = l * A1 - A0 - eps;
+      if (f <= 0) lo = l; else hi = l;
+      const double fp = l * A2;
+      double nl = (fp > 0) ? l - f / fp : 0.5 * (lo + hi);
+      if (!(nl > lo && nl < hi)) nl = 0.5 * (lo + hi);
+      if (fabs(nl - l) <= 1e-15 * l) { l = nl; break; }
+      l = nl;
+    }
+    return l;
+  }
+};
+
+// Start of the search from the cumulants of d under p:
+// KL(lam) = sum_n (n - 1) kappa_n lam^n / n! ~ k2 lam^2/2 + k3 lam^3/3 + k4 lam^4/8.
+__device__ inline double cumulant_start(const RowStats& R, double eps) {
+  if (!(R.var > 0)) return 0.5;
+  const double l2 = sqrt(2.0 * eps / R.var);
+  double l = l2;
+  for (int it = 0; it < 20; ++it) {
+    const double f = R.var * l * l / 2 + R.k3 * l * l * l / 3 + R.k4 * l * l * l * l / 8 - eps;
+    const double fp = R.var * l + R.k3 * l * l + R.k4 * l * l * l / 2;
+    if (!(fp > 0)) { l = l2; break; }
+    const double nl = l - f / fp;
+    if (!(nl > 0.25 * l2 && nl < 4.0 * l2)) { l = l2; break; }
+    l = nl;
+  }
+  return l;
+}
+
 // Largest lambda in [0, 1] with KL(q_lambda || p) <= eps (Eq. trust_region).
+// Each lambda sweep evaluates a symmetric three-node stencil {c - h, c, c + h}
+// (shifted below 1 when it would pass the teacher endpoint).  When the nodes
+// bracket the root, the Hermite interpolant of A gives lambda* and A(lambda*);
+// its top Newton term bounds the truncation error, and a stencil whose
+// estimate exceeds HERMITE_TOL * eps is followed by a tight +-2% stencil.
 template <typename T, int NT>
 __device__ LamResult lambda_search(Block<NT>& B, const T* srow, const T* trow, int V,
-                                   const RowStats& R0, double eps) {
+                                   const RowStats& R, double eps) {
   LamResult out;
-  RowStats R = R0;
   if (R.dmin == R.dmax) {
     // t - s constant: p = pi, KL = 0 for every lambda, lambda* = 1, q = p
     out.lam = 1.0f; out.A = 0.0; out.KL = 0.0; out.c = R.dmin;
@@ -390,70 +491,95 @@ __device__ LamResult lambda_search(Block<NT>& B, const T* srow, const T* trow, i
     out.lam = 0.0f; out.A = 0.0; out.KL = 0.0;
     return out;
   }
-  // first sweep: the teacher endpoint and a small-lambda start,
-  // KL(lam) ~ lam^2 Var_p(d) / 2  =>  lam0 = sqrt(2 eps / Var)
-  double l0 = R.var > 0 ? sqrt(2.0 * eps / R.var) : 0.5;
-  l0 = fmin(fmax(l0, 1e-6), 0.999);
-  LamEval E2[2];
-  {
-    const float cand[2] = {static_cast<float>(l0), 1.0f};
-    lam_sweep<T, NT, 2>(B, srow, trow, V, R, cand, E2);
-  }
   // A KL below KL_ACCURATE is resolved with the expm1 form of the sweep: the
   // plain form carries ~2^-24 absolute error per weight, too much next to a
   // KL of that size.  Its overflow guard needs lam * (dmax - c) <= 60.
   const bool acc_ok = (static_cast<double>(R.dmax) - R.c) <= 60.0;
-  if (E2[1].KL <= eps) {
-    out.lam = 1.0f; out.A = E2[1].A; out.KL = E2[1].KL;
-    if (E2[1].KL < KL_ACCURATE && acc_ok) {
-      LamEval E1[1];
-      const float one[1] = {1.0f};
-      lam_sweep<T, NT, 1, true>(B, srow, trow, V, R, one, E1);
-      if (E1[0].KL <= eps) { out.A = E1[0].A; out.KL = E1[0].KL; return out; }
-      E2[1] = E1[0];  // the accurate value says the endpoint is infeasible
-    } else {
+  bool acc = eps < KL_ACCURATE && acc_ok;
+  constexpr double DELTA0 = 0.25;       // first stencil half-width, relative
+  constexpr double DELTA_TIGHT = 0.02;  // refinement stencil half-width
+  constexpr double HERMITE_TOL = 1e-6;  // accepted truncation estimate, relative to eps
+  constexpr double LMAX = 1.0 - 1e-6;
+  double lo = 0.0, hi = 1.0;  // KL(lo) <= eps < KL(hi) (hi = 1 until a node above is seen)
+  LamEval feas;               // the largest evaluated lambda that is feasible (lambda = 0 is)
+  feas.lam = 0.0f; feas.A = 0.0; feas.KL = 0.0;
+  double lg = fmin(fmax(cumulant_start(R, eps), 1e-7), LMAX);
+  double delta = DELTA0;
+  bool try_one = R.kl1_est <= 1.05 * eps + 1e-5;
+  for (int sweep = 0; sweep < 12; ++sweep) {
+    double h = delta * lg;
+    double c0 = lg;
+    if (try_one) {
+      h = delta / (1.0 + delta);
+      c0 = 1.0 - h;
+    } else if (lg + h > 1.0) {
+      h = fmin(h, 0.49);
+      c0 = 1.0 - h;
+    }
+    float L[3] = {static_cast<float>(c0 - h), static_cast<float>(c0),
+                  static_cast<float>(fmin(c0 + h, 1.0))};
+    if (!(L[0] > 0.0f && L[0] < L[1] && L[1] < L[2])) {  // spacing below float resolution
+      L[1] = static_cast<float>(c0);
+      L[0] = static_cast<float>(c0 * (1 - 4e-6));
+      L[2] = static_cast<float>(fmin(c0 * (1 + 4e-6), 1.0));
+    }
+    LamEval E[3];
+    if (acc) lam_sweep<T, NT, 3, true>(B, srow, trow, V, R, L, E);
+    else lam_sweep<T, NT, 3>(B, srow, trow, V, R, L, E);
+    if (L[2] == 1.0f && E[2].KL <= eps) {
+      if (!acc && acc_ok && E[2].KL < KL_ACCURATE) {
+        acc = true;  // resolve a small endpoint KL with the accurate form
+        try_one = true;
+        continue;
+      }
+      out.lam = 1.0f; out.A = E[2].A; out.KL = E[2].KL;
       return out;
     }
-  }
-  const bool acc = eps < KL_ACCURATE && acc_ok;
-  double lo = 0.0, hi = 1.0;
-  LamEval cur = E2[0];
-  if (acc) {
-    LamEval E1[1];
-    const float c0[1] = {E2[0].lam};
-    lam_sweep<T, NT, 1, true>(B, srow, trow, V, R, c0, E1);
-    cur = E1[0];
-  }
-  const double leps = log(eps);
-  for (int it = 0; it < 24; ++it) {
-    const double l = cur.lam;
-    if (cur.KL <= eps) lo = fmax(lo, l); else hi = fmin(hi, l);
-    double nl;
-    bool newton_ok = cur.KL > 0 && cur.KLp > 0 && isfinite(cur.KL);
-    double step = 0;
-    if (newton_ok) {
-      // Newton on log KL(lam) - log eps
-      step = -(log(cur.KL) - leps) * cur.KL / cur.KLp;
-      nl = l + step;
-      if (!(nl > lo && nl < hi)) newton_ok = false;
+    try_one = false;
+    for (int j = 0; j < 3; ++j) {
+      if (E[j].KL <= eps) {
+        if (static_cast<double>(L[j]) >= lo) { lo = L[j]; feas = E[j]; }
+      } else {
+        hi = fmin(hi, static_cast<double>(L[j]));
+      }
     }
-    if (!newton_ok) nl = (lo > 0) ? sqrt(lo * hi) : 0.25 * hi;
-    const float nlf = static_cast<float>(nl);
-    if (newton_ok && (fabs(step) <= 2e-8 * l || nlf == cur.lam)) {
-      // converged: extrapolate A and KL from the last evaluation to lambda*
-      const double dl = static_cast<double>(nlf) - l;
-      out.lam = nlf;
-      out.A = cur.A + cur.Eq * dl + 0.5 * cur.Var * dl * dl;
-      out.KL = cur.KL + cur.KLp * dl;
-      return out;
+    if (E[0].KL <= eps && eps < E[2].KL) {
+      Hermite3 H;
+      H.build(E);
+      const int k = (E[1].KL <= eps) ? 1 : 0;
+      const double root = H.solve(eps, L[k], L[k + 1]);
+      const double h0 = static_cast<double>(L[1]) - L[0], h1 = static_cast<double>(L[2]) - L[1];
+      const bool regular = h1 <= 1.5 * h0 && h0 <= 1.5 * h1;
+      const bool accurate = H.top_term(root) <= HERMITE_TOL * eps;
+      if ((regular && (accurate || delta <= 1.05 * DELTA_TIGHT)) || sweep >= 10) {
+        const float lf = static_cast<float>(root);
+        double A0, A1, A2;
+        H.eval(static_cast<double>(lf), A0, A1, A2);
+        out.lam = lf;
+        out.A = A0;
+        out.KL = fmax(static_cast<double>(lf) * A1 - A0, 0.0);
+        return out;
+      }
+      lg = fmin(root, LMAX);
+      delta = DELTA_TIGHT;
+      continue;
     }
-    LamEval E1[1];
-    const float cand[1] = {nlf};
-    if (acc) lam_sweep<T, NT, 1, true>(B, srow, trow, V, R, cand, E1);
-    else lam_sweep<T, NT, 1>(B, srow, trow, V, R, cand, E1);
-    cur = E1[0];
+    // root outside the stencil: Newton in log KL from the nearest node
+    const bool above = E[2].KL < eps;
+    const LamEval& n = above ? E[2] : E[0];
+    double g = above ? 0.5 * (static_cast<double>(n.lam) + hi) : 0.5 * (lo + n.lam);
+    if (n.KL > 0 && n.KLp > 0) {
+      const double t = n.lam - (log(n.KL) - log(eps)) * n.KL / n.KLp;
+      if (t > lo && t < hi) g = t;
+    }
+    g = fmin(fmax(g, 1e-7), LMAX);
+    delta = fmin(fmax(fabs(g - n.lam) / g, DELTA_TIGHT), 0.3);
+    lg = g;
+    if (above && L[2] < 1.0f && hi >= 1.0) try_one = lg * (1.0 + delta) >= 1.0;
   }
-  out.lam = cur.lam; out.A = cur.A; out.KL = cur.KL;
+  // not reached in practice (the bracket shrinks every sweep): keep the
+  // largest feasible evaluated lambda
+  out.lam = feas.lam; out.A = feas.A; out.KL = feas.KL;
   return out;
 }
 

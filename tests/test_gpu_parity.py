@@ -60,10 +60,17 @@ def test_mid_sampled_rows(saki_lib, eps):
     rng = np.random.default_rng(int(eps * 100))
     rows = np.unique(np.concatenate([[0, 1, 4095], rng.choice(4096, 45, replace=False)]))
     out, o, R = run_and_compare(saki_lib, s, t, eps, workloads.coupling_seed("mid"), rows=rows)
-    # properties on every row
-    assert np.all(o["row_status"] == 0)
-    assert np.all(o["kl"] <= eps * (1 + 1e-5) + 1e-9)
-    assert np.all(o["tv"] <= np.sqrt(o["kl"] / 2) * (1 + 1e-5) + 1e-7)
+    # properties on every row; rows that break one are compared with the oracle
+    bad = np.nonzero((o["row_status"] != 0) | (o["kl"] > eps * (1 + 1e-5) + 1e-9) |
+                     (o["tv"] > np.sqrt(o["kl"] / 2) * (1 + 1e-5) + 1e-7))[0]
+    if bad.size:
+        say(f"rows breaking a property: {bad[:10].tolist()} (of {bad.size})")
+        ii = torch.as_tensor(bad[:4], device=DEV)
+        R2 = parity.compare_couple(o, f64(s[ii]), f64(t[ii]), eps, workloads.coupling_seed("mid"), 0,
+                                   bad[:4])
+        say(R2.summary())
+        R2.check()
+    assert bad.size == 0
 
 
 def _row_properties(o, eps, grad=None):
