@@ -18,6 +18,36 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
 
+KERNEL_SOURCES = ["paper_2609_36601_amd/csrc/saki.hip", "paper_2609_36601_amd/csrc/row_engine.hpp",
+                  "paper_2609_36601_amd/csrc/device_util.hpp"]
+
+# HBM traffic of one couple-kernel launch on the large workload (eps 0.2), from
+# two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch;
+# profiles/couple_kernel_large.md).  A plain 1 GiB device copy reads
+# FETCH_SIZE = 524,308 KiB and WRITE_SIZE = 1,048,576 KiB on the same box, so
+# FETCH_SIZE is scaled by 2.0 and WRITE_SIZE by 1.0.  Keyed by the SHA-256 of
+# the kernel sources: a changed kernel reports traffic = null until re-measured.
+MEASURED_TRAFFIC = {
+    "23bc66102a3329049d74bb4b5e2310b5881561afcd3027fbe7d47719f5392d0d":
+        dict(fetch_kib=67821501.1, write_kib=56363053.0, fetch_scale=2.0, write_scale=1.0),
+}
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic_bytes():
+    m = MEASURED_TRAFFIC.get(kernel_source_hash())
+    if m is None:
+        return None
+    return (m["fetch_kib"] * m["fetch_scale"] + m["write_kib"] * m["write_scale"]) * 1024.0
+
 
 def _oracle_rows(args):
     """CPU oracle on a batch of rows (runs in a worker process)."""
@@ -68,6 +98,8 @@ def main():
     ap.add_argument("--rows", type=int, default=None, help="override the row count (debug)")
     ap.add_argument("--cpu-sample", type=int, default=64)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run one 1 GiB device copy before timing (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
@@ -96,6 +128,14 @@ def main():
     ws = torch.empty(max(saki.workspace_bytes(saki.SAKI_OP_COUPLE, n, V), 8), dtype=torch.uint8,
                      device=dev)
     torch.cuda.synchronize()
+    if args.calibrate_copy:
+        # a plain copy of known size: its FETCH_SIZE / WRITE_SIZE per byte moved
+        # scales the counters read for the coupling kernel
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     def step():
         saki.saki_couple(s, t, args.eps, seed, 0, out, route, ws)
@@ -146,7 +186,8 @@ def main():
                                "rho~U(0.3,0.95), coupling + routed loss + fp32 grad",
                    "rows": n, "vocab": V, "eps": args.eps, "grad_dtype": "f32"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None},
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": measured_traffic_bytes() if n == cfg["rows"] and args.eps == 0.2 else None},
         "cpu_baseline": cpu,
         "stats": {"correction_rate": corr_rate, "mean_tv": mean_tv, "mean_lambda": mean_lam},
     }
