@@ -62,6 +62,69 @@ struct Loader<float> {
   static __device__ __forceinline__ float load1(const float* p) { return *p; }
 };
 
+// ---------------------------------------------------------------------------
+// Streaming loads through the global address space (global_load, not flat).
+// Frag<T> holds one lane's 16 packed entries of one array in one chunk.
+// ---------------------------------------------------------------------------
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) const u32x4 g_cu32x4;
+
+__device__ __forceinline__ uint4 gload16(const void* p) {
+  const u32x4 v = *(g_cu32x4*)(p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+template <typename T>
+struct Frag;
+template <>
+struct Frag<uint16_t> {
+  uint4 q[2];
+};
+template <>
+struct Frag<float> {
+  uint4 q[4];
+};
+
+template <typename T>
+__device__ __forceinline__ void frag_load(Frag<T>& f, const T* row, int c, int lane) {
+  const T* p = row + c * CHUNK + 8 * lane;
+  if constexpr (sizeof(T) == 2) {
+    f.q[0] = gload16(p);
+    f.q[1] = gload16(p + 512);
+  } else {
+    f.q[0] = gload16(p);
+    f.q[1] = gload16(p + 4);
+    f.q[2] = gload16(p + 512);
+    f.q[3] = gload16(p + 516);
+  }
+}
+
+__device__ __forceinline__ void unpack_bf16x8(const uint4 q, float* y) {
+  y[0] = __uint_as_float(q.x << 16);
+  y[1] = __uint_as_float(q.x & 0xffff0000u);
+  y[2] = __uint_as_float(q.y << 16);
+  y[3] = __uint_as_float(q.y & 0xffff0000u);
+  y[4] = __uint_as_float(q.z << 16);
+  y[5] = __uint_as_float(q.z & 0xffff0000u);
+  y[6] = __uint_as_float(q.w << 16);
+  y[7] = __uint_as_float(q.w & 0xffff0000u);
+}
+
+// x[e] in the elem_offset order.
+__device__ __forceinline__ void frag_unpack(const Frag<uint16_t>& f, float* x) {
+  unpack_bf16x8(f.q[0], x);
+  unpack_bf16x8(f.q[1], x + 8);
+}
+__device__ __forceinline__ void frag_unpack(const Frag<float>& f, float* x) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    x[4 * i + 0] = __uint_as_float(f.q[i].x);
+    x[4 * i + 1] = __uint_as_float(f.q[i].y);
+    x[4 * i + 2] = __uint_as_float(f.q[i].z);
+    x[4 * i + 3] = __uint_as_float(f.q[i].w);
+  }
+}
+
 // Loads the 16 entries of this lane in chunk c.  With TAIL the chunk may end
 // before 1024 entries: missing entries are not read and their bit in *valid is 0.
 template <typename T, bool TAIL>
@@ -98,14 +161,21 @@ __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
   return (u + rounding) >> 16;
 }
 
+// Gradient rows are written once and not read back: non-temporal stores.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) f32x4 g_f32x4;
+typedef __attribute__((address_space(1))) u32x4 g_u32x4;
+
 template <typename G>
 struct Storer;
 
 template <>
 struct Storer<float> {
   static __device__ __forceinline__ void store8(float* p, const float* x) {
-    *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
-    *reinterpret_cast<float4*>(p + 4) = make_float4(x[4], x[5], x[6], x[7]);
+    f32x4 a = {x[0], x[1], x[2], x[3]};
+    f32x4 b = {x[4], x[5], x[6], x[7]};
+    __builtin_nontemporal_store(a, (g_f32x4*)(p));
+    __builtin_nontemporal_store(b, (g_f32x4*)(p + 4));
   }
   static __device__ __forceinline__ void store1(float* p, float x) { *p = x; }
 };
@@ -118,7 +188,8 @@ struct Storer<uint16_t> {
     q.y = f32_to_bf16_bits(x[2]) | (f32_to_bf16_bits(x[3]) << 16);
     q.z = f32_to_bf16_bits(x[4]) | (f32_to_bf16_bits(x[5]) << 16);
     q.w = f32_to_bf16_bits(x[6]) | (f32_to_bf16_bits(x[7]) << 16);
-    *reinterpret_cast<uint4*>(p) = q;
+    u32x4 v = {q.x, q.y, q.z, q.w};
+    __builtin_nontemporal_store(v, (g_u32x4*)(p));
   }
   static __device__ __forceinline__ void store1(uint16_t* p, float x) {
     *p = static_cast<uint16_t>(f32_to_bf16_bits(x));
@@ -186,6 +257,12 @@ __device__ __forceinline__ void wave_argmax(float& val, int& idx) {
   }
 }
 
+__device__ __forceinline__ int wave_min(int v) {
+#pragma unroll
+  for (int o = WAVE / 2; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, WAVE));
+  return v;
+}
+
 // ---------------------------------------------------------------------------
 // Philox-4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11) and the stream layout:
 // key = (seed lo, seed hi), counter = (block j, stream, g lo, g hi); the four
@@ -212,11 +289,15 @@ __device__ __forceinline__ float word_to_uniform(uint32_t x) {
   return static_cast<float>(2u * (x >> 9) + 1u) * 0x1p-24f;
 }
 
+// Block j of (seed, stream, g): the words of indices 4j .. 4j+3.
+__device__ __forceinline__ uint4 philox_block(uint64_t seed, uint32_t stream, uint64_t g, uint32_t j) {
+  return philox4x32_10(make_uint4(j, stream, static_cast<uint32_t>(g), static_cast<uint32_t>(g >> 32)),
+                       static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32));
+}
+
 __device__ __forceinline__ float philox_uniform(uint64_t seed, uint32_t stream, uint64_t g,
                                                 uint32_t index) {
-  const uint4 w = philox4x32_10(
-      make_uint4(index >> 2, stream, static_cast<uint32_t>(g), static_cast<uint32_t>(g >> 32)),
-      static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32));
+  const uint4 w = philox_block(seed, stream, g, index >> 2);
   const uint32_t sel = index & 3u;
   const uint32_t x = sel == 0 ? w.x : sel == 1 ? w.y : sel == 2 ? w.z : w.w;
   return word_to_uniform(x);

@@ -1,8 +1,10 @@
 // SAKI coupling-and-routing kernels for gfx950 and the C ABI of include/saki.h.
 //
-// One workgroup of NT = 512 threads (8 waves) owns one row at a time and
-// walks the grid's rows persistently; the row engine (row_engine.hpp) runs the
-// stats sweep, the lambda sweeps and the final sweep over that row.
+// One workgroup of NT = 256 threads (4 waves) owns one row at a time and
+// walks the grid's rows persistently; two workgroups share a compute unit, so
+// one row's serial steps (reductions, the lambda search, the races) overlap
+// the other's streaming sweeps.  The row engine (row_engine.hpp) runs the
+// stats sweep, the lambda sweeps and the final sweep over a row.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -16,8 +18,8 @@
 
 namespace saki {
 
-constexpr int NT = 512;
-constexpr int WG_PER_CU = 1;
+constexpr int NT = 256;
+constexpr int WG_PER_CU = 2;
 
 struct CoupleParams {
   const void* s;
@@ -41,7 +43,7 @@ struct CoupleParams {
 __device__ __forceinline__ float nanf_() { return __builtin_nanf(""); }
 
 template <typename T, typename G, bool ROUTE, bool GRAD>
-__global__ __launch_bounds__(NT) void couple_kernel(CoupleParams P) {
+__global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
   __shared__ RowShared<NT> sh;
   Block<NT> B(sh);
   const int V = P.V;
@@ -92,8 +94,7 @@ __global__ __launch_bounds__(NT) void couple_kernel(CoupleParams P) {
 
     // accept test, Eq. accept in the log form exp(min(0, log q(z) - log p(z)))
     const float sz = Loader<T>::load1(srow + z), tz = Loader<T>::load1(trow + z);
-    const double xz = (static_cast<double>(tz) - static_cast<double>(sz)) - static_cast<double>(L.c);
-    const double alpha = exp(fmin(0.0, static_cast<double>(L.lam) * xz - L.A));
+    const double alpha = exp(fmin(0.0, L.log_ratio(sz, tz)));
     const double u = static_cast<double>(philox_uniform(P.seed, ACCEPT, g, 0));
     const bool C = !(u < alpha);
 
@@ -103,9 +104,9 @@ __global__ __launch_bounds__(NT) void couple_kernel(CoupleParams P) {
     const float coef = ROUTE ? static_cast<float>(static_cast<double>(P.grad_scale) * M * (C ? 1.0 : adv)) : 0.0f;
     const int hot = C ? R.vstar : z;
 
-    const bool acc = L.KL < KL_ACCURATE;
-    const double TV = acc ? final_sweep<T, G, NT, GRAD, true>(B, srow, trow, grow, V, R, L, C, coef, hot)
-                          : final_sweep<T, G, NT, GRAD, false>(B, srow, trow, grow, V, R, L, C, coef, hot);
+    const FinalConst F = final_const(R, L);
+    const double TV = F.acc ? final_sweep<T, G, NT, GRAD, true>(B, srow, trow, grow, V, F, C, coef, hot)
+                            : final_sweep<T, G, NT, GRAD, false>(B, srow, trow, grow, V, F, C, coef, hot);
 
     int y = z;
     if (C) {
@@ -113,17 +114,13 @@ __global__ __launch_bounds__(NT) void couple_kernel(CoupleParams P) {
         const float m = sh.chunk_a[c];
         return m > 0.0f ? log(static_cast<double>(m)) : -__builtin_huge_val();
       });
-      const float invS = static_cast<float>(1.0 / R.sum_s);
-      const float laml = L.lam * LOG2E;
-      const float Al = static_cast<float>(L.A * static_cast<double>(LOG2E));
       // a residual that rounds to zero everywhere in float (lambda* x within
       // rounding of A*) leaves no chunk with mass; the proposal is kept then
       if (c1 < nch) {
         const int yc = elem_race<NT>(B, c1, V, P.seed, RES_ELEM, g, [&](int v) {
           float p;
           const float sv = Loader<T>::load1(srow + v), tv = Loader<T>::load1(trow + v);
-          const float w = acc ? res_weight<true>(sv, tv, R.ms, invS, L.c, laml, Al, &p)
-                              : res_weight<false>(sv, tv, R.ms, invS, L.c, laml, Al, &p);
+          const float w = F.acc ? res_weight<true>(sv, tv, F, &p) : res_weight<false>(sv, tv, F, &p);
           return w > 0.0f ? flog2(w) * LN2 : -finf();
         });
         if (yc < V) y = yc;
@@ -134,8 +131,7 @@ __global__ __launch_bounds__(NT) void couple_kernel(CoupleParams P) {
       const float sy = Loader<T>::load1(srow + y), ty = Loader<T>::load1(trow + y);
       const double logp_y = static_cast<double>(sy) - R.lse_s;
       const double logt_y = static_cast<double>(ty) - R.lse_t;
-      const double xy = (static_cast<double>(ty) - static_cast<double>(sy)) - static_cast<double>(L.c);
-      const double logq_y = logp_y + static_cast<double>(L.lam) * xy - L.A;
+      const double logq_y = logp_y + L.log_ratio(sy, ty);
       const saki_couple_out& o = P.out;
       if (o.lambda) o.lambda[r] = L.lam;
       if (o.kl) o.kl[r] = static_cast<float>(L.KL);
@@ -205,7 +201,7 @@ __device__ void write_skipped(const saki_couple_out& o, int64_t r, int32_t draft
 }
 
 template <typename T>
-__global__ __launch_bounds__(NT) void verify_kernel(VerifyParams P) {
+__global__ __launch_bounds__(NT, WG_PER_CU) void verify_kernel(VerifyParams P) {
   __shared__ RowShared<NT> sh;
   Block<NT> B(sh);
   const int V = P.V;
@@ -237,30 +233,25 @@ __global__ __launch_bounds__(NT) void verify_kernel(VerifyParams P) {
       }
       const LamResult L = lambda_search<T, NT>(B, srow, trow, V, R, P.eps);
       const float sz = Loader<T>::load1(srow + z), tz = Loader<T>::load1(trow + z);
-      const double xz = (static_cast<double>(tz) - static_cast<double>(sz)) - static_cast<double>(L.c);
-      const double alpha = exp(fmin(0.0, static_cast<double>(L.lam) * xz - L.A));
+      const double alpha = exp(fmin(0.0, L.log_ratio(sz, tz)));
       const double u = static_cast<double>(philox_uniform(P.seed, ACCEPT, g, 0));
       const bool accept = u < alpha;
       double TV = __builtin_nan("");
-      const bool acc = L.KL < KL_ACCURATE;
+      const FinalConst F = final_const(R, L);
       if (need_tv || !accept)
-        TV = acc ? final_sweep<T, float, NT, false, true>(B, srow, trow, nullptr, V, R, L, !accept, 0.0f, -1)
-                 : final_sweep<T, float, NT, false, false>(B, srow, trow, nullptr, V, R, L, !accept, 0.0f, -1);
+        TV = F.acc ? final_sweep<T, float, NT, false, true>(B, srow, trow, nullptr, V, F, !accept, 0.0f, -1)
+                   : final_sweep<T, float, NT, false, false>(B, srow, trow, nullptr, V, F, !accept, 0.0f, -1);
       int y = z;
       if (!accept) {
         const int c1 = chunk_race<NT>(B, nch, P.seed, RES_CHUNK, g, [&](int c) {
           const float m = sh.chunk_a[c];
           return m > 0.0f ? log(static_cast<double>(m)) : -__builtin_huge_val();
         });
-        const float invS = static_cast<float>(1.0 / R.sum_s);
-        const float laml = L.lam * LOG2E;
-        const float Al = static_cast<float>(L.A * static_cast<double>(LOG2E));
         if (c1 < nch) {
           const int yc = elem_race<NT>(B, c1, V, P.seed, RES_ELEM, g, [&](int v) {
             float p;
             const float sv = Loader<T>::load1(srow + v), tv = Loader<T>::load1(trow + v);
-          const float w = acc ? res_weight<true>(sv, tv, R.ms, invS, L.c, laml, Al, &p)
-                              : res_weight<false>(sv, tv, R.ms, invS, L.c, laml, Al, &p);
+            const float w = F.acc ? res_weight<true>(sv, tv, F, &p) : res_weight<false>(sv, tv, F, &p);
             return w > 0.0f ? flog2(w) * LN2 : -finf();
           });
           if (yc < V) y = yc;
@@ -270,7 +261,6 @@ __global__ __launch_bounds__(NT) void verify_kernel(VerifyParams P) {
         const float sy = Loader<T>::load1(srow + y), ty = Loader<T>::load1(trow + y);
         const double logp_y = static_cast<double>(sy) - R.lse_s;
         const double logt_y = static_cast<double>(ty) - R.lse_t;
-        const double xy = (static_cast<double>(ty) - static_cast<double>(sy)) - static_cast<double>(L.c);
         if (o.lambda) o.lambda[r] = L.lam;
         if (o.kl) o.kl[r] = static_cast<float>(L.KL);
         if (o.tv) o.tv[r] = static_cast<float>(TV);
@@ -278,7 +268,7 @@ __global__ __launch_bounds__(NT) void verify_kernel(VerifyParams P) {
         if (o.margin) o.margin[r] = static_cast<float>(fabs(u - alpha));
         if (o.logp_token) o.logp_token[r] = static_cast<float>(logp_y);
         if (o.logt_token) o.logt_token[r] = static_cast<float>(logt_y);
-        if (o.logq_token) o.logq_token[r] = static_cast<float>(logp_y + static_cast<double>(L.lam) * xy - L.A);
+        if (o.logq_token) o.logq_token[r] = static_cast<float>(logp_y + L.log_ratio(sy, ty));
         if (o.proposal) o.proposal[r] = z;
         if (o.token) o.token[r] = y;
         if (o.teacher_argmax) o.teacher_argmax[r] = R.vstar;
@@ -353,7 +343,7 @@ __device__ __forceinline__ void lse_chunk(const T* srow, int V, int c, int lane,
 }
 
 template <typename T, typename G, bool GRAD>
-__global__ __launch_bounds__(NT) void route_kernel(RouteParams P) {
+__global__ __launch_bounds__(NT, WG_PER_CU) void route_kernel(RouteParams P) {
   __shared__ RowShared<NT> sh;
   Block<NT> B(sh);
   constexpr int NW = NT / WAVE;
