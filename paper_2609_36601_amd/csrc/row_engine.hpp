@@ -183,18 +183,23 @@ struct StatsAcc {
   double Ss, St;                // per-lane sums of exp(s - Ms), exp(t - Mt)
   float S1, S2, S3, S4;         // per-lane p-weighted powers of d (relative to Ms)
   float T1;                     // per-lane pi-weighted sum of d (relative to Mt)
-  float tbest;                  // wave-uniform running max of t ...
-  int tidx;                     // ... and its lowest index
+  int tidx;                     // wave-uniform lowest index of the running max of t
   float dmin, dmax;             // per-lane range of d
   __device__ void init() {
     Ms = -finf(); Mt = -finf();
     Ss = St = 0.0;
     S1 = S2 = S3 = S4 = T1 = 0.f;
-    tbest = -finf(); tidx = 0x7fffffff;
+    tidx = 0x7fffffff;
     dmin = finf(); dmax = -finf();
   }
 };
 
+// Exponents are taken relative to the wave's running maxima Ms, Mt, so the
+// common chunk needs no cross-lane step before its exp2: only a chunk that
+// raises a running maximum (the wave's first chunk, then rarely) reduces it
+// over the wave and rescales the sums.  The arguments (x - M) log2(e) have
+// an exact subtraction, so the largest terms carry no rounding from the shift.
+// The proposal mass of chunk c is kept as (Ms, sum_c exp(s - Ms)).
 template <bool TAIL>
 __device__ __forceinline__ void stats_math(const float* s, const float* t, uint32_t vm, int c,
                                            int lane, bool keep_chunks, float* ca, float* cb,
@@ -210,27 +215,36 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
       lmax = fmaxf(lmax, d);
     }
   }
-  const float cms = wave_max(ls), cmt = wave_max(lt);
   a.dmin = fminf(a.dmin, lmin);
   a.dmax = fmaxf(a.dmax, lmax);
-  if (cmt > a.tbest) {
-    // a new running maximum of t (wave-uniform, rare): its lowest index here
+  if (wave_any(ls > a.Ms)) {
+    const float cms = wave_max(ls);
+    const float f = fexp2((a.Ms - cms) * LOG2E);
+    a.Ss *= static_cast<double>(f);
+    a.S1 *= f; a.S2 *= f; a.S3 *= f; a.S4 *= f;
+    a.Ms = cms;
+  }
+  if (wave_any(lt > a.Mt)) {
+    // a new running maximum of t: its lowest index in this chunk
+    const float cmt = wave_max(lt);
     int li = 0x7fffffff;
 #pragma unroll
     for (int e = EPL - 1; e >= 0; --e)
       if (SAKI_VALID(e) && t[e] == cmt) li = c * CHUNK + elem_offset(lane, e);
     a.tidx = wave_min(li);
-    a.tbest = cmt;
+    const float f = fexp2((a.Mt - cmt) * LOG2E);
+    a.St *= static_cast<double>(f);
+    a.T1 *= f;
+    a.Mt = cmt;
   }
-  // exponent arguments as (x - max) log2(e): the subtraction is exact, so the
-  // largest terms carry no rounding from the shift.  Normalisers: float sums
-  // of four entries (within three roundings each), then double.
+  // normalisers: float sums of four entries (within three roundings each),
+  // then double
   double ps = 0.0, pt = 0.0;
   float gs = 0.f, gt = 0.f, p1 = 0.f, p2 = 0.f, p3 = 0.f, p4 = 0.f, t1 = 0.f;
 #pragma unroll
   for (int e = 0; e < EPL; ++e) {
-    float es = fexp2((s[e] - cms) * LOG2E);
-    float et = fexp2((t[e] - cmt) * LOG2E);
+    float es = fexp2((s[e] - a.Ms) * LOG2E);
+    float et = fexp2((t[e] - a.Mt) * LOG2E);
     if (TAIL && !SAKI_VALID(e)) { es = 0.f; et = 0.f; }
     const float d = t[e] - s[e];
     const float ed = es * d;
@@ -253,34 +267,17 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
   if (keep_chunks) {
     const float csum = static_cast<float>(wave_sum(ps));
     if (lane == 0) {
-      *ca = cms;
+      *ca = a.Ms;
       *cb = csum;
     }
   }
-  // fold this chunk into the wave's running sums (all lanes share Ms, Mt)
-  if (cms > a.Ms) {
-    const float f = fexp2((a.Ms - cms) * LOG2E);
-    a.Ss *= static_cast<double>(f);
-    a.S1 *= f; a.S2 *= f; a.S3 *= f; a.S4 *= f;
-    a.Ms = cms;
-  }
-  if (cmt > a.Mt) {
-    const float f = fexp2((a.Mt - cmt) * LOG2E);
-    a.St *= static_cast<double>(f);
-    a.T1 *= f;
-    a.Mt = cmt;
-  }
-  // chunks below the running maximum are rescaled; the chunk holding the
-  // maximum is added unscaled (factor exactly 1)
-  const float gS = (cms == a.Ms) ? 1.0f : fexp2((cms - a.Ms) * LOG2E);
-  const float gT = (cmt == a.Mt) ? 1.0f : fexp2((cmt - a.Mt) * LOG2E);
-  a.Ss += ps * static_cast<double>(gS);
-  a.S1 = fmaf(p1, gS, a.S1);
-  a.S2 = fmaf(p2, gS, a.S2);
-  a.S3 = fmaf(p3, gS, a.S3);
-  a.S4 = fmaf(p4, gS, a.S4);
-  a.St += pt * static_cast<double>(gT);
-  a.T1 = fmaf(t1, gT, a.T1);
+  a.Ss += ps;
+  a.S1 += p1;
+  a.S2 += p2;
+  a.S3 += p3;
+  a.S4 += p4;
+  a.St += pt;
+  a.T1 += t1;
 }
 
 // The block's maxima, rescaled sums, argmax and range of d.
@@ -305,7 +302,7 @@ __device__ StatsBlock stats_combine_block(Block<NT, SH>& B, StatsAcc& a) {
                  static_cast<double>(a.T1) * gt};
   B.sum(v);
   O.Ss = v[0]; O.S1 = v[1]; O.S2 = v[2]; O.S3 = v[3]; O.S4 = v[4]; O.St = v[5]; O.T1 = v[6];
-  float tb = a.tbest;
+  float tb = a.Mt;
   int ti = a.tidx;
   B.argmax(tb, ti);
   O.tbest = tb;
