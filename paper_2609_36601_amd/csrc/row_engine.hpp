@@ -39,18 +39,16 @@ struct RowStats {
   double sum_s;        // sum exp(s - ms)
   float c;             // centring constant: E_p[d] rounded to float
   float cL;            // c log2(e) rounded to float; X = fma(d, log2 e, -cL)
+  double mean_p;       // E_p[d]
   double var;          // Var_p[d] = kappa_2 (starting point of the lambda search)
   double k3, k4;       // third and fourth cumulants of d under p
+  double mean_pi;      // E_pi[d]
+  double var_pi;       // Var_pi[d]
   double kl1_est;      // KL(pi || p) = E_pi[d] - (lse_t - lse_s), a first estimate
   float dmin, dmax;    // range of d = t - s
   float tmax;          // max t
   int vstar;           // argmax t, lowest index on ties
   bool finite;
-};
-
-// Result of one lambda evaluation.
-struct LamEval {
-  double lam, A, Eq, Var, KL, KLp;
 };
 
 template <int NT, typename SH = RowShared<NT>>
@@ -182,13 +180,13 @@ struct StatsAcc {
   float Ms, Mt;                 // wave-uniform running maxima of s and t
   double Ss, St;                // per-lane sums of exp(s - Ms), exp(t - Mt)
   float S1, S2, S3, S4;         // per-lane p-weighted powers of d (relative to Ms)
-  float T1;                     // per-lane pi-weighted sum of d (relative to Mt)
+  float T1, T2;                 // per-lane pi-weighted sums of d, d^2 (relative to Mt)
   int tidx;                     // wave-uniform lowest index of the running max of t
   float dmin, dmax;             // per-lane range of d
   __device__ void init() {
     Ms = -finf(); Mt = -finf();
     Ss = St = 0.0;
-    S1 = S2 = S3 = S4 = T1 = 0.f;
+    S1 = S2 = S3 = S4 = T1 = T2 = 0.f;
     tidx = 0x7fffffff;
     dmin = finf(); dmax = -finf();
   }
@@ -235,12 +233,13 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
     const float f = fexp2((a.Mt - cmt) * LOG2E);
     a.St *= static_cast<double>(f);
     a.T1 *= f;
+    a.T2 *= f;
     a.Mt = cmt;
   }
   // normalisers: float sums of four entries (within three roundings each),
   // then double
   double ps = 0.0, pt = 0.0;
-  float gs = 0.f, gt = 0.f, p1 = 0.f, p2 = 0.f, p3 = 0.f, p4 = 0.f, t1 = 0.f;
+  float gs = 0.f, gt = 0.f, p1 = 0.f, p2 = 0.f, p3 = 0.f, p4 = 0.f, t1 = 0.f, t2 = 0.f;
 #pragma unroll
   for (int e = 0; e < EPL; ++e) {
     float es = fexp2((s[e] - a.Ms) * LOG2E);
@@ -254,7 +253,9 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
     p2 += ed2;
     p3 += ed3;
     p4 = fmaf(ed3, d, p4);
-    t1 = fmaf(et, d, t1);
+    const float etd = et * d;
+    t1 += etd;
+    t2 = fmaf(etd, d, t2);
     gs += es;
     gt += et;
     if ((e & 3) == 3) {
@@ -278,12 +279,13 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
   a.S4 += p4;
   a.St += pt;
   a.T1 += t1;
+  a.T2 += t2;
 }
 
 // The block's maxima, rescaled sums, argmax and range of d.
 struct StatsBlock {
   float ms, mt;
-  double Ss, S1, S2, S3, S4, St, T1;
+  double Ss, S1, S2, S3, S4, St, T1, T2;
   float tbest;
   int tidx;
   float dmin, dmax;
@@ -297,11 +299,11 @@ __device__ StatsBlock stats_combine_block(Block<NT, SH>& B, StatsAcc& a) {
   // rescale each wave's sums to the block maxima, then add in a fixed order
   const double gs = (a.Ms == -finf()) ? 0.0 : (a.Ms == O.ms) ? 1.0 : static_cast<double>(fexp2((a.Ms - O.ms) * LOG2E));
   const double gt = (a.Mt == -finf()) ? 0.0 : (a.Mt == O.mt) ? 1.0 : static_cast<double>(fexp2((a.Mt - O.mt) * LOG2E));
-  double v[7] = {a.Ss * gs, static_cast<double>(a.S1) * gs, static_cast<double>(a.S2) * gs,
+  double v[8] = {a.Ss * gs, static_cast<double>(a.S1) * gs, static_cast<double>(a.S2) * gs,
                  static_cast<double>(a.S3) * gs, static_cast<double>(a.S4) * gs, a.St * gt,
-                 static_cast<double>(a.T1) * gt};
+                 static_cast<double>(a.T1) * gt, static_cast<double>(a.T2) * gt};
   B.sum(v);
-  O.Ss = v[0]; O.S1 = v[1]; O.S2 = v[2]; O.S3 = v[3]; O.S4 = v[4]; O.St = v[5]; O.T1 = v[6];
+  O.Ss = v[0]; O.S1 = v[1]; O.S2 = v[2]; O.S3 = v[3]; O.S4 = v[4]; O.St = v[5]; O.T1 = v[6]; O.T2 = v[7];
   float tb = a.Mt;
   int ti = a.tidx;
   B.argmax(tb, ti);
@@ -328,7 +330,10 @@ __device__ inline RowStats row_stats_from(const StatsBlock& O) {
   R.var = fmax(E2 - Ed * Ed, 0.0);
   R.k3 = E3 - 3.0 * Ed * E2 + 2.0 * Ed * Ed * Ed;
   R.k4 = (E4 - 4.0 * Ed * E3 + 6.0 * Ed * Ed * E2 - 3.0 * Ed * Ed * Ed * Ed) - 3.0 * R.var * R.var;
-  R.kl1_est = O.T1 / O.St - (R.lse_t - R.lse_s);
+  R.mean_p = Ed;
+  R.mean_pi = O.T1 / O.St;
+  R.var_pi = fmax(O.T2 / O.St - R.mean_pi * R.mean_pi, 0.0);
+  R.kl1_est = R.mean_pi - (R.lse_t - R.lse_s);
   R.c = static_cast<float>(Ed);
   if (!isfinite(R.c)) R.c = 0.0f;
   R.cL = R.c * LOG2E;
@@ -352,14 +357,14 @@ __device__ RowStats stats_sweep(Block<NT>& B, const T* srow, const T* trow, int 
 }
 
 // ---------------------------------------------------------------------------
-// Lambda sweep: sums at three nodes lam_j = base + j step.  For node j the
-// weights are w_v = p~_v 2^{lam_j X_v}, p~_v = 2^{a_v}, a_v = (s_v - ms) log2 e.
-// The sums kept are W_j = sum (w - p~) (so that A = log1p(W_j / sum p~) keeps
-// its relative precision when A is small), S1_j = sum w X, S2_j = sum w X^2.
-//   FAST: w_0 = 2^{a + base X}, r = 2^{step X}, w_1 = w_0 r, w_2 = w_1 r
-//         (two exp2 for the three nodes; no overflow shifts).
-//   GEN : one exp2 per node, with a shift sigl_j (log2 units) where
-//         lam_j (dmax - c) could overflow float.
+// Lambda sweep: the sums at one node lam over the row.  The weights are
+// w_v = p~_v 2^{lam X_v}, p~_v = 2^{a_v}, a_v = (s_v - ms) log2 e, and the
+// sums kept are W = sum (w - p~) (so that A = log1p(W / sum p~) keeps its
+// relative precision when A is small) and S_k = sum w X^k, k = 1..4, which
+// give A(lam) and its first four derivatives, the cumulants of x under q_lam.
+//   FAST: w = 2^{a + lam X}.
+//   GEN : w = 2^{a + lam X - sigl}, with a shift sigl (log2 units) where
+//         lam (dmax - c) could overflow float.
 //   ACC : w - p~ = p~ expm1(lam x), with expm1 accurate for small arguments
 //         (rows whose KL is small).
 // ---------------------------------------------------------------------------
@@ -379,132 +384,103 @@ __device__ __forceinline__ float expm1_sel(float y, float e) {
   return (fabsf(y) < 0.0625f) ? poly : em;
 }
 
-struct LamNodes {
-  float base, step;  // nodes lam_j = base + j step, exact in float
-  float sigl[3];     // GEN: per-node overflow shift (log2 units), else 0
+// A(lam) and its derivatives (natural units), and KL = lam A' - A.
+struct LamEval {
+  double lam, A, A1, A2, A3, A4, KL;
 };
 
 template <int MODE, bool TAIL>
 __device__ __forceinline__ void lam_math(const float* s, const float* t, uint32_t vm, float ms,
-                                         float cL, const LamNodes& N, double (&W)[3],
-                                         double (&S1)[3], double (&S2)[3]) {
-  float w_[3] = {0.f, 0.f, 0.f}, a_[3] = {0.f, 0.f, 0.f}, q_[3] = {0.f, 0.f, 0.f};
-  const float lam[3] = {N.base, N.base + N.step, N.base + 2.0f * N.step};
+                                         float cL, float lam, float sigl, double (&acc)[5]) {
+  float W = 0.f, S1 = 0.f, S2 = 0.f, S3 = 0.f, S4 = 0.f;
 #pragma unroll
   for (int e = 0; e < EPL; ++e) {
     const float a = (s[e] - ms) * LOG2E;
     float pt = fexp2(a);
     const float X = fmaf(t[e] - s[e], LOG2E, -cL);
-    float w[3], u[3];
+    float w, u;
     if (MODE == LAM_FAST) {
-      w[0] = fexp2(fmaf(N.base, X, a));
-      const float r = fexp2(N.step * X);
-      if (TAIL && !SAKI_VALID(e)) { pt = 0.f; w[0] = 0.f; }
-      w[1] = w[0] * r;
-      w[2] = w[1] * r;
-#pragma unroll
-      for (int j = 0; j < 3; ++j) u[j] = w[j] - pt;
+      w = fexp2(fmaf(lam, X, a));
+      u = w - pt;
     } else if (MODE == LAM_GEN) {
-#pragma unroll
-      for (int j = 0; j < 3; ++j) {
-        w[j] = fexp2(fmaf(lam[j], X, a) - N.sigl[j]);
-        u[j] = (N.sigl[j] == 0.f) ? (w[j] - pt) : w[j];
-        if (TAIL && !SAKI_VALID(e)) { w[j] = 0.f; u[j] = 0.f; }
-      }
+      w = fexp2(fmaf(lam, X, a) - sigl);
+      u = (sigl == 0.f) ? (w - pt) : w;
     } else {
-#pragma unroll
-      for (int j = 0; j < 3; ++j) {
-        const float yl = lam[j] * X;
-        const float ee = fexp2(yl);
-        w[j] = pt * ee;
-        u[j] = pt * expm1_sel(yl * LN2, ee);
-        if (TAIL && !SAKI_VALID(e)) { w[j] = 0.f; u[j] = 0.f; }
-      }
+      const float yl = lam * X;
+      const float ee = fexp2(yl);
+      w = pt * ee;
+      u = pt * expm1_sel(yl * LN2, ee);
     }
-#pragma unroll
-    for (int j = 0; j < 3; ++j) {
-      const float wx = w[j] * X;
-      w_[j] += u[j];
-      a_[j] += wx;
-      q_[j] = fmaf(wx, X, q_[j]);
-    }
+    if (TAIL && !SAKI_VALID(e)) { w = 0.f; u = 0.f; }
+    const float wx = w * X;
+    const float wx2 = wx * X;
+    const float wx3 = wx2 * X;
+    W += u;
+    S1 += wx;
+    S2 += wx2;
+    S3 += wx3;
+    S4 = fmaf(wx3, X, S4);
   }
-#pragma unroll
-  for (int j = 0; j < 3; ++j) {
-    W[j] += static_cast<double>(w_[j]);
-    S1[j] += static_cast<double>(a_[j]);
-    S2[j] += static_cast<double>(q_[j]);
-  }
+  acc[0] += static_cast<double>(W);
+  acc[1] += static_cast<double>(S1);
+  acc[2] += static_cast<double>(S2);
+  acc[3] += static_cast<double>(S3);
+  acc[4] += static_cast<double>(S4);
 }
 
-// A, A', A'' (natural units), KL and KL' at the nodes from the row sums
-// v = {W_j, S1_j, S2_j} and b0 = sum p~.
-__device__ __forceinline__ void lam_finish(const double* v, double b0, const LamNodes& N,
-                                           LamEval (&out)[3]) {
-#pragma unroll
-  for (int j = 0; j < 3; ++j) {
-    const double w = v[3 * j], s1 = v[3 * j + 1], s2 = v[3 * j + 2];
-    LamEval& E = out[j];
-    E.lam = static_cast<double>(N.base) + j * static_cast<double>(N.step);
-    double S0;
-    if (N.sigl[j] == 0.f) {
-      S0 = b0 + w;
-      E.A = log1p(w / b0);
-    } else {
-      // sigl is in log2 units: the shift in natural units is sigl ln 2
-      S0 = w;
-      E.A = static_cast<double>(N.sigl[j]) * LN2_D + log(w / b0);
-    }
-    const double m1 = s1 / S0;  // E_q[X]
-    E.Eq = m1 * LN2_D;
-    E.Var = fmax(s2 / S0 - m1 * m1, 0.0) * (LN2_D * LN2_D);
-    E.KL = fmax(E.lam * E.Eq - E.A, 0.0);  // non-negative; rounding can give -1e-16 when p ~ pi
-    E.KLp = E.lam * E.Var;
+// A and its derivatives at lam from the row sums v = {W, S1..S4} (log2
+// units) and b0 = sum p~.
+__device__ inline LamEval lam_finish(const double (&v)[5], double b0, float lam, float sigl) {
+  LamEval E;
+  E.lam = lam;
+  double S0;
+  if (sigl == 0.f) {
+    S0 = b0 + v[0];
+    E.A = log1p(v[0] / b0);
+  } else {
+    // sigl is in log2 units: the shift in natural units is sigl ln 2
+    S0 = v[0];
+    E.A = static_cast<double>(sigl) * LN2_D + log(v[0] / b0);
   }
+  // raw moments of X under q, then its cumulants; x = X ln 2
+  const double m1 = v[1] / S0, m2 = v[2] / S0, m3 = v[3] / S0, m4 = v[4] / S0;
+  const double c2 = fmax(m2 - m1 * m1, 0.0);
+  const double c3 = m3 - 3.0 * m1 * m2 + 2.0 * m1 * m1 * m1;
+  const double c4 = m4 - 4.0 * m1 * m3 + 6.0 * m1 * m1 * m2 - 3.0 * m1 * m1 * m1 * m1 - 3.0 * c2 * c2;
+  const double l1 = LN2_D, l2 = l1 * l1;
+  E.A1 = m1 * l1;
+  E.A2 = c2 * l2;
+  E.A3 = c3 * l2 * l1;
+  E.A4 = c4 * l2 * l2;
+  E.KL = fmax(E.lam * E.A1 - E.A, 0.0);  // non-negative; rounding can give -1e-16 when p ~ pi
+  return E;
 }
 
 template <typename T, int NT, int MODE>
-__device__ void lam_sweep_mode(Block<NT>& B, const T* srow, const T* trow, int V, const RowStats& R,
-                               const LamNodes& N, LamEval (&out)[3]) {
+__device__ LamEval lam_sweep_mode(Block<NT>& B, const T* srow, const T* trow, int V, const RowStats& R,
+                                  float lam, float sigl) {
   constexpr int NW = NT / WAVE;
-  double W[3] = {0, 0, 0}, S1[3] = {0, 0, 0}, S2[3] = {0, 0, 0};
+  double v[5] = {0, 0, 0, 0, 0};
   for_chunks<T, NW>(srow, trow, V, B.wave, B.lane,
                     [&](auto tail, const float* s, const float* t, uint32_t vm, int c) {
                       constexpr bool TAIL = decltype(tail)::value;
-                      lam_math<MODE, TAIL>(s, t, vm, R.ms, R.cL, N, W, S1, S2);
+                      lam_math<MODE, TAIL>(s, t, vm, R.ms, R.cL, lam, sigl, v);
                     });
-  double v[9];
-#pragma unroll
-  for (int j = 0; j < 3; ++j) { v[3 * j] = W[j]; v[3 * j + 1] = S1[j]; v[3 * j + 2] = S2[j]; }
   B.sum(v);
-  lam_finish(v, R.sum_s, N, out);
+  return lam_finish(v, R.sum_s, lam, sigl);
 }
 
-// Evaluates the nodes base + j step (j = 0, 1, 2) over the whole row; acc
-// selects the expm1 form.  Every thread gets the same E.
+// Evaluates A and its derivatives at lam over the whole row; acc selects the
+// expm1 form.  Every thread gets the same result.
 template <typename T, int NT>
-__device__ void lam_sweep(Block<NT>& B, const T* srow, const T* trow, int V, const RowStats& R,
-                          float base, float step, bool acc, LamEval (&E)[3]) {
-  LamNodes N;
-  N.base = base;
-  N.step = step;
-  N.sigl[0] = N.sigl[1] = N.sigl[2] = 0.f;
-  const double top = static_cast<double>(R.dmax) - R.c;  // largest x
-  const double lam2 = static_cast<double>(base) + 2.0 * step;
-  if (acc) {
-    lam_sweep_mode<T, NT, LAM_ACC>(B, srow, trow, V, R, N, E);
-  } else if (lam2 * top <= 60.0 && static_cast<double>(step) * top <= 20.0) {
-    // no weight can overflow, and where a node-0 weight underflows the node 1
-    // and 2 weights are below 2^-60 of the row sum
-    lam_sweep_mode<T, NT, LAM_FAST>(B, srow, trow, V, R, N, E);
-  } else {
-    // keep lam_j x - sig_j <= 60 (natural units) for every entry
-    for (int j = 0; j < 3; ++j) {
-      const double tj = (static_cast<double>(base) + j * static_cast<double>(step)) * top;
-      N.sigl[j] = (tj > 60.0) ? static_cast<float>((tj - 60.0) * static_cast<double>(LOG2E)) : 0.0f;
-    }
-    lam_sweep_mode<T, NT, LAM_GEN>(B, srow, trow, V, R, N, E);
-  }
+__device__ LamEval lam_sweep(Block<NT>& B, const T* srow, const T* trow, int V, const RowStats& R,
+                             float lam, bool acc) {
+  const double top = static_cast<double>(lam) * (static_cast<double>(R.dmax) - R.c);  // largest lam x
+  if (acc) return lam_sweep_mode<T, NT, LAM_ACC>(B, srow, trow, V, R, lam, 0.0f);
+  if (top <= 60.0) return lam_sweep_mode<T, NT, LAM_FAST>(B, srow, trow, V, R, lam, 0.0f);
+  // keep lam x - sig <= 60 (natural units) for every entry
+  const float sigl = static_cast<float>((top - 60.0) * static_cast<double>(LOG2E));
+  return lam_sweep_mode<T, NT, LAM_GEN>(B, srow, trow, V, R, lam, sigl);
 }
 
 // Rows whose KL (the radius, or KL(pi||p) at the teacher endpoint) is below
@@ -530,79 +506,31 @@ struct LamResult {
   }
 };
 
-// Degree-8 Hermite interpolant of A(lambda) through three nodes carrying
-// A, A' and A'' (Newton divided differences with each node repeated three
-// times).  KL(lambda) = lambda A'(lambda) - A(lambda) on the interpolant.
-struct Hermite3 {
-  double z[9], a[9];
-  __device__ void build(const LamEval (&E)[3]) {
-    // in-place divided differences; order 1 and 2 differences over a repeated
-    // node are A' and A'' / 2 at that node
-#pragma unroll
-    for (int i = 0; i < 9; ++i) {
-      z[i] = E[i / 3].lam;
-      a[i] = E[i / 3].A;
-    }
-#pragma unroll
-    for (int j = 1; j < 9; ++j) {
-#pragma unroll
-      for (int i = 8; i >= j; --i) {
-        if (i / 3 == (i - j) / 3) {
-          a[i] = (j == 1) ? E[i / 3].Eq : 0.5 * E[i / 3].Var;
-        } else {
-          a[i] = (a[i] - a[i - 1]) / (z[i] - z[i - j]);
-        }
-      }
-    }
+// Quartic Taylor model of A around a node: A(l) ~ sum_k A_k (l - lam)^k / k!,
+// and KL(l) = l A'(l) - A(l) on it.
+struct TaylorA {
+  LamEval n;
+  __device__ void eval(double l, double& A, double& Ap) const {
+    const double d = l - n.lam;
+    A = n.A + d * (n.A1 + d * (0.5 * n.A2 + d * (n.A3 / 6.0 + d * (n.A4 / 24.0))));
+    Ap = n.A1 + d * (n.A2 + d * (0.5 * n.A3 + d * (n.A4 / 6.0)));
   }
-  // A, A', A'' at l
-  __device__ void eval(double l, double& p0, double& p1, double& p2) const {
-    double p = a[8], dp = 0.0, ddp = 0.0;
-#pragma unroll
-    for (int j = 7; j >= 0; --j) {
-      const double h = l - z[j];
-      ddp = ddp * h + 2.0 * dp;
-      dp = dp * h + p;
-      p = p * h + a[j];
-    }
-    p0 = p; p1 = dp; p2 = ddp;
+  __device__ double kl(double l) const {
+    double A, Ap;
+    eval(l, A, Ap);
+    return l * Ap - A;
   }
-  // size of d/dl (l T'(l) - T(l)) for the top Newton term T: an estimate of
-  // the interpolant's truncation error in KL at l
-  __device__ double top_term(double l) const {
-    double prod = a[8], dprod = 0.0;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const double h = l - z[j];
-      dprod = dprod * h + prod;
-      prod = prod * h;
-    }
-    return fabs(l * dprod - prod);
-  }
-  // root of lambda A' - A = eps in [lo, hi], where KL(lo) <= eps < KL(hi):
-  // safeguarded Newton from the secant point; stops once the step is below
-  // 1e-13 relative (far under the float resolution lambda* is returned in)
-  __device__ double solve(double eps, double lo, double hi, double flo, double fhi) const {
-    double l = (flo < 0 && fhi > 0) ? lo + (hi - lo) * (-flo / (fhi - flo)) : 0.5 * (lo + hi);
-    for (int it = 0; it < 40; ++it) {
-      double A0, A1, A2;
-      eval(l, A0, A1, A2);
-      const double f = l * A1 - A0 - eps;
-      if (f == 0.0) break;
-      if (f < 0) lo = l; else hi = l;
-      const double fp = l * A2;
-      double nl = (fp > 0) ? l - f / fp : 0.5 * (lo + hi);
-      if (!(nl > lo && nl < hi)) nl = 0.5 * (lo + hi);
-      const bool done = fabs(nl - l) <= 1e-13 * l || (hi - lo) <= 1e-13 * l;
-      l = nl;
-      if (done) break;
-    }
-    return l;
+  __device__ bool usable() const {
+    return isfinite(n.A) && isfinite(n.A1) && isfinite(n.A2) && isfinite(n.A3) && isfinite(n.A4);
   }
 };
 
-// Start of the search from the cumulants of d under p:
-// KL(lam) = sum_n (n - 1) kappa_n lam^n / n! ~ k2 lam^2/2 + k3 lam^3/3 + k4 lam^4/8.
+// Starting points of the search.  Cumulant start: KL(lam) = sum_n (n - 1)
+// kappa_n lam^n / n! ~ k2 lam^2/2 + k3 lam^3/3 + k4 lam^4/8 with the
+// cumulants of d under p.  Two-ended start: the degree-7 polynomial A(lam)
+// with A(0) = 0, A^(k)(0) = kappa_k (k = 1..4, of x = d - c under p) and
+// A(1) = lse_t - lse_s - c, A'(1) = E_pi[x], A''(1) = Var_pi(x) at the teacher
+// end; KL = eps is solved on it by bisection.
 __device__ inline double cumulant_start(const RowStats& R, double eps) {
   if (!(R.var > 0)) return 0.5;
   const double l2 = sqrt(2.0 * eps / R.var);
@@ -618,17 +546,45 @@ __device__ inline double cumulant_start(const RowStats& R, double eps) {
   return l;
 }
 
+__device__ inline double two_ended_start(const RowStats& R, double eps) {
+  double c[8];
+  c[0] = 0.0;
+  c[1] = R.mean_p - R.c;
+  c[2] = R.var / 2.0;
+  c[3] = R.k3 / 6.0;
+  c[4] = R.k4 / 24.0;
+  const double a1 = R.lse_t - R.lse_s - R.c, d1 = R.mean_pi - R.c, dd1 = R.var_pi;
+  const double r0 = a1 - (c[1] + c[2] + c[3] + c[4]);
+  const double r1 = d1 - (c[1] + 2.0 * c[2] + 3.0 * c[3] + 4.0 * c[4]);
+  const double r2 = dd1 - (2.0 * c[2] + 6.0 * c[3] + 12.0 * c[4]);
+  c[5] = 0.5 * (42.0 * r0 - 12.0 * r1 + r2);
+  c[6] = 0.5 * (-70.0 * r0 + 22.0 * r1 - 2.0 * r2);
+  c[7] = 0.5 * (30.0 * r0 - 10.0 * r1 + r2);
+  auto kl = [&](double l) {
+    double v = 0.0;
+#pragma unroll
+    for (int j = 7; j >= 2; --j) v = (v + (j - 1) * c[j]) * l;
+    return v * l;
+  };
+  if (!(kl(1.0) > eps)) return -1.0;
+  double lo = 0.0, hi = 1.0;
+  for (int it = 0; it < 50; ++it) {
+    const double m = 0.5 * (lo + hi);
+    if (kl(m) <= eps) lo = m; else hi = m;
+  }
+  return lo;
+}
+
 // Largest lambda in [0, 1] with KL(q_lambda || p) <= eps (Eq. trust_region).
-// Each lambda sweep evaluates an evenly spaced three-node stencil
-// {c - h, c, c + h} (shifted below 1 when it would pass the teacher
-// endpoint).  base and step are multiples of q = 2^(floor(log2 c) - 19), so
-// the nodes are exact in float and the endpoint node is exactly 1.  When the
-// nodes bracket the root, the Hermite interpolant of A gives lambda* and
-// A(lambda*); its top Newton term bounds the truncation error, and a stencil
-// whose estimate exceeds HERMITE_TOL * eps is followed by a tight +-2% one.
-// sweep3(base, step, acc, E) evaluates the three nodes over the whole row.
-template <typename Sweep3>
-__device__ LamResult lambda_search_with(const RowStats& R, double eps, Sweep3&& sweep3) {
+// Each sweep evaluates A and its first four derivatives at one node; KL = eps
+// is then solved on the quartic Taylor model around the node, inside the
+// bracket [lo, hi] of evaluated nodes and within 30% of the node.  The root
+// is accepted when five times the model's last term is below TAYLOR_TOL eps
+// (the next term is smaller by about |l - node| times the cumulant growth);
+// otherwise the next node is that root (or the edge of the trust interval).
+// sweep1(lam, acc) evaluates one node over the whole row.
+template <typename Sweep1>
+__device__ LamResult lambda_search_with(const RowStats& R, double eps, Sweep1&& sweep1) {
   LamResult out;
   if (R.dmin == R.dmax) {
     // t - s constant: p = pi, KL = 0 for every lambda, lambda* = 1, q = p
@@ -647,86 +603,85 @@ __device__ LamResult lambda_search_with(const RowStats& R, double eps, Sweep3&& 
   // KL of that size.  Its overflow guard needs lam (dmax - c) <= 60.
   const bool acc_ok = (static_cast<double>(R.dmax) - R.c) <= 60.0;
   bool acc = eps < KL_ACCURATE && acc_ok;
-  constexpr double DELTA0 = 0.25;       // first stencil half-width, relative
-  constexpr double DELTA_TIGHT = 0.02;  // refinement stencil half-width
-  constexpr double HERMITE_TOL = 1e-6;  // accepted truncation estimate, relative to eps
+  constexpr double TAYLOR_TOL = 1e-7;
+  constexpr double TRUST = 0.3;
   constexpr double LMAX = 1.0 - 1e-6;
   double lo = 0.0, hi = 1.0;  // KL(lo) <= eps < KL(hi) (hi = 1 until a node above is seen)
   LamEval feas;               // the largest evaluated lambda that is feasible (lambda = 0 is)
   feas.lam = 0.0; feas.A = 0.0; feas.KL = 0.0;
-  double lg = fmin(fmax(cumulant_start(R, eps), 1e-7), LMAX);
-  double delta = DELTA0;
+  const double l_cum = cumulant_start(R, eps);
+  const double l_two = two_ended_start(R, eps);
+  double lg = (l_two > 0.0 && fabs(l_two - l_cum) <= 0.3 * l_cum) ? l_two : l_cum;
+  lg = fmin(fmax(lg, 1e-7), LMAX);
   bool try_one = R.kl1_est <= 1.05 * eps + 1e-5;
   for (int sweep = 0; sweep < 12; ++sweep) {
-    double h = delta * lg;
-    double c0 = lg;
-    if (try_one) {
-      h = delta / (1.0 + delta);
-      c0 = 1.0 - h;
-    } else if (lg + h > 1.0) {
-      h = fmin(h, 0.49);
-      c0 = 1.0 - h;
-    }
-    // nodes on the grid of q = 2^(floor(log2 c0) - 19)
-    int ex;
-    frexp(c0, &ex);
-    const double q = ldexp(1.0, ex - 20);
-    const double step = fmax(rint(h / q), 1.0) * q;
-    double base = rint((c0 - step) / q) * q;
-    if (try_one || base + 2.0 * step > 1.0) base = 1.0 - 2.0 * step;
-    if (!(base > 0.0)) base = step;
-    LamEval E[3];
-    sweep3(static_cast<float>(base), static_cast<float>(step), acc, E);
-    if (E[2].lam == 1.0 && E[2].KL <= eps) {
-      if (!acc && acc_ok && E[2].KL < KL_ACCURATE) {
+    const float lf = try_one ? 1.0f : static_cast<float>(lg);
+    const LamEval E = sweep1(lf, acc);
+    if (lf == 1.0f && E.KL <= eps) {
+      if (!acc && acc_ok && E.KL < KL_ACCURATE) {
         acc = true;  // resolve a small endpoint KL with the accurate form
-        try_one = true;
         continue;
       }
-      out.lam = 1.0f; out.A = E[2].A; out.KL = E[2].KL;
+      out.lam = 1.0f; out.A = E.A; out.KL = E.KL;
       return out;
     }
     try_one = false;
-#pragma unroll
-    for (int j = 0; j < 3; ++j) {
-      if (E[j].KL <= eps) {
-        if (E[j].lam >= lo) { lo = E[j].lam; feas = E[j]; }
-      } else {
-        hi = fmin(hi, E[j].lam);
-      }
+    if (E.KL <= eps) {
+      if (E.lam >= lo) { lo = E.lam; feas = E; }
+    } else {
+      hi = fmin(hi, E.lam);
     }
-    if (E[0].KL <= eps && eps < E[2].KL) {
-      Hermite3 H;
-      H.build(E);
-      const bool k1 = E[1].KL <= eps;
-      const double root = k1 ? H.solve(eps, E[1].lam, E[2].lam, E[1].KL - eps, E[2].KL - eps)
-                             : H.solve(eps, E[0].lam, E[1].lam, E[0].KL - eps, E[1].KL - eps);
-      const bool accurate = H.top_term(root) <= HERMITE_TOL * eps;
-      if (accurate || delta <= 1.05 * DELTA_TIGHT || sweep >= 10) {
-        const float lf = static_cast<float>(root);
-        double A0, A1, A2;
-        H.eval(static_cast<double>(lf), A0, A1, A2);
-        out.lam = lf;
-        out.A = A0;
-        out.KL = fmax(static_cast<double>(lf) * A1 - A0, 0.0);
-        return out;
-      }
-      lg = fmin(root, LMAX);
-      delta = DELTA_TIGHT;
+    TaylorA M;
+    M.n = E;
+    if (!M.usable()) {
+      lg = 0.5 * (lo + hi);
       continue;
     }
-    // root outside the stencil: Newton in log KL from the nearest node
-    const bool above = E[2].KL < eps;
-    const LamEval& n = above ? E[2] : E[0];
-    double g = above ? 0.5 * (n.lam + hi) : 0.5 * (lo + n.lam);
-    if (n.KL > 0 && n.KLp > 0) {
-      const double t = n.lam - (log(n.KL) - log(eps)) * n.KL / n.KLp;
-      if (t > lo && t < hi) g = t;
+    const double a = fmax(lo, E.lam * (1.0 - TRUST)), b = fmin(hi, E.lam * (1.0 + TRUST));
+    const double fa = M.kl(a) - eps, fb = M.kl(b) - eps;
+    if (fa <= 0.0 && fb > 0.0) {
+      // safeguarded Newton on the model inside [a, b]
+      double l = fmin(fmax(E.lam, a), b), xa = a, xb = b;
+      for (int it = 0; it < 60; ++it) {
+        double A, Ap;
+        M.eval(l, A, Ap);
+        const double f = l * Ap - A - eps;
+        if (f == 0.0) break;
+        if (f < 0.0) xa = l; else xb = l;
+        const double dd = l - E.lam;
+        const double fp = l * (E.A2 + dd * (E.A3 + dd * (0.5 * E.A4)));  // l A''
+        double nl = (fp > 0.0) ? l - f / fp : 0.5 * (xa + xb);
+        if (!(nl > xa && nl < xb)) nl = 0.5 * (xa + xb);
+        const bool done = fabs(nl - l) <= 1e-14 * l || (xb - xa) <= 1e-14 * l;
+        l = nl;
+        if (done) break;
+      }
+      const double d = l - E.lam;
+      const double err = 5.0 * fabs(E.A4) * d * d * d * d / 24.0;
+      if (err <= TAYLOR_TOL * eps) {
+        const float lr = static_cast<float>(l);
+        double A, Ap;
+        M.eval(static_cast<double>(lr), A, Ap);
+        out.lam = lr;
+        out.A = A;
+        out.KL = fmax(static_cast<double>(lr) * Ap - A, 0.0);
+        return out;
+      }
+      lg = fmin(fmax(l, 1e-7), LMAX);
+      continue;
     }
-    g = fmin(fmax(g, 1e-7), LMAX);
-    delta = fmin(fmax(fabs(g - n.lam) / g, DELTA_TIGHT), 0.3);
-    lg = g;
-    if (above && E[2].lam < 1.0 && hi >= 1.0) try_one = lg * (1.0 + delta) >= 1.0;
+    // the model's root is outside the trust interval: go to its edge
+    if (fb <= 0.0) {
+      if (b >= 1.0 || E.lam * (1.0 + TRUST) >= 1.0) {
+        try_one = hi >= 1.0;  // the teacher endpoint may be feasible
+        lg = fmin(0.5 * (E.lam + hi), LMAX);
+      } else {
+        lg = b;
+      }
+    } else {
+      lg = a;
+    }
+    lg = fmin(fmax(lg, 1e-7), LMAX);
   }
   // not reached in practice (the bracket shrinks every sweep): keep the
   // largest feasible evaluated lambda
@@ -737,8 +692,8 @@ __device__ LamResult lambda_search_with(const RowStats& R, double eps, Sweep3&& 
 template <typename T, int NT>
 __device__ LamResult lambda_search(Block<NT>& B, const T* srow, const T* trow, int V,
                                    const RowStats& R, double eps) {
-  return lambda_search_with(R, eps, [&](float base, float step, bool acc, LamEval (&E)[3]) {
-    lam_sweep<T, NT>(B, srow, trow, V, R, base, step, acc, E);
+  return lambda_search_with(R, eps, [&](float lam, bool acc) {
+    return lam_sweep<T, NT>(B, srow, trow, V, R, lam, acc);
   });
 }
 
@@ -859,26 +814,19 @@ __device__ void grad_sweep(Block<NT>& B, const T* srow, G* grow, int V, float ms
 // consecutive indices.
 // ---------------------------------------------------------------------------
 
-// Chunk level.  logw(c) returns ln W_c up to a row constant, or -inf.
+// Chunk level.  logw(c) returns ln W_c up to a row constant, or -inf.  One
+// chunk per thread: the double-precision logs dominate, not the Philox block.
 template <int NT, typename F>
 __device__ int chunk_race(Block<NT>& B, int nchunks, uint64_t seed, uint32_t stream, uint64_t g,
                           F logw) {
   double best = __builtin_huge_val();
   int bi = 0x7fffffff;
-  for (int j = B.tid; 4 * j < nchunks; j += NT) {
-    const uint4 w = philox_block(seed, stream, g, static_cast<uint32_t>(j));
-    const uint32_t words[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int c = 4 * j + k;
-      if (c < nchunks) {
-        const double lw = logw(c);
-        if (lw > -__builtin_huge_val()) {
-          const double u = static_cast<double>(word_to_uniform(words[k]));
-          const double key = log(-log(u)) - lw;
-          if (key < best) { best = key; bi = c; }
-        }
-      }
+  for (int c = B.tid; c < nchunks; c += NT) {
+    const double lw = logw(c);
+    if (lw > -__builtin_huge_val()) {
+      const double u = static_cast<double>(philox_uniform(seed, stream, g, static_cast<uint32_t>(c)));
+      const double key = log(-log(u)) - lw;
+      if (key < best) { best = key; bi = c; }
     }
   }
   B.argmin(best, bi);
