@@ -69,8 +69,10 @@ struct Loader<float> {
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(1))) const u32x4 g_cu32x4;
 
+template <bool LAST = false>
 __device__ __forceinline__ uint4 gload16(const void* p) {
-  const u32x4 v = *(g_cu32x4*)(p);
+  // LAST: the data is not read again (non-temporal: no cache allocation)
+  const u32x4 v = LAST ? __builtin_nontemporal_load((g_cu32x4*)(p)) : *(g_cu32x4*)(p);
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
@@ -85,17 +87,17 @@ struct Frag<float> {
   uint4 q[4];
 };
 
-template <typename T>
+template <bool LAST, typename T>
 __device__ __forceinline__ void frag_load(Frag<T>& f, const T* row, int c, int lane) {
   const T* p = row + c * CHUNK + 8 * lane;
   if constexpr (sizeof(T) == 2) {
-    f.q[0] = gload16(p);
-    f.q[1] = gload16(p + 512);
+    f.q[0] = gload16<LAST>(p);
+    f.q[1] = gload16<LAST>(p + 512);
   } else {
-    f.q[0] = gload16(p);
-    f.q[1] = gload16(p + 4);
-    f.q[2] = gload16(p + 512);
-    f.q[3] = gload16(p + 516);
+    f.q[0] = gload16<LAST>(p);
+    f.q[1] = gload16<LAST>(p + 4);
+    f.q[2] = gload16<LAST>(p + 512);
+    f.q[3] = gload16<LAST>(p + 516);
   }
 }
 

@@ -138,21 +138,22 @@ struct Block {
 // Chunk streaming.  body(tail, s, t, vm, c) gets this lane's 16 entries of s
 // and t in chunk c (elem_offset layout) and the valid mask vm; tail is a
 // std::integral_constant<bool, TAIL> (TAIL: the ragged last chunk).  Full
-// chunks are visited with the next chunk's loads already issued.
+// chunks are visited with the next chunk's loads already issued.  LAST marks
+// the row's last pass: its loads do not allocate in the caches.
 // ---------------------------------------------------------------------------
-template <typename T, int NW, typename Body>
+template <typename T, int NW, bool LAST = false, typename Body>
 __device__ __forceinline__ void for_chunks(const T* srow, const T* trow, int V, int wave, int lane,
                                            Body&& body) {
   const int nfull = V / CHUNK;
   if (wave < nfull) {
     Frag<T> fs, ft;
-    frag_load(fs, srow, wave, lane);
-    frag_load(ft, trow, wave, lane);
+    frag_load<LAST>(fs, srow, wave, lane);
+    frag_load<LAST>(ft, trow, wave, lane);
     for (int c = wave; c < nfull; c += NW) {
       Frag<T> ns, nt;
       if (c + NW < nfull) {
-        frag_load(ns, srow, c + NW, lane);
-        frag_load(nt, trow, c + NW, lane);
+        frag_load<LAST>(ns, srow, c + NW, lane);
+        frag_load<LAST>(nt, trow, c + NW, lane);
       }
       float s[EPL], t[EPL];
       frag_unpack(fs, s);
@@ -737,7 +738,7 @@ __device__ double final_sweep(Block<NT>& B, const T* srow, const T* trow, G* gro
   constexpr int NW = NT / WAVE;
   const int hot_chunk = hot >= 0 ? hot / CHUNK : -1;
   double TV = 0;
-  for_chunks<T, NW>(srow, trow, V, B.wave, B.lane,
+  for_chunks<T, NW, true>(srow, trow, V, B.wave, B.lane,
                     [&](auto tail, const float* s, const float* t, uint32_t vm, int c) {
                       constexpr bool TAIL = decltype(tail)::value;
                       float tv = 0.f, g[EPL];
