@@ -17,6 +17,9 @@ routing   routed loss and its gradient (Sec. 3.4, Eq. general_objective,
           App. B, App. H).
 verify    speculative block verification with first-rejection semantics
           (Sec. 3.5, App. F, App. I).
+supervision  teacher-sampled correction targets (App. C) and the Random-TM /
+          TV-Weighted-TM placement controls (Sec. 4.1, placement-control
+          appendix).
 
 Every function works in float64 on the exact input values (bf16 and fp32
 logits convert exactly to float64).

@@ -37,6 +37,9 @@ STREAM_PROP_ELEM = 1    # proposal race, one uniform per vocab id
 STREAM_ACCEPT = 2       # accept test, index 0
 STREAM_RES_CHUNK = 3    # residual race, one uniform per vocab chunk
 STREAM_RES_ELEM = 4     # residual race, one uniform per vocab id
+STREAM_TS_CHUNK = 5     # teacher-sampled target race, one uniform per vocab chunk
+STREAM_TS_ELEM = 6      # teacher-sampled target race, one uniform per vocab id
+STREAM_SELECT = 7       # placement controls, index 0 of each position
 
 
 def philox4(counter, key, word_bits=32, rounds=10):
