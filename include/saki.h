@@ -15,7 +15,10 @@
  *      to the student logits                      (Sec. 3.4, Eq. general_objective, App. H);
  *   5. for speculative blocks of k drafted tokens, commits the longest accepted
  *      prefix and draws the correction at the first rejection
- *                                                 (Sec. 3.5, App. F, App. I).
+ *                                                 (Sec. 3.5, App. F, App. I);
+ *   6. supervision variants: a correction target drawn from the teacher
+ *      instead of its mode (App. C), and the Random-TM / TV-Weighted-TM
+ *      placement controls (Sec. 4.1, placement-control appendix).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -105,6 +108,9 @@ typedef struct {
   int32_t *teacher_argmax;/* v* = argmax_v t_v, lowest index on ties                    */
   uint8_t *corrected;     /* C: 1 if the proposal was rejected                          */
   uint8_t *row_status;    /* SAKI_ROW_*                                                  */
+  int32_t *target;        /* index of the gradient's indicator: y at accepted rows; at a
+                             correction v*, or the teacher draw v~ with
+                             SAKI_TARGET_SAMPLE; -1 at rows without outputs         */
 } saki_couple_out;
 
 /* Routing arguments (Eq. general_objective).  row loss
@@ -112,6 +118,12 @@ typedef struct {
  *   A_r = log pi_T(y_r) - log p(y_r)   (detached advantage, Eq. k1_advantage_token),
  * gradient  g[r, j] = grad_scale * M_r * d l_r / d s[r, j]
  *         = grad_scale * M_r * [ (1 - C_r) * (-A_r) * (1[j = y_r] - p_j) + C_r * (p_j - 1[j = v*_r]) ]. */
+/* Supervision target at corrections (saki_route_args.correction_target). */
+#define SAKI_TARGET_MODE 0   /* v* = argmax t (Eq. teacher_mode_loss)                        */
+#define SAKI_TARGET_SAMPLE 1 /* v~ ~ pi_T, L_TS = -log pi_theta(v~) (App. C, teacher-sampled
+                                supervision): the two-level exponential race of the coupling
+                                on log pi_T with Philox streams 5 (chunks) and 6 (entries)  */
+
 typedef struct {
   const uint8_t *valid_mask; /* M, [n_rows] (0 / non-zero); NULL = every row valid        */
   float grad_scale;          /* the caller's 1 / N_valid over the WHOLE batch (App. H)    */
@@ -120,12 +132,15 @@ typedef struct {
   double *loss_sum;          /* one double: OVERWRITTEN with sum_r grad_scale * l_r, or NULL */
   void *grad;                /* [n_rows, grad_stride] gradient, or NULL (loss only)       */
   int64_t grad_stride;       /* elements between gradient rows, >= vocab                  */
+  int32_t correction_target; /* SAKI_TARGET_MODE or SAKI_TARGET_SAMPLE (saki_couple; the
+                                standalone saki_route_loss takes its targets as input)    */
 } saki_route_args;
 
 /* Operation codes for saki_workspace_bytes. */
 #define SAKI_OP_COUPLE 0
 #define SAKI_OP_ROUTE 1
 #define SAKI_OP_VERIFY 2
+#define SAKI_OP_SELECT 3
 
 /* Bytes of caller workspace that one call of `op` on n_rows rows of `vocab`
  * entries needs (device memory, any contents, 256-byte aligned).  For
@@ -175,6 +190,31 @@ saki_status saki_spec_verify(const saki_rows *in, int32_t k, const int32_t *draf
                              uint64_t seed, int32_t eos_id, int32_t *accepted_len,
                              int32_t *correction, const saki_couple_out *per_pos, void *ws,
                              size_t ws_bytes, saki_stream_t stream);
+
+/* Placement controls (Sec. 4.1; placement-control appendix).  Rows are grouped
+ * into trajectories: trajectory i holds rows [traj_offsets[i], traj_offsets[i+1])
+ * (device int64 array of n_traj + 1 non-decreasing entries in [0, n_rows]; a
+ * trajectory whose range is malformed is skipped and its rows are not written).
+ * For each trajectory with valid rows V_i (valid_mask non-zero, or every row
+ * when valid_mask is NULL), m_i = sum over V_i of corrected, and exactly m_i
+ * rows of V_i get selected = 1, every other row 0:
+ *   SAKI_SELECT_RANDOM       m_i rows of V_i uniformly without replacement;
+ *   SAKI_SELECT_TV_WEIGHTED  m_i rows without replacement with weights tv
+ *                            (keys -log U / tv, the m_i smallest win); when fewer
+ *                            than m_i valid rows have tv > 0, the rest are filled
+ *                            uniformly from the rows with tv = 0 (or NaN).
+ * U is the Philox uniform of stream 7, index 0, of the global row row_offset + r.
+ * Selected rows take the teacher-mode loss and the others keep RKL: pass
+ * `selected` as `corrected` to saki_route_loss.  tv, corrected (uint8) and
+ * selected are [n_rows] device arrays; ws holds one double per row
+ * (saki_workspace_bytes(SAKI_OP_SELECT, n_rows, 0)), 8-byte aligned. */
+#define SAKI_SELECT_RANDOM 0
+#define SAKI_SELECT_TV_WEIGHTED 1
+saki_status saki_select_positions(int32_t mode, int64_t n_traj, int64_t n_rows,
+                                  const int64_t *traj_offsets, const float *tv,
+                                  const uint8_t *corrected, const uint8_t *valid_mask,
+                                  uint64_t seed, int64_t row_offset, uint8_t *selected,
+                                  void *ws, size_t ws_bytes, saki_stream_t stream);
 
 /* Static description of a status code. */
 const char *saki_status_str(saki_status s);

@@ -14,7 +14,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libsaki.so")
 
 SAKI_F32, SAKI_BF16 = 0, 1
-SAKI_OP_COUPLE, SAKI_OP_ROUTE, SAKI_OP_VERIFY = 0, 1, 2
+SAKI_OP_COUPLE, SAKI_OP_ROUTE, SAKI_OP_VERIFY, SAKI_OP_SELECT = 0, 1, 2, 3
+SAKI_TARGET_MODE, SAKI_TARGET_SAMPLE = 0, 1
+SAKI_SELECT_RANDOM, SAKI_SELECT_TV_WEIGHTED = 0, 1
 SAKI_MAX_VOCAB = 1 << 21
 SAKI_CHUNK = 1024
 ROW_OK, ROW_NONFINITE, ROW_BAD_DRAFT, ROW_SKIPPED = 0, 1, 2, 3
@@ -24,7 +26,7 @@ STATUS = {0: "SAKI_OK", 1: "SAKI_E_NULLPTR", 2: "SAKI_E_SHAPE", 3: "SAKI_E_VALUE
           8: "SAKI_E_LAUNCH"}
 
 EXPORTED = ["saki_workspace_bytes", "saki_couple", "saki_route_loss", "saki_spec_verify",
-            "saki_status_str", "saki_last_error"]
+            "saki_select_positions", "saki_status_str", "saki_last_error"]
 
 
 class SakiRows(ctypes.Structure):
@@ -36,9 +38,10 @@ class SakiRows(ctypes.Structure):
 
 COUPLE_FLOAT_FIELDS = ["lambda", "kl", "tv", "accept_prob", "margin", "logp_token",
                        "logt_token", "logq_token"]
-COUPLE_INT_FIELDS = ["proposal", "token", "teacher_argmax"]
+COUPLE_INT_FIELDS = ["proposal", "token", "teacher_argmax", "target"]
 COUPLE_U8_FIELDS = ["corrected", "row_status"]
-COUPLE_FIELDS = COUPLE_FLOAT_FIELDS + COUPLE_INT_FIELDS + COUPLE_U8_FIELDS
+# struct order of saki_couple_out
+COUPLE_FIELDS = COUPLE_FLOAT_FIELDS + ["proposal", "token", "teacher_argmax"] + COUPLE_U8_FIELDS + ["target"]
 
 
 class SakiCoupleOut(ctypes.Structure):
@@ -49,7 +52,7 @@ class SakiRouteArgs(ctypes.Structure):
     _fields_ = [("valid_mask", ctypes.c_void_p), ("grad_scale", ctypes.c_float),
                 ("grad_dtype", ctypes.c_int32), ("row_loss", ctypes.c_void_p),
                 ("loss_sum", ctypes.c_void_p), ("grad", ctypes.c_void_p),
-                ("grad_stride", ctypes.c_int64)]
+                ("grad_stride", ctypes.c_int64), ("correction_target", ctypes.c_int32)]
 
 
 class SakiError(RuntimeError):
@@ -87,6 +90,12 @@ def load(path=LIB_PATH):
                                      ctypes.c_void_p, ctypes.c_void_p,
                                      ctypes.POINTER(SakiCoupleOut), ctypes.c_void_p,
                                      ctypes.c_size_t, ctypes.c_void_p]
+    lib.saki_select_positions.restype = ctypes.c_int
+    lib.saki_select_positions.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int64,
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int64,
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                          ctypes.c_void_p]
     lib.saki_status_str.restype = ctypes.c_char_p
     lib.saki_status_str.argtypes = [ctypes.c_int]
     lib.saki_last_error.restype = ctypes.c_char_p
@@ -153,11 +162,11 @@ def _couple_struct(out):
     return SakiCoupleOut(*[_ptr(out.get(f)) for f in COUPLE_FIELDS])
 
 
-def _route_struct(valid_mask, grad_scale, row_loss, loss_sum, grad):
+def _route_struct(valid_mask, grad_scale, row_loss, loss_sum, grad, correction_target=SAKI_TARGET_MODE):
     gdt = _dtype_code(grad.dtype) if grad is not None else SAKI_F32
     gstride = grad.stride(0) if grad is not None else 0
     return SakiRouteArgs(_ptr(valid_mask), float(grad_scale), gdt, _ptr(row_loss),
-                         _ptr(loss_sum), _ptr(grad), gstride)
+                         _ptr(loss_sum), _ptr(grad), gstride, int(correction_target))
 
 
 def saki_couple(student, teacher, eps, seed, row_offset=0, out=None, route=None,
@@ -166,7 +175,8 @@ def saki_couple(student, teacher, eps, seed, row_offset=0, out=None, route=None,
 
     out:   dict field -> tensor (missing fields are not written)
     route: None, or dict with optional keys valid_mask, grad_scale, row_loss,
-           loss_sum (float64 tensor of 1), grad (2-D float32/bfloat16 tensor).
+           loss_sum (float64 tensor of 1), grad (2-D float32/bfloat16 tensor),
+           correction_target (SAKI_TARGET_MODE or SAKI_TARGET_SAMPLE).
     """
     load()
     rows = _rows(student, teacher, row_offset)
@@ -174,7 +184,8 @@ def saki_couple(student, teacher, eps, seed, row_offset=0, out=None, route=None,
     rt = None
     if route is not None:
         rt = _route_struct(route.get("valid_mask"), route.get("grad_scale", 1.0),
-                           route.get("row_loss"), route.get("loss_sum"), route.get("grad"))
+                           route.get("row_loss"), route.get("loss_sum"), route.get("grad"),
+                           route.get("correction_target", SAKI_TARGET_MODE))
     ws_b = 0 if workspace is None else workspace.numel() * workspace.element_size()
     st = _lib.saki_couple(ctypes.byref(rows), float(eps), int(seed) & (2**64 - 1),
                           ctypes.byref(co), ctypes.byref(rt) if rt is not None else None,
@@ -213,7 +224,7 @@ def saki_spec_verify(student, teacher, k, draft, eps, seed, row_offset=0, eos_id
 # Convenience wrappers that allocate their outputs (tests, examples).
 # ---------------------------------------------------------------------------
 def couple(student, teacher, eps, seed, row_offset=0, route=False, grad_dtype=None,
-           valid_mask=None, grad_scale=1.0, stream=None):
+           valid_mask=None, grad_scale=1.0, correction_target=SAKI_TARGET_MODE, stream=None):
     n, V = student.shape
     dev = student.device
     out = alloc_couple_out(n, dev)
@@ -222,7 +233,8 @@ def couple(student, teacher, eps, seed, row_offset=0, route=False, grad_dtype=No
     if route:
         rargs = dict(valid_mask=valid_mask, grad_scale=grad_scale,
                      row_loss=torch.empty(n, dtype=torch.float32, device=dev),
-                     loss_sum=torch.empty(1, dtype=torch.float64, device=dev))
+                     loss_sum=torch.empty(1, dtype=torch.float64, device=dev),
+                     correction_target=correction_target)
         if grad_dtype is not None:
             rargs["grad"] = alloc_rows(n, V, grad_dtype, dev)
         nb = workspace_bytes(SAKI_OP_COUPLE, n, V)
@@ -260,3 +272,29 @@ def spec_verify(student, teacher, k, draft, eps, seed, row_offset=0, eos_id=-1, 
     if pp is not None:
         out["per_pos"] = pp
     return out
+
+
+def saki_select_positions(mode, traj_offsets, tv, corrected, selected, seed, valid_mask=None,
+                          row_offset=0, workspace=None, stream=None):
+    """Call saki_select_positions on preallocated buffers (traj_offsets: int64 [n_traj + 1])."""
+    load()
+    n_traj = traj_offsets.numel() - 1
+    n_rows = tv.numel()
+    ws_b = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = _lib.saki_select_positions(int(mode), n_traj, n_rows, _ptr(traj_offsets), _ptr(tv),
+                                    _ptr(corrected), _ptr(valid_mask), int(seed) & (2**64 - 1),
+                                    int(row_offset), _ptr(selected), _ptr(workspace), ws_b,
+                                    _stream(stream))
+    _check(st)
+
+
+def select_positions(mode, traj_offsets, tv, corrected, seed, valid_mask=None, row_offset=0,
+                     stream=None):
+    """Placement-control selection mask (uint8 [n_rows]); allocates its output and workspace."""
+    n = tv.numel()
+    sel = torch.empty(n, dtype=torch.uint8, device=tv.device)
+    ws = torch.empty(max(workspace_bytes(SAKI_OP_SELECT, n, 0), 8), dtype=torch.uint8,
+                     device=tv.device)
+    saki_select_positions(mode, traj_offsets, tv, corrected, sel, seed, valid_mask, row_offset, ws,
+                          stream)
+    return sel

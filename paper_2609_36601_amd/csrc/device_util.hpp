@@ -313,7 +313,11 @@ __device__ __forceinline__ void wave_argmax(float& val, int& idx) {
 // key = (seed lo, seed hi), counter = (block j, stream, g lo, g hi); the four
 // words of block j are the uniforms for indices 4j .. 4j+3 of the stream.
 // ---------------------------------------------------------------------------
-enum Stream : uint32_t { PROP_CHUNK = 0, PROP_ELEM = 1, ACCEPT = 2, RES_CHUNK = 3, RES_ELEM = 4 };
+enum Stream : uint32_t {
+  PROP_CHUNK = 0, PROP_ELEM = 1, ACCEPT = 2, RES_CHUNK = 3, RES_ELEM = 4,
+  TS_CHUNK = 5, TS_ELEM = 6,  // teacher-sampled correction target
+  SELECT = 7                  // placement controls, index 0 of each position
+};
 
 __device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
 #pragma unroll

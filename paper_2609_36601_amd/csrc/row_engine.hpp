@@ -25,8 +25,10 @@ constexpr int RED_MAX = 12;  // widest block reduction (doubles per thread)
 template <int NT>
 struct RowShared {
   static constexpr int NW = NT / WAVE;
-  float chunk_a[MAX_CHUNKS];  // proposal: chunk max of s | residual: chunk mass
-  float chunk_b[MAX_CHUNKS];  // proposal: chunk sum of exp(s - chunk max)
+  float chunk_a[MAX_CHUNKS];  // proposal: reference max of s | residual: chunk mass
+  float chunk_b[MAX_CHUNKS];  // proposal: chunk sum of exp(s - reference)
+  float chunk_c[MAX_CHUNKS];  // teacher draw: reference max of t
+  float chunk_d[MAX_CHUNKS];  // teacher draw: chunk sum of exp(t - reference)
   double red_d[NW][RED_MAX];
   float red_f[NW][4];
   int red_i[NW][4];
@@ -199,9 +201,9 @@ struct StatsAcc {
 // over the wave and rescales the sums.  The arguments (x - M) log2(e) have
 // an exact subtraction, so the largest terms carry no rounding from the shift.
 // The proposal mass of chunk c is kept as (Ms, sum_c exp(s - Ms)).
-template <bool TAIL>
+template <bool TAIL, typename SH>
 __device__ __forceinline__ void stats_math(const float* s, const float* t, uint32_t vm, int c,
-                                           int lane, bool keep_chunks, float* ca, float* cb,
+                                           int lane, bool keep_chunks, bool keep_teacher, SH& sh,
                                            StatsAcc& a) {
   float ls = -finf(), lt = -finf(), lmin = finf(), lmax = -finf();
 #pragma unroll
@@ -269,8 +271,15 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
   if (keep_chunks) {
     const float csum = static_cast<float>(wave_sum(ps));
     if (lane == 0) {
-      *ca = a.Ms;
-      *cb = csum;
+      sh.chunk_a[c] = a.Ms;
+      sh.chunk_b[c] = csum;
+    }
+  }
+  if (keep_teacher) {
+    const float csum = static_cast<float>(wave_sum(pt));
+    if (lane == 0) {
+      sh.chunk_c[c] = a.Mt;
+      sh.chunk_d[c] = csum;
     }
   }
   a.Ss += ps;
@@ -343,16 +352,17 @@ __device__ inline RowStats row_stats_from(const StatsBlock& O) {
   return R;
 }
 
+// keep_chunks: store the proposal chunk masses (of p); keep_teacher: those of pi.
 template <typename T, int NT>
-__device__ RowStats stats_sweep(Block<NT>& B, const T* srow, const T* trow, int V, bool keep_chunks) {
+__device__ RowStats stats_sweep(Block<NT>& B, const T* srow, const T* trow, int V, bool keep_chunks,
+                                bool keep_teacher = false) {
   constexpr int NW = NT / WAVE;
   StatsAcc a;
   a.init();
   for_chunks<T, NW>(srow, trow, V, B.wave, B.lane,
                     [&](auto tail, const float* s, const float* t, uint32_t vm, int c) {
                       constexpr bool TAIL = decltype(tail)::value;
-                      stats_math<TAIL>(s, t, vm, c, B.lane, keep_chunks, &B.sh.chunk_a[c],
-                                       &B.sh.chunk_b[c], a);
+                      stats_math<TAIL>(s, t, vm, c, B.lane, keep_chunks, keep_teacher, B.sh, a);
                     });
   return row_stats_from(stats_combine_block(B, a));
 }

@@ -38,6 +38,7 @@ struct CoupleParams {
   double* scaled_loss;  // workspace [n_rows] or NULL
   void* grad;
   int64_t grad_stride;
+  int target_mode;      // SAKI_TARGET_MODE or SAKI_TARGET_SAMPLE
 };
 
 __device__ __forceinline__ float nanf_() { return __builtin_nanf(""); }
@@ -55,7 +56,8 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
     const uint64_t g = static_cast<uint64_t>(P.row_offset + r);
     const float M = (ROUTE && P.valid) ? (P.valid[r] ? 1.0f : 0.0f) : 1.0f;
 
-    const RowStats R = stats_sweep<T, NT>(B, srow, trow, V, true);
+    const bool sample_target = ROUTE && P.target_mode == SAKI_TARGET_SAMPLE;
+    const RowStats R = stats_sweep<T, NT>(B, srow, trow, V, true, sample_target);
     if (!R.finite) {
       if (GRAD) grad_sweep<T, G, NT>(B, srow, grow, V, 0.0f, 1.0, 0.0f, -1, M != 0.0f);
       if (B.tid == 0) {
@@ -71,6 +73,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
         if (o.proposal) o.proposal[r] = -1;
         if (o.token) o.token[r] = -1;
         if (o.teacher_argmax) o.teacher_argmax[r] = -1;
+        if (o.target) o.target[r] = -1;
         if (o.corrected) o.corrected[r] = 0;
         if (o.row_status) o.row_status[r] = SAKI_ROW_NONFINITE;
         if (ROUTE) {
@@ -102,7 +105,18 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
     const double logt_z = static_cast<double>(tz) - R.lse_t;
     const double adv = logt_z - logp_z;
     const float coef = ROUTE ? static_cast<float>(static_cast<double>(P.grad_scale) * M * (C ? 1.0 : adv)) : 0.0f;
-    const int hot = C ? R.vstar : z;
+    // the gradient's indicator: the proposal when accepted; at a correction
+    // the teacher mode, or a draw from pi by the same two-level race on its
+    // own streams (teacher chunk masses from the stats sweep)
+    int hot = C ? R.vstar : z;
+    if (sample_target && C) {
+      const int ct = chunk_race<NT>(B, nch, P.seed, TS_CHUNK, g, [&](int c) {
+        return static_cast<double>(sh.chunk_c[c]) + log(static_cast<double>(sh.chunk_d[c]));
+      });
+      const int vt = elem_race<NT>(B, ct < nch ? ct : 0, V, P.seed, TS_ELEM, g,
+                                   [&](int v) { return Loader<T>::load1(trow + v); });
+      if (vt < V) hot = vt;
+    }
 
     const FinalConst F = final_const(R, L);
     const double TV = F.acc ? final_sweep<T, G, NT, GRAD, true>(B, srow, trow, grow, V, F, C, coef, hot)
@@ -144,13 +158,14 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
       if (o.proposal) o.proposal[r] = z;
       if (o.token) o.token[r] = y;
       if (o.teacher_argmax) o.teacher_argmax[r] = R.vstar;
+      if (o.target) o.target[r] = hot;
       if (o.corrected) o.corrected[r] = C ? 1 : 0;
       if (o.row_status) o.row_status[r] = SAKI_ROW_OK;
       if (ROUTE) {
         double l = 0.0;
         if (M != 0.0f) {
           if (C) {
-            const double logp_v = static_cast<double>(Loader<T>::load1(srow + R.vstar)) - R.lse_s;
+            const double logp_v = static_cast<double>(Loader<T>::load1(srow + hot)) - R.lse_s;
             l = -logp_v;
           } else {
             l = -adv * logp_z;
@@ -196,6 +211,7 @@ __device__ void write_skipped(const saki_couple_out& o, int64_t r, int32_t draft
   if (o.proposal) o.proposal[r] = draft;
   if (o.token) o.token[r] = -1;
   if (o.teacher_argmax) o.teacher_argmax[r] = -1;
+  if (o.target) o.target[r] = -1;
   if (o.corrected) o.corrected[r] = 0;
   if (o.row_status) o.row_status[r] = status;
 }
@@ -272,6 +288,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void verify_kernel(VerifyParams P) {
         if (o.proposal) o.proposal[r] = z;
         if (o.token) o.token[r] = y;
         if (o.teacher_argmax) o.teacher_argmax[r] = R.vstar;
+        if (o.target) o.target[r] = accept ? z : R.vstar;
         if (o.corrected) o.corrected[r] = accept ? 0 : 1;
         if (o.row_status) o.row_status[r] = SAKI_ROW_OK;
       }
@@ -400,6 +417,133 @@ __global__ __launch_bounds__(1024) void loss_sum_kernel(const double* x, int64_t
   if (threadIdx.x == 0) *out = part[0];
 }
 
+
+// ---------------------------------------------------------------------------
+// Placement controls (Random-TM, TV-Weighted-TM): per trajectory, select
+// m = corrections among the valid positions.  Keys in double: ln E with
+// E = -ln U (Random-TM, and the uniform fill of TV-Weighted-TM from the
+// positions with TV = 0), ln E - ln TV for the positions with TV > 0.  The k
+// smallest keys of a tier are found exactly: bisection over the keys'
+// order-preserving 64-bit images gives the k-th smallest, ties to the lower row.
+// ---------------------------------------------------------------------------
+constexpr int SNT = 256;
+
+struct SelectParams {
+  int mode;
+  int64_t n_traj;
+  int64_t n_rows;
+  const int64_t* off;
+  const float* tv;
+  const uint8_t* corrected;
+  const uint8_t* valid;
+  uint64_t seed;
+  int64_t row_offset;
+  uint8_t* sel;   // holds each row's tier (0, 1; 2 = not valid) until the end
+  double* keys;   // workspace [n_rows]
+};
+
+struct SelShared {
+  double red_d[SNT / WAVE][RED_MAX];
+  float red_f[SNT / WAVE][4];
+  int red_i[SNT / WAVE][4];
+  int scan[SNT];
+};
+
+__device__ __forceinline__ uint64_t order_bits(double k) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, k);
+  return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
+}
+
+// Number of rows of tier `tier` in [a, b) whose key image is <= x (or < x).
+__device__ __forceinline__ double count_le(const SelectParams& P, int64_t a, int64_t b, int tier,
+                                           uint64_t x, bool strict) {
+  double n = 0;
+  for (int64_t r = a; r < b; ++r) {
+    if (P.sel[r] != tier) continue;
+    const uint64_t o = order_bits(P.keys[r]);
+    n += strict ? (o < x) : (o <= x);
+  }
+  return n;
+}
+
+// Marks (sel = 3) the k smallest rows of `tier` in the trajectory; thread j
+// owns rows [a, b), contiguous and in order across threads.
+__device__ void select_smallest(Block<SNT, SelShared>& B, const SelectParams& P, int64_t a, int64_t b,
+                                int tier, double k) {
+  uint64_t lo = 0, hi = ~0ull;
+  while (lo < hi) {
+    const uint64_t mid = lo + (hi - lo) / 2;
+    double v[1] = {count_le(P, a, b, tier, mid, false)};
+    B.sum(v);
+    if (v[0] >= k) hi = mid; else lo = mid + 1;
+  }
+  const uint64_t T = lo;
+  double v[1] = {count_le(P, a, b, tier, T, true)};
+  B.sum(v);
+  const int need = static_cast<int>(k - v[0]);  // rows with key image T to take, lowest rows first
+  int eq = 0;
+  for (int64_t r = a; r < b; ++r) eq += (P.sel[r] == tier && order_bits(P.keys[r]) == T);
+  B.sh.scan[B.tid] = eq;
+  __syncthreads();
+  int before = 0;
+  for (int j = 0; j < B.tid; ++j) before += B.sh.scan[j];
+  __syncthreads();
+  for (int64_t r = a; r < b; ++r) {
+    if (P.sel[r] != tier) continue;
+    const uint64_t o = order_bits(P.keys[r]);
+    if (o < T || (o == T && before++ < need)) P.sel[r] = 3;
+  }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(SNT) void select_kernel(SelectParams P) {
+  __shared__ SelShared sh;
+  Block<SNT, SelShared> B(sh);
+  for (int64_t i = blockIdx.x; i < P.n_traj; i += gridDim.x) {
+    const int64_t lo = P.off[i], hi = P.off[i + 1];
+    if (lo < 0 || hi < lo || hi > P.n_rows) continue;  // malformed range: rows left unwritten
+    const int64_t per = (hi - lo + SNT - 1) / SNT;
+    const int64_t a = min(hi, lo + B.tid * per), b = min(hi, a + per);
+    double cnt[2] = {0, 0};  // corrections among valid rows, rows of tier 0
+    for (int64_t r = a; r < b; ++r) {
+      const bool M = P.valid ? (P.valid[r] != 0) : true;
+      uint8_t tier = 2;
+      double key = __builtin_huge_val();
+      if (M) {
+        const double u = static_cast<double>(philox_uniform(P.seed, SELECT, static_cast<uint64_t>(P.row_offset + r), 0));
+        const double lE = log(-log(u));
+        const double d = static_cast<double>(P.tv[r]);
+        if (P.mode == SAKI_SELECT_RANDOM) {
+          tier = 0; key = lE;
+        } else if (d > 0.0) {
+          tier = 0; key = lE - log(d);
+        } else {
+          tier = 1; key = lE;
+        }
+        cnt[0] += (P.corrected[r] != 0);
+        cnt[1] += (tier == 0);
+      }
+      P.keys[r] = key;
+      P.sel[r] = tier;
+    }
+    __syncthreads();
+    B.sum(cnt);
+    const double m = cnt[0], n0 = cnt[1];
+    if (m > 0) {
+      if (m <= n0) {
+        select_smallest(B, P, a, b, 0, m);
+      } else {
+        for (int64_t r = a; r < b; ++r)
+          if (P.sel[r] == 0) P.sel[r] = 3;
+        __syncthreads();
+        select_smallest(B, P, a, b, 1, m - n0);
+      }
+    }
+    for (int64_t r = a; r < b; ++r) P.sel[r] = (P.sel[r] == 3) ? 1 : 0;
+    __syncthreads();
+  }
+}
+
 }  // namespace saki
 
 // ===========================================================================
@@ -461,6 +605,8 @@ saki_status check_route(const saki_route_args* rt, int64_t vocab, bool* want_los
   *want_loss_sum = false;
   if (!rt) return SAKI_OK;
   if (!isfinite(rt->grad_scale)) return fail(SAKI_E_VALUE, "grad_scale is not finite");
+  if (rt->correction_target != SAKI_TARGET_MODE && rt->correction_target != SAKI_TARGET_SAMPLE)
+    return fail(SAKI_E_VALUE, "unknown correction_target");
   if (rt->grad) {
     if (rt->grad_dtype != SAKI_F32 && rt->grad_dtype != SAKI_BF16) return fail(SAKI_E_DTYPE, "unknown grad dtype");
     if (rt->grad_stride < vocab) return fail(SAKI_E_SHAPE, "grad_stride < vocab");
@@ -516,6 +662,8 @@ size_t saki_workspace_bytes(int op, int64_t n_rows, int64_t vocab) {
       return loss_ws_bytes(n_rows);
     case SAKI_OP_VERIFY:
       return 0;
+    case SAKI_OP_SELECT:
+      return loss_ws_bytes(n_rows);
     default:
       return 0;
   }
@@ -556,6 +704,7 @@ saki_status saki_couple(const saki_rows* in, double eps, uint64_t seed, const sa
     P.scaled_loss = want_sum ? static_cast<double*>(ws) : nullptr;
     P.grad = route->grad;
     P.grad_stride = route->grad_stride;
+    P.target_mode = route->correction_target;
   }
   const int grid = static_cast<int>(std::min<int64_t>(in->n_rows, static_cast<int64_t>(cus) * saki::WG_PER_CU));
   hipStream_t hs = static_cast<hipStream_t>(stream);
@@ -679,6 +828,42 @@ saki_status saki_spec_verify(const saki_rows* in, int32_t k, const int32_t* draf
   else
     hipLaunchKernelGGL(saki::verify_kernel<float>, dim3(grid), dim3(saki::NT), 0, hs, P);
   st = launched("verify_kernel");
+  if (st != SAKI_OK) return st;
+  return ok();
+}
+
+saki_status saki_select_positions(int32_t mode, int64_t n_traj, int64_t n_rows,
+                                  const int64_t* traj_offsets, const float* tv,
+                                  const uint8_t* corrected, const uint8_t* valid_mask, uint64_t seed,
+                                  int64_t row_offset, uint8_t* selected, void* ws, size_t ws_bytes,
+                                  saki_stream_t stream) {
+  if (mode != SAKI_SELECT_RANDOM && mode != SAKI_SELECT_TV_WEIGHTED) return fail(SAKI_E_VALUE, "unknown mode");
+  if (n_traj < 0 || n_rows < 0) return fail(SAKI_E_SHAPE, "n_traj < 0 or n_rows < 0");
+  if (row_offset < 0) return fail(SAKI_E_VALUE, "row_offset < 0");
+  if (n_traj == 0 || n_rows == 0) return ok();
+  if (!traj_offsets || !tv || !corrected || !selected)
+    return fail(SAKI_E_NULLPTR, "traj_offsets, tv, corrected and selected are required");
+  if (!ws) return fail(SAKI_E_WORKSPACE, "workspace is NULL");
+  if (ws_bytes < loss_ws_bytes(n_rows)) return fail(SAKI_E_WORKSPACE, "workspace too small");
+  if ((reinterpret_cast<uintptr_t>(ws) & 7u) != 0) return fail(SAKI_E_ALIGN, "workspace must be 8-byte aligned");
+  int cus = 0;
+  saki_status st = device_cus(&cus);
+  if (st != SAKI_OK) return st;
+  saki::SelectParams P{};
+  P.mode = mode;
+  P.n_traj = n_traj;
+  P.n_rows = n_rows;
+  P.off = traj_offsets;
+  P.tv = tv;
+  P.corrected = corrected;
+  P.valid = valid_mask;
+  P.seed = seed;
+  P.row_offset = row_offset;
+  P.sel = selected;
+  P.keys = static_cast<double*>(ws);
+  const int grid = static_cast<int>(std::min<int64_t>(n_traj, static_cast<int64_t>(cus) * 4));
+  hipLaunchKernelGGL(saki::select_kernel, dim3(grid), dim3(saki::SNT), 0, static_cast<hipStream_t>(stream), P);
+  st = launched("select_kernel");
   if (st != SAKI_OK) return st;
   return ok();
 }

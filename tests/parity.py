@@ -10,7 +10,7 @@ and losses of magnitude below one); unscaled gradients to 2e-3 absolute.
 """
 import numpy as np
 
-from oracle import coupling, routing, verify
+from oracle import coupling, routing, supervision, verify
 
 MARGIN = 1e-6
 RTOL = 1e-5
@@ -58,9 +58,10 @@ class Report:
 
 
 def compare_couple(gpu, s, t, eps, seed, row_offset, rows, report=None, grad=None,
-                   valid=None, grad_scale=1.0):
+                   valid=None, grad_scale=1.0, target_sample=False):
     """Compare GPU outputs (dict of numpy arrays indexed by row) on `rows` with
-    the oracle run on those rows' logits s, t (float64 arrays [len(rows), V])."""
+    the oracle run on those rows' logits s, t (float64 arrays [len(rows), V]).
+    target_sample: corrections were supervised on a teacher draw (App. C)."""
     R = report or Report()
     rows = np.asarray(rows)
     orc_all = [coupling.couple_rows(s[i:i + 1], t[i:i + 1], eps, seed, row_offset + int(r))
@@ -109,10 +110,21 @@ def compare_couple(gpu, s, t, eps, seed, row_offset, rows, report=None, grad=Non
             if not close(g[key], o[key], atol=1e-6):
                 R.fail(f"{tag}: {key} {g[key]!r} vs {o[key]!r}")
             R.note(key, rel_err(g[key], o[key], atol=1e-6))
+        # the gradient's target: y, or at a correction v* / the teacher draw
+        tgt, tgaps = supervision.correction_targets(orc_all[i], t[i:i + 1], seed, row_offset + int(r),
+                                                    sample=target_sample)
+        target = int(tgt[0])
+        if "target" in g and int(g["target"]) != target:
+            if min(tgaps[0]) < MARGIN:
+                R.near_tie += 1
+                continue
+            R.fail(f"{tag}: target {g['target']} vs {target} (gaps {tgaps[0]})")
+            continue
         if "row_loss" in gpu:
             M = None if valid is None else valid[r:r + 1]
-            rl, _, og = routing.couple_and_route(orc_all[i], s[i:i + 1], M, grad_scale,
-                                                 want_grad=grad is not None)
+            adv = o["logt_token"] - o["logp_token"]
+            rl, _, og = routing.route_rows(s[i:i + 1], [o["token"]], [o["corrected"]], [target], [adv],
+                                           M, grad_scale, want_grad=grad is not None)
             if not close(gpu["row_loss"][r], rl[0], atol=1e-6):
                 R.fail(f"{tag}: row_loss {gpu['row_loss'][r]!r} vs {rl[0]!r}")
             R.note("row_loss", rel_err(gpu["row_loss"][r], rl[0], atol=1e-6))

@@ -102,3 +102,26 @@ def test_workspace_sizes(lib):
     assert saki.workspace_bytes(saki.SAKI_OP_COUPLE, 0, 10) == 0
     assert saki.workspace_bytes(saki.SAKI_OP_COUPLE, 1000, 10) >= 8000
     assert saki.workspace_bytes(saki.SAKI_OP_ROUTE, 33, 10) % 256 == 0
+
+
+def test_correction_target_is_checked(lib):
+    rt = binding.SakiRouteArgs(None, 1.0, 0, None, None, None, 0, 7)  # unknown target
+    assert _couple(lib, _rows(), route=rt) == 3
+    assert b"correction_target" in lib.saki_last_error()
+
+
+def test_select_positions_argument_errors(lib):
+    f = lib.saki_select_positions
+    p = 64
+    # mode, n_traj, n_rows, offsets, tv, corrected, valid, seed, row_offset, selected, ws, ws_bytes, stream
+    assert f(5, 2, 10, p, p, p, None, 1, 0, p, p, 1024, None) == 3          # unknown mode
+    assert f(0, -1, 10, p, p, p, None, 1, 0, p, p, 1024, None) == 2         # n_traj < 0
+    assert f(0, 2, -3, p, p, p, None, 1, 0, p, p, 1024, None) == 2          # n_rows < 0
+    assert f(1, 2, 10, p, p, p, None, 1, -1, p, p, 1024, None) == 3         # row_offset < 0
+    assert f(1, 2, 10, None, p, p, None, 1, 0, p, p, 1024, None) == 1       # no offsets
+    assert f(1, 2, 10, p, p, p, None, 1, 0, None, p, 1024, None) == 1       # no output
+    assert f(1, 2, 10, p, p, p, None, 1, 0, p, None, 0, None) == 6          # no workspace
+    assert f(1, 2, 10, p, p, p, None, 1, 0, p, p, 16, None) == 6            # too small
+    assert f(1, 2, 10, p, p, p, None, 1, 0, p, 68, 1024, None) == 5         # misaligned
+    assert f(1, 0, 10, None, None, None, None, 1, 0, None, None, 0, None) == 0  # nothing to do
+    assert saki.workspace_bytes(saki.SAKI_OP_SELECT, 100, 0) >= 800

@@ -32,18 +32,20 @@ def f64(x):
 
 
 def run_and_compare(saki, s, t, eps, seed, row_offset=0, rows=None, grad=True, valid=None,
-                    grad_dtype=torch.float32):
-    say(f"couple n={s.shape[0]} V={s.shape[1]} dtype={s.dtype} eps={eps} offset={row_offset}")
+                    grad_dtype=torch.float32, target_sample=False):
+    say(f"couple n={s.shape[0]} V={s.shape[1]} dtype={s.dtype} eps={eps} offset={row_offset} "
+        f"target_sample={target_sample}")
     vm = None if valid is None else torch.as_tensor(valid, dtype=torch.uint8, device=DEV)
     out = saki.couple(s, t, eps, seed, row_offset, route=True,
-                      grad_dtype=grad_dtype if grad else None, valid_mask=vm, grad_scale=1.0)
+                      grad_dtype=grad_dtype if grad else None, valid_mask=vm, grad_scale=1.0,
+                      correction_target=saki.SAKI_TARGET_SAMPLE if target_sample else saki.SAKI_TARGET_MODE)
     torch.cuda.synchronize()
     o = np_out(out)
     rows = np.arange(s.shape[0]) if rows is None else np.asarray(rows)
     g = f64(out["grad"][torch.as_tensor(rows, device=DEV)]) if grad else None
     R = parity.compare_couple(o, f64(s[torch.as_tensor(rows, device=DEV)]),
                               f64(t[torch.as_tensor(rows, device=DEV)]), eps, seed, row_offset,
-                              rows, grad=g, valid=valid)
+                              rows, grad=g, valid=valid, target_sample=target_sample)
     say(R.summary())
     R.check()
     return out, o, R
