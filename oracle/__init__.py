@@ -20,6 +20,7 @@ verify    speculative block verification with first-rejection semantics
 supervision  teacher-sampled correction targets (App. C) and the Random-TM /
           TV-Weighted-TM placement controls (Sec. 4.1, placement-control
           appendix).
+probe     fixed-prefix probe metrics C_1, C_k, KL(T || S), H(S).
 
 Every function works in float64 on the exact input values (bf16 and fp32
 logits convert exactly to float64).
