@@ -55,6 +55,7 @@ extern "C" {
 #define SAKI_MAX_VOCAB (1 << 21) /* 2,097,152 entries per row */
 #define SAKI_CHUNK 1024          /* vocab entries per race chunk (sampler definition) */
 #define SAKI_MAX_BLOCK_K 64      /* largest speculative block length */
+#define SAKI_MAX_PROBE_K 64      /* largest teacher Top-k of the probe metrics */
 
 typedef void *saki_stream_t; /* a hipStream_t; NULL = the default stream */
 
@@ -215,6 +216,24 @@ saki_status saki_select_positions(int32_t mode, int64_t n_traj, int64_t n_rows,
                                   const uint8_t *corrected, const uint8_t *valid_mask,
                                   uint64_t seed, int64_t row_offset, uint8_t *selected,
                                   void *ws, size_t ws_bytes, saki_stream_t stream);
+
+/* Fixed-prefix probe metrics (the paper's probe analysis), per row of
+ * student / teacher logits: S = softmax(student), T = softmax(teacher),
+ *   c1[r]      = S(v*), v* the teacher's Top-1 (lowest index on ties);
+ *   ck[r]      = sum of S over the teacher's Top-k set (the k largest teacher
+ *                logits, ties to the lower index; k = 16 in the paper);
+ *   kl_ts[r]   = KL(T || S) = E_T[t - s] - (lse_t - lse_s), the conflict measure
+ *                (accumulated in double from float partial sums: relative error
+ *                ~1e-7 x E_T[t - s] / KL);
+ *   entropy[r] = H(S);
+ *   topk       = [n_rows, k] the Top-k indices, best first.
+ * Every output may be NULL.  1 <= k <= min(SAKI_MAX_PROBE_K, vocab).  Rows with a
+ * non-finite logit get NaN metrics, topk -1 and row_status SAKI_ROW_NONFINITE.
+ * One workgroup per row, with ~40 sweeps over the teacher row for the exact
+ * Top-k threshold: meant for probe sets, not for every training position. */
+saki_status saki_probe_metrics(const saki_rows *in, int32_t k, float *c1, float *ck, float *kl_ts,
+                               float *entropy, int32_t *topk, uint8_t *row_status,
+                               saki_stream_t stream);
 
 /* Static description of a status code. */
 const char *saki_status_str(saki_status s);

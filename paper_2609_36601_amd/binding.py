@@ -26,7 +26,8 @@ STATUS = {0: "SAKI_OK", 1: "SAKI_E_NULLPTR", 2: "SAKI_E_SHAPE", 3: "SAKI_E_VALUE
           8: "SAKI_E_LAUNCH"}
 
 EXPORTED = ["saki_workspace_bytes", "saki_couple", "saki_route_loss", "saki_spec_verify",
-            "saki_select_positions", "saki_status_str", "saki_last_error"]
+            "saki_select_positions", "saki_probe_metrics", "saki_status_str", "saki_last_error"]
+SAKI_MAX_PROBE_K = 64
 
 
 class SakiRows(ctypes.Structure):
@@ -96,6 +97,10 @@ def load(path=LIB_PATH):
                                           ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int64,
                                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                           ctypes.c_void_p]
+    lib.saki_probe_metrics.restype = ctypes.c_int
+    lib.saki_probe_metrics.argtypes = [ctypes.POINTER(SakiRows), ctypes.c_int32, ctypes.c_void_p,
+                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     lib.saki_status_str.restype = ctypes.c_char_p
     lib.saki_status_str.argtypes = [ctypes.c_int]
     lib.saki_last_error.restype = ctypes.c_char_p
@@ -298,3 +303,27 @@ def select_positions(mode, traj_offsets, tv, corrected, seed, valid_mask=None, r
     saki_select_positions(mode, traj_offsets, tv, corrected, sel, seed, valid_mask, row_offset, ws,
                           stream)
     return sel
+
+
+def saki_probe_metrics(student, teacher, k, c1=None, ck=None, kl_ts=None, entropy=None, topk=None,
+                       row_status=None, stream=None):
+    """Call saki_probe_metrics on preallocated outputs (any may be None)."""
+    load()
+    rows = _rows(student, teacher, 0)
+    st = _lib.saki_probe_metrics(ctypes.byref(rows), int(k), _ptr(c1), _ptr(ck), _ptr(kl_ts),
+                                 _ptr(entropy), _ptr(topk), _ptr(row_status), _stream(stream))
+    _check(st)
+
+
+def probe_metrics(student, teacher, k=16, stream=None):
+    """Probe metrics per row; allocates its outputs."""
+    n = student.shape[0]
+    dev = student.device
+    out = dict(c1=torch.empty(n, dtype=torch.float32, device=dev),
+               ck=torch.empty(n, dtype=torch.float32, device=dev),
+               kl_ts=torch.empty(n, dtype=torch.float32, device=dev),
+               entropy=torch.empty(n, dtype=torch.float32, device=dev),
+               topk=torch.empty(n, k, dtype=torch.int32, device=dev),
+               row_status=torch.empty(n, dtype=torch.uint8, device=dev))
+    saki_probe_metrics(student, teacher, k, stream=stream, **out)
+    return out

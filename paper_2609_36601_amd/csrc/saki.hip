@@ -178,6 +178,12 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
   }
 }
 
+}  // namespace saki
+
+#include "probe.hpp"
+
+namespace saki {
+
 // ---------------------------------------------------------------------------
 // Speculative verification: one workgroup per block, positions in order.
 // ---------------------------------------------------------------------------
@@ -828,6 +834,40 @@ saki_status saki_spec_verify(const saki_rows* in, int32_t k, const int32_t* draf
   else
     hipLaunchKernelGGL(saki::verify_kernel<float>, dim3(grid), dim3(saki::NT), 0, hs, P);
   st = launched("verify_kernel");
+  if (st != SAKI_OK) return st;
+  return ok();
+}
+
+saki_status saki_probe_metrics(const saki_rows* in, int32_t k, float* c1, float* ck, float* kl_ts,
+                               float* entropy, int32_t* topk, uint8_t* row_status,
+                               saki_stream_t stream) {
+  saki_status st = check_rows(in);
+  if (st != SAKI_OK) return st;
+  if (k < 1 || k > SAKI_MAX_PROBE_K || k > in->vocab) return fail(SAKI_E_SHAPE, "k outside [1, min(SAKI_MAX_PROBE_K, vocab)]");
+  if (in->n_rows == 0) return ok();
+  int cus = 0;
+  st = device_cus(&cus);
+  if (st != SAKI_OK) return st;
+  saki::ProbeParams P{};
+  P.s = in->student;
+  P.t = in->teacher;
+  P.n_rows = in->n_rows;
+  P.stride = in->row_stride;
+  P.V = static_cast<int>(in->vocab);
+  P.k = k;
+  P.c1 = c1;
+  P.ck = ck;
+  P.kl_ts = kl_ts;
+  P.entropy = entropy;
+  P.topk = topk;
+  P.row_status = row_status;
+  const int grid = static_cast<int>(std::min<int64_t>(in->n_rows, static_cast<int64_t>(cus) * saki::WG_PER_CU));
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (in->dtype == SAKI_BF16)
+    hipLaunchKernelGGL(saki::probe_kernel<uint16_t>, dim3(grid), dim3(saki::NT), 0, hs, P);
+  else
+    hipLaunchKernelGGL(saki::probe_kernel<float>, dim3(grid), dim3(saki::NT), 0, hs, P);
+  st = launched("probe_kernel");
   if (st != SAKI_OK) return st;
   return ok();
 }

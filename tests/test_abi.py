@@ -125,3 +125,14 @@ def test_select_positions_argument_errors(lib):
     assert f(1, 2, 10, p, p, p, None, 1, 0, p, 68, 1024, None) == 5         # misaligned
     assert f(1, 0, 10, None, None, None, None, 1, 0, None, None, 0, None) == 0  # nothing to do
     assert saki.workspace_bytes(saki.SAKI_OP_SELECT, 100, 0) >= 800
+
+
+def test_probe_metrics_argument_errors(lib):
+    f = lib.saki_probe_metrics
+    rows = _rows()
+    assert f(None, 16, None, None, None, None, None, None, None) == 1
+    assert f(ctypes.byref(rows), 0, None, None, None, None, None, None, None) == 2
+    assert f(ctypes.byref(rows), 65, None, None, None, None, None, None, None) == 2
+    assert f(ctypes.byref(_rows(vocab=8, row_stride=8)), 9, None, None, None, None, None, None, None) == 2
+    assert f(ctypes.byref(_rows(n_rows=0, student=0, teacher=0)), 4, None, None, None, None, None, None,
+             None) == 0
