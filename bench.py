@@ -126,6 +126,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one 1 GiB device copy before timing (counter calibration)")
+    ap.add_argument("--workload", choices=("couple", "verify"), default="couple",
+                    help="couple: the headline (coupling + routed loss + fp32 gradient); "
+                         "verify: speculative verification of 8,192 blocks of k = 8")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
@@ -138,6 +141,8 @@ def main():
 
     saki.load()
     dev = torch.device("cuda:0")
+    if args.workload == "verify":
+        return bench_verify(args, saki, workloads, dev)
     cfg = workloads.CONFIGS["large"]
     n = args.rows or cfg["rows"]
     V = cfg["V"]
@@ -221,6 +226,107 @@ def main():
                      "traffic": measured_traffic_bytes() if n == cfg["rows"] and args.eps == 0.2 else None},
         "cpu_baseline": cpu,
         "stats": {"correction_rate": corr_rate, "mean_tv": mean_tv, "mean_lambda": mean_lam},
+    }
+    print(json.dumps(line), flush=True)
+
+
+def _oracle_blocks(args):
+    os.environ.setdefault("OMP_NUM_THREADS", "1")
+    from oracle import verify
+    s, t, draft, k, eps, seed, offsets = args
+    t0 = time.perf_counter()
+    for i in range(len(offsets)):
+        sl = slice(i * k, (i + 1) * k)
+        verify.verify_blocks(s[sl], t[sl], k, draft[sl], eps, seed, int(offsets[i]))
+    return time.perf_counter() - t0
+
+
+def bench_verify(args, saki, workloads, dev):
+    """Speculative verification (Sec. 3.5): 256 sequences x 32 blocks of k = 8
+    draft positions, V = 151,936 bf16, eps 0.2; accepted-prefix length and the
+    correction of every block."""
+    import numpy as np
+    import torch
+    cfg = workloads.CONFIGS["verify"]
+    k, V = cfg["k"], cfg["V"]
+    n = args.rows or cfg["rows"]
+    n -= n % k
+    nb = n // k
+    seed = workloads.coupling_seed("verify")
+    print(f"# generating {n} x {V} bf16 rows and student drafts", file=sys.stderr, flush=True)
+    s = torch.empty(n, V, dtype=torch.bfloat16, device=dev)
+    t = torch.empty_like(s)
+    workloads.fill("verify", s, t)
+    draft = workloads.drafts(s)
+    acc = torch.empty(nb, dtype=torch.int32, device=dev)
+    corr = torch.empty(nb, dtype=torch.int32, device=dev)
+    ws = torch.empty(max(saki.workspace_bytes(saki.SAKI_OP_VERIFY, n, V), 8), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+
+    def step():
+        saki.saki_spec_verify(s, t, k, draft, args.eps, seed, 0, -1, acc, corr, None, ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    ev[0].record(stream)
+    for i in range(args.steps):
+        step()
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+    ms = sum(per) / len(per)
+    al = acc.cpu().numpy()
+    evaluated = int(np.minimum(al + 1, k).sum())  # positions each block reads before it stops
+    print(f"# per-step ms: {[round(x, 3) for x in per]}; mean accepted length {al.mean():.3f}; "
+          f"positions evaluated {evaluated} of {n}", file=sys.stderr, flush=True)
+    achieved = evaluated * 2 * V * 2 / (ms * 1e-3) / 1e9
+    attainable = attainable_read_gbs(dev)
+    cpu = None
+    if not args.no_cpu_baseline:
+        n_sample = max(1, args.cpu_sample // k)
+        blocks = np.linspace(0, nb - 1, n_sample).astype(np.int64)
+        idx = torch.as_tensor(np.concatenate([np.arange(b * k, (b + 1) * k) for b in blocks]), device=dev)
+        S = s[idx].float().cpu().numpy().astype(np.float64)
+        T = t[idx].float().cpu().numpy().astype(np.float64)
+        D = draft[idx].cpu().numpy()
+        workers = max(1, min(16, os.cpu_count() or 1))
+        parts = np.array_split(np.arange(n_sample), workers)
+        jobs = [(np.concatenate([S[b * k:(b + 1) * k] for b in p]), np.concatenate([T[b * k:(b + 1) * k] for b in p]),
+                 np.concatenate([D[b * k:(b + 1) * k] for b in p]), k, args.eps, seed, blocks[p] * k)
+                for p in parts if len(p)]
+        ctx = mp.get_context("spawn")
+        with ctx.Pool(len(jobs)) as pool:
+            pool.map(_noop, range(len(jobs)))
+            t0 = time.perf_counter()
+            busy = pool.map(_oracle_blocks, jobs)
+            wall = time.perf_counter() - t0
+        cpu = dict(value=n_sample / wall, unit="blocks/s", cores=len(jobs), kind="oracle",
+                   sample=f"{n_sample} blocks of the same workload (evenly spaced), {len(jobs)} "
+                          f"single-threaded worker processes; {sum(busy):.1f} s of CPU work in {wall:.1f} s wall")
+    line = {
+        "metric": "speculative-verify blocks/sec (k=8, V=151,936 bf16)",
+        "value": nb / (ms * 1e-3),
+        "unit": "blocks/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 in, f32/f64 accumulation",
+        "data": "synthetic",
+        "config": {"workload": "verify: 256 seq x 32 blocks x k=8 = 65,536 rows, V=151,936 bf16, "
+                               "rho~U(0.2,0.99) per block, drafts z~softmax(s)",
+                   "blocks": nb, "k": k, "vocab": V, "eps": args.eps,
+                   "mean_accepted_length": float(al.mean()), "positions_evaluated": evaluated},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "attainable_read": attainable,
+                     "frac_attainable": achieved / attainable, "traffic": None},
+        "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
 

@@ -271,8 +271,9 @@ def spec_verify(student, teacher, k, draft, eps, seed, row_offset=0, eos_id=-1, 
     acc = torch.empty(nb, dtype=torch.int32, device=dev)
     corr = torch.empty(nb, dtype=torch.int32, device=dev)
     pp = alloc_couple_out(n, dev) if per_pos else None
+    ws = torch.empty(max(workspace_bytes(SAKI_OP_VERIFY, n, V), 8), dtype=torch.uint8, device=dev)
     saki_spec_verify(student, teacher, k, draft, eps, seed, row_offset, eos_id, acc, corr, pp,
-                     None, stream)
+                     ws, stream)
     out = dict(accepted_len=acc, correction=corr)
     if pp is not None:
         out["per_pos"] = pp

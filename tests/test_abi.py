@@ -92,6 +92,7 @@ def test_verify_and_route_argument_errors(lib):
     assert not_multiple == 2
     no_draft = lib.saki_spec_verify(ctypes.byref(rows), 3, None, 0.1, 1, -1, acc, acc, None, None, 0, None)
     assert no_draft == 1
+
     rt = binding.SakiRouteArgs(None, 1.0, 0, None, None, None, 0)
     assert lib.saki_route_loss(16, 9, 4, 64, 64, 64, 64, 64, 64, ctypes.byref(rt), None, 0, None) == 4
     assert lib.saki_route_loss(16, 1, 4, 64, 64, None, 64, 64, 64, ctypes.byref(rt), None, 0, None) == 1
