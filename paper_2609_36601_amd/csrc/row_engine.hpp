@@ -147,22 +147,36 @@ template <typename T, int NW, bool LAST = false, typename Body>
 __device__ __forceinline__ void for_chunks(const T* srow, const T* trow, int V, int wave, int lane,
                                            Body&& body) {
   const int nfull = V / CHUNK;
+  auto run = [&](const Frag<T>& fs, const Frag<T>& ft, int c) {
+    float s[EPL], t[EPL];
+    frag_unpack(fs, s);
+    frag_unpack(ft, t);
+    body(std::integral_constant<bool, false>(), s, t, 0xffffu, c);
+  };
   if (wave < nfull) {
-    Frag<T> fs, ft;
-    frag_load<LAST>(fs, srow, wave, lane);
-    frag_load<LAST>(ft, trow, wave, lane);
-    for (int c = wave; c < nfull; c += NW) {
-      Frag<T> ns, nt;
-      if (c + NW < nfull) {
-        frag_load<LAST>(ns, srow, c + NW, lane);
-        frag_load<LAST>(nt, trow, c + NW, lane);
+    // two fragment buffers used in turn: chunk c is processed while the
+    // loads of the wave's next chunk are in flight, without register copies
+    Frag<T> as, at, bs, bt;
+    frag_load<LAST>(as, srow, wave, lane);
+    frag_load<LAST>(at, trow, wave, lane);
+    int c = wave;
+    for (;;) {
+      const bool more_b = c + NW < nfull;
+      if (more_b) {
+        frag_load<LAST>(bs, srow, c + NW, lane);
+        frag_load<LAST>(bt, trow, c + NW, lane);
       }
-      float s[EPL], t[EPL];
-      frag_unpack(fs, s);
-      frag_unpack(ft, t);
-      body(std::integral_constant<bool, false>(), s, t, 0xffffu, c);
-      fs = ns;
-      ft = nt;
+      run(as, at, c);
+      if (!more_b) break;
+      c += NW;
+      const bool more_a = c + NW < nfull;
+      if (more_a) {
+        frag_load<LAST>(as, srow, c + NW, lane);
+        frag_load<LAST>(at, trow, c + NW, lane);
+      }
+      run(bs, bt, c);
+      if (!more_a) break;
+      c += NW;
     }
   }
   if ((V % CHUNK) != 0 && (nfull % NW) == wave) {
@@ -400,13 +414,23 @@ struct LamEval {
   double lam, A, A1, A2, A3, A4, KL;
 };
 
+// 2^-d0 for d0 = ms log2(e) - msL, the rounding of the float shift msL.
+__device__ __forceinline__ double shift_correction(float ms, float msL) {
+  const double d0 = static_cast<double>(LOG2E) * static_cast<double>(ms) - static_cast<double>(msL);
+  return exp2(-d0);
+}
+
+// a = fma(s, log2 e, -msL) with msL = ms log2 e rounded to float: the rounding
+// of the shift, d0 = ms log2 e - msL (exact in double), is one offset for every
+// entry of the row, so every weight and every p~ carries the factor 2^d0; the
+// row sums are multiplied by 2^-d0 once (shift_correction).
 template <int MODE, bool TAIL>
-__device__ __forceinline__ void lam_math(const float* s, const float* t, uint32_t vm, float ms,
+__device__ __forceinline__ void lam_math(const float* s, const float* t, uint32_t vm, float msL,
                                          float cL, float lam, float sigl, double (&acc)[5]) {
   float W = 0.f, S1 = 0.f, S2 = 0.f, S3 = 0.f, S4 = 0.f;
 #pragma unroll
   for (int e = 0; e < EPL; ++e) {
-    const float a = (s[e] - ms) * LOG2E;
+    const float a = fmaf(s[e], LOG2E, -msL);
     float pt = fexp2(a);
     const float X = fmaf(t[e] - s[e], LOG2E, -cL);
     float w, u;
@@ -472,12 +496,16 @@ __device__ LamEval lam_sweep_mode(Block<NT>& B, const T* srow, const T* trow, in
                                   float lam, float sigl) {
   constexpr int NW = NT / WAVE;
   double v[5] = {0, 0, 0, 0, 0};
+  const float msL = R.ms * LOG2E;
   for_chunks<T, NW>(srow, trow, V, B.wave, B.lane,
                     [&](auto tail, const float* s, const float* t, uint32_t vm, int c) {
                       constexpr bool TAIL = decltype(tail)::value;
-                      lam_math<MODE, TAIL>(s, t, vm, R.ms, R.cL, lam, sigl, v);
+                      lam_math<MODE, TAIL>(s, t, vm, msL, R.cL, lam, sigl, v);
                     });
   B.sum(v);
+  const double corr = shift_correction(R.ms, msL);
+#pragma unroll
+  for (int j = 0; j < 5; ++j) v[j] *= corr;
   return lam_finish(v, R.sum_s, lam, sigl);
 }
 
@@ -495,8 +523,12 @@ __device__ LamEval lam_sweep(Block<NT>& B, const T* srow, const T* trow, int V, 
 }
 
 // Rows whose KL (the radius, or KL(pi||p) at the teacher endpoint) is below
-// this use the expm1 forms of the sweeps.
+// this use the expm1 forms of the lambda sweeps.
 constexpr double KL_ACCURATE = 0.01;
+// ... and below this, the expm1 form of the final sweep: there 2^y - 1 carries
+// ~6e-8 absolute error per entry, which summed over the positive residual is
+// ~1e-5 of a TV near 0.01 (TV <= sqrt(KL / 2)).
+constexpr double TV_ACCURATE = 0.1;
 
 // Result of the lambda search.
 struct LamResult {
@@ -714,18 +746,19 @@ __device__ LamResult lambda_search(Block<NT>& B, const T* srow, const T* trow, i
 //   w_v = p_v [q_v/p_v - 1]_+ ;  grad_v = coef * (p_v - 1[v = hot]).
 // ---------------------------------------------------------------------------
 struct FinalConst {
-  float ms, invS, cL, lam, AL;  // AL = A* log2(e)
-  bool acc;                     // expm1 form (rows whose KL is small)
+  float msL, invS, cL, lam, AL;  // msL = ms log2(e); AL = A* log2(e)
+  bool acc;                      // expm1 form (rows whose KL is small)
 };
 
 __device__ inline FinalConst final_const(const RowStats& R, const LamResult& L) {
   FinalConst F;
-  F.ms = R.ms;
-  F.invS = static_cast<float>(1.0 / R.sum_s);
+  F.msL = R.ms * LOG2E;
+  // p = 2^{fma(s, log2 e, -msL)} * invS: the shift's rounding is folded into invS
+  F.invS = static_cast<float>(shift_correction(R.ms, F.msL) / R.sum_s);
   F.cL = L.cL;
   F.lam = L.qp ? 0.0f : L.lam;
   F.AL = L.qp ? 0.0f : static_cast<float>(L.A * static_cast<double>(LOG2E));
-  F.acc = L.KL < KL_ACCURATE;
+  F.acc = L.KL < TV_ACCURATE;
   return F;
 }
 
@@ -733,7 +766,7 @@ __device__ inline FinalConst final_const(const RowStats& R, const LamResult& L) 
 // the same function, so its weights are bit-identical to the chunk masses'.
 template <bool ACC>
 __device__ __forceinline__ float res_weight(float s, float t, const FinalConst& F, float* p_out) {
-  const float p = fexp2((s - F.ms) * LOG2E) * F.invS;
+  const float p = fexp2(fmaf(s, LOG2E, -F.msL)) * F.invS;
   const float X = fmaf(t - s, LOG2E, -F.cL);
   const float y2 = fmaf(F.lam, X, -F.AL);  // log2 of q/p
   const float ee = fexp2(y2);
