@@ -19,7 +19,7 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
 
 KERNEL_SOURCES = ["paper_2609_36601_amd/csrc/saki.hip", "paper_2609_36601_amd/csrc/row_engine.hpp",
-                  "paper_2609_36601_amd/csrc/device_util.hpp"]
+                  "paper_2609_36601_amd/csrc/device_util.hpp", "paper_2609_36601_amd/csrc/probe.hpp"]
 
 # HBM traffic of one couple-kernel launch on the large workload (eps 0.2), from
 # two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch;
@@ -28,8 +28,8 @@ KERNEL_SOURCES = ["paper_2609_36601_amd/csrc/saki.hip", "paper_2609_36601_amd/cs
 # FETCH_SIZE is scaled by 2.0 and WRITE_SIZE by 1.0.  Keyed by the SHA-256 of
 # the kernel sources: a changed kernel reports traffic = null until re-measured.
 MEASURED_TRAFFIC = {
-    "d62f991ce079a8b87f99fb8d441a5e8686471c9d2c3ddf1aa4bc8ac86cbbd2b6":
-        dict(fetch_kib=58884108.3, write_kib=40717110.3, fetch_scale=2.0, write_scale=1.0),
+    "db761d824e8b301f2206f589e800dbd23f52453829684234f40674aba6c3d3c6":
+        dict(fetch_kib=59447445.8, write_kib=40671994.2, fetch_scale=2.0, write_scale=1.0),
 }
 
 
@@ -122,7 +122,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--eps", type=float, default=0.2)
     ap.add_argument("--rows", type=int, default=None, help="override the row count (debug)")
-    ap.add_argument("--cpu-sample", type=int, default=128)
+    ap.add_argument("--cpu-sample", type=int, default=256)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one 1 GiB device copy before timing (counter calibration)")
