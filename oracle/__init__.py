@@ -21,6 +21,9 @@ supervision  teacher-sampled correction targets (App. C) and the Random-TM /
           TV-Weighted-TM placement controls (Sec. 4.1, placement-control
           appendix).
 probe     fixed-prefix probe metrics C_1, C_k, KL(T || S), H(S).
+rollout   multi-wave speculative rollout: drafting, verification,
+          first-rejection commit and rollback, token-aligned metadata
+          (Sec. 3.5, App. F Prop. spec_exact, App. I).
 
 Every function works in float64 on the exact input values (bf16 and fp32
 logits convert exactly to float64).

@@ -143,3 +143,111 @@ def drafts(student, seed=0, k=8):
 def n_blocks_of(name):
     cfg = CONFIGS[name]
     return math.ceil(cfg["rows"] / cfg["block"])
+
+
+# ---------------------------------------------------------------------------
+# A synthetic autoregressive source: a stand-in for the student and teacher
+# networks of a rollout (the paper's engine holds real models; these logits
+# depend on the whole prefix through a 64-bit state, so rollouts exercise
+# first-rejection commit and rollback).  Pure integer hashing on the host
+# (numpy uint64), so every consumer sees the same exact values:
+#   state_0(seq)   = mix(seed ^ (seq + 1) * K0)
+#   state_{t+1}    = mix(state_t ^ (y_t + 1) * K1)
+#   a_v(state)     = mix(state ^ (v + 1) * K2)
+#   s_v = ((a_v >> 32) % 33 - 16) / 4            (student, in [-4, 4])
+#   t_v = s_v / 2 + ((a_v & 0xffffffff) % 17 - 8) / 4   (teacher, multiples of 1/8)
+# mix is the SplitMix64 output function (Steele, Lea, Flood, OOPSLA 2014).
+# All values are exact in bf16, f32 and f64.
+# ---------------------------------------------------------------------------
+_M64 = (1 << 64) - 1
+_K0, _K1, _K2 = 0x9E3779B97F4A7C15, 0xD6E8FEB86659FD93, 0xA0761D6478BD642F
+
+
+def _mix(x):
+    import numpy as np
+    x = np.asarray(x, dtype=np.uint64)
+    with np.errstate(over="ignore"):
+        z = x + np.uint64(0x9E3779B97F4A7C15)
+        z = (z ^ (z >> np.uint64(30))) * np.uint64(0xBF58476D1CE4E5B9)
+        z = (z ^ (z >> np.uint64(27))) * np.uint64(0x94D049BB133111EB)
+        return z ^ (z >> np.uint64(31))
+
+
+class SyntheticAR:
+    """Prefix-hash student/teacher logits over V tokens (see above)."""
+
+    def __init__(self, V, seed=0):
+        self.V = int(V)
+        self.seed = int(seed) & _M64
+
+    def initial(self, seq_ids):
+        import numpy as np
+        seq = np.asarray(seq_ids, dtype=np.uint64)
+        with np.errstate(over="ignore"):
+            return _mix(np.uint64(self.seed) ^ ((seq + np.uint64(1)) * np.uint64(_K0)))
+
+    def advance(self, states, tokens):
+        import numpy as np
+        tok = np.asarray(tokens, dtype=np.int64).astype(np.uint64)
+        with np.errstate(over="ignore"):
+            return _mix(np.asarray(states, dtype=np.uint64) ^ ((tok + np.uint64(1)) * np.uint64(_K1)))
+
+    def logits(self, states):
+        """(s, t) as float32 arrays [len(states), V] (exact values)."""
+        import numpy as np
+        st = np.asarray(states, dtype=np.uint64)[:, None]
+        v = np.arange(self.V, dtype=np.uint64)[None, :]
+        with np.errstate(over="ignore"):
+            a = _mix(st ^ ((v + np.uint64(1)) * np.uint64(_K2)))
+        hi = (a >> np.uint64(32)).astype(np.int64)
+        lo = (a & np.uint64(0xFFFFFFFF)).astype(np.int64)
+        s = ((hi % 33) - 16).astype(np.float32) / 4.0
+        t = s / 2.0 + ((lo % 17) - 8).astype(np.float32) / 4.0
+        return s, t
+
+
+def _i64(c):
+    """A uint64 constant as the int64 with the same bits."""
+    return c - (1 << 64) if c >= (1 << 63) else c
+
+
+def _mix_t(x):
+    """SplitMix64 output function on int64 tensors (two's-complement wrap)."""
+    def srl(v, k):
+        return (v >> k) & ((1 << (64 - k)) - 1)
+    z = x + _i64(0x9E3779B97F4A7C15)
+    z = (z ^ srl(z, 30)) * _i64(0xBF58476D1CE4E5B9)
+    z = (z ^ srl(z, 27)) * _i64(0x94D049BB133111EB)
+    return z ^ srl(z, 31)
+
+
+class SyntheticARTorch:
+    """SyntheticAR on int64 torch tensors (any device): same states and logits."""
+
+    def __init__(self, V, seed=0, device="cpu"):
+        self.V = int(V)
+        self.seed = _i64(int(seed) & _M64)
+        self.device = device
+
+    def initial(self, seq_ids):
+        import torch
+        seq = torch.as_tensor(seq_ids, dtype=torch.int64, device=self.device)
+        return _mix_t(self.seed ^ ((seq + 1) * _i64(_K0)))
+
+    def advance(self, states, tokens):
+        import torch
+        tok = tokens.to(torch.int64)
+        return _mix_t(states ^ ((tok + 1) * _i64(_K1)))
+
+    def logits_into(self, states, s_out=None, t_out=None):
+        """Writes s and/or t for `states` [n] into [n, V] views (any float dtype)."""
+        import torch
+        v = torch.arange(self.V, dtype=torch.int64, device=states.device)
+        a = _mix_t(states[:, None] ^ ((v[None, :] + 1) * _i64(_K2)))
+        hi = (a >> 32) & 0xFFFFFFFF
+        s = ((hi % 33) - 16).to(torch.float32) / 4.0
+        if s_out is not None:
+            s_out.copy_(s)
+        if t_out is not None:
+            lo = a & 0xFFFFFFFF
+            t_out.copy_(s / 2.0 + ((lo % 17) - 8).to(torch.float32) / 4.0)
