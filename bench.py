@@ -19,7 +19,8 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
 
 KERNEL_SOURCES = ["paper_2609_36601_amd/csrc/saki.hip", "paper_2609_36601_amd/csrc/row_engine.hpp",
-                  "paper_2609_36601_amd/csrc/device_util.hpp", "paper_2609_36601_amd/csrc/probe.hpp"]
+                  "paper_2609_36601_amd/csrc/device_util.hpp", "paper_2609_36601_amd/csrc/probe.hpp",
+                  "paper_2609_36601_amd/csrc/rollout.hpp"]
 
 # HBM traffic of one couple-kernel launch on the large workload (eps 0.2), from
 # two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch;

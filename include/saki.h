@@ -18,7 +18,10 @@
  *                                                 (Sec. 3.5, App. F, App. I);
  *   6. supervision variants: a correction target drawn from the teacher
  *      instead of its mode (App. C), and the Random-TM / TV-Weighted-TM
- *      placement controls (Sec. 4.1, placement-control appendix).
+ *      placement controls (Sec. 4.1, placement-control appendix);
+ *   7. the other steps of a speculative rollout wave: student draft sampling,
+ *      and the first-rejection commit with token-aligned metadata packing
+ *                                                 (App. I; App. F, Prop. spec_exact).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -191,6 +194,64 @@ saki_status saki_spec_verify(const saki_rows *in, int32_t k, const int32_t *draf
                              uint64_t seed, int32_t eos_id, int32_t *accepted_len,
                              int32_t *correction, const saki_couple_out *per_pos, void *ws,
                              size_t ws_bytes, saki_stream_t stream);
+
+/* Student draft sampling for speculative rollouts (App. I, step 1).
+ * z_r ~ p_r = softmax(student row r) by the coupling's two-level exponential
+ * race on the proposal streams (0: chunks, 1: entries) of the global row
+ * g = in->row_offset + r * row_step, so a draft equals the proposal that
+ * saki_couple draws at row g (up to float rounding of near-tied race keys).
+ * With row_step = k, drafting position j of a wave whose verification rows
+ * start at G uses row_offset = G + j: draft j of sequence b is keyed by the row
+ * b*k + j that verifies it.  in->teacher is not read and may be NULL.
+ *   token      [n_rows] z_r, or -1 for a row with a non-finite student logit
+ *   row_status [n_rows] SAKI_ROW_OK / SAKI_ROW_NONFINITE, or NULL
+ * row_step >= 1; the last row's g must stay below 2^63. */
+saki_status saki_sample(const saki_rows *in, int64_t row_step, uint64_t seed, int32_t *token,
+                        uint8_t *row_status, saki_stream_t stream);
+
+/* Token-aligned trajectories of a speculative rollout (App. I, steps 7-8).
+ * Arrays of [n_seq, max_len] entries are row-major per sequence; position
+ * i of sequence b is entry b * max_len + i.  Optional arrays may be NULL. */
+#define SAKI_SEQ_RUNNING 0
+#define SAKI_SEQ_FINISHED 1 /* reached max_len, or committed eos_id                       */
+#define SAKI_SEQ_STOPPED 2  /* a wave committed nothing (bad logits or an out-of-vocabulary
+                               draft at the block's first position), or length was invalid */
+typedef struct {
+  int64_t n_seq;           /* sequences, >= 0                                               */
+  int64_t max_len;         /* positions per sequence, 0 .. 2^31 - 1                         */
+  int32_t *tokens;         /* [n_seq, max_len] committed tokens (required)                  */
+  uint8_t *corrected;      /* [n_seq, max_len] 1 at a correction, 0 at an accepted draft     */
+  float *lambda;           /* [n_seq, max_len] lambda* at the position                      */
+  float *kl;               /* [n_seq, max_len] KL(q || p)                                   */
+  float *tv;               /* [n_seq, max_len] TV(p, q)                                     */
+  float *logp_token;       /* [n_seq, max_len] log p(y)                                     */
+  float *logt_token;       /* [n_seq, max_len] log pi_T(y)                                  */
+  int32_t *teacher_argmax; /* [n_seq, max_len] v*                                           */
+  int32_t *length;         /* [n_seq] committed tokens so far; read and updated (required)  */
+  uint8_t *done;           /* [n_seq] SAKI_SEQ_*; read and updated (required)               */
+} saki_traj;
+
+/* First-rejection commit of one speculative wave (App. I, steps 7-8; App. F).
+ * Inputs are the outputs of saki_spec_verify over n_seq blocks of k positions
+ * (block b = sequence b): accepted_len and correction [n_seq], and per_pos, its
+ * per-position outputs [n_seq * k], of which token is required and lambda, kl,
+ * tv, logp_token, logt_token, teacher_argmax are copied where both sides are
+ * non-NULL (NaN / -1 where only the destination is).  For each sequence with
+ * done == SAKI_SEQ_RUNNING, the n accepted drafts and, if n < k and
+ * correction >= 0, the correction are appended at positions length .. in token
+ * order, at most max_len - length of them; every later position of the block
+ * is discarded.  Then length grows by the count m, and done becomes
+ * SAKI_SEQ_FINISHED when length reaches max_len or the last committed token is
+ * eos_id (eos_id >= 0), SAKI_SEQ_STOPPED when m = 0.  Sequences not running
+ * are left as they are.
+ *   n_commit  [n_seq] m (0 for sequences not running), or NULL
+ * The caller's model continues sequence b from the state after its committed
+ * prefix: the draft state after m - 1 drafts, advanced by the last committed
+ * token (this is the rollback of every later speculative state).
+ * Requirements: 1 <= k <= SAKI_MAX_BLOCK_K, max_len <= 2^31 - 1. */
+saki_status saki_commit(const saki_traj *traj, int32_t k, int32_t eos_id,
+                        const int32_t *accepted_len, const int32_t *correction,
+                        const saki_couple_out *per_pos, int32_t *n_commit, saki_stream_t stream);
 
 /* Placement controls (Sec. 4.1; placement-control appendix).  Rows are grouped
  * into trajectories: trajectory i holds rows [traj_offsets[i], traj_offsets[i+1])

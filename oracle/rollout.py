@@ -79,42 +79,87 @@ def committed_state(model, H, b, m, last):
     return model.advance(np.array([H[m - 1][b]]), np.array([last]))[0]
 
 
+def commit_wave(traj, k, eos_id, accepted_len, correction, per_pos):
+    """First-rejection commit of one wave into token-aligned trajectories.
+
+    traj: dict of numpy arrays tokens, corrected, teacher_argmax, lam, kl, tv,
+    logp, logt ([B, max_len]), length and done ([B]), updated in place.
+    per_pos: dict of [B * k] arrays token (the committed token of each
+    verified position: the draft where accepted, the correction where
+    rejected), lam, kl, tv, logp, logt, teacher_argmax.
+    For each running sequence b the n = accepted_len[b] accepted drafts and,
+    if n < k and correction[b] >= 0, the correction are appended, cut at
+    max_len; later positions of the block are dropped.  Returns the number m
+    committed per sequence (0 for sequences not running).
+    """
+    B = traj["length"].shape[0]
+    max_len = traj["tokens"].shape[1]
+    n_commit = np.zeros(B, np.int64)
+    for b in range(B):
+        if traj["done"][b] != DONE_RUNNING:
+            continue
+        length = int(traj["length"][b])
+        if length < 0 or length > max_len:
+            traj["done"][b] = DONE_STOPPED
+            continue
+        n = min(max(int(accepted_len[b]), 0), k)
+        want = n + (1 if n < k and correction[b] >= 0 else 0)
+        m = min(want, max_len - length)
+        for j in range(m):
+            r = b * k + j
+            pos = length + j
+            traj["tokens"][b, pos] = per_pos["token"][r]
+            traj["corrected"][b, pos] = 1 if j == n else 0
+            for key in ("lam", "kl", "tv", "logp", "logt", "teacher_argmax"):
+                traj[key][b, pos] = per_pos[key][r]
+        traj["length"][b] = length + m
+        n_commit[b] = m
+        if m == 0:
+            traj["done"][b] = DONE_STOPPED
+        elif length + m >= max_len or (eos_id >= 0 and per_pos["token"][b * k + m - 1] == eos_id):
+            traj["done"][b] = DONE_FINISHED
+    return n_commit
+
+
+def new_trajectories(B, max_len):
+    traj = dict(tokens=np.full((B, max_len), -1, np.int64),
+                corrected=np.zeros((B, max_len), np.int64),
+                teacher_argmax=np.full((B, max_len), -1, np.int64),
+                length=np.zeros(B, np.int64), done=np.zeros(B, np.int64),
+                margin=np.full((B, max_len), np.nan))
+    for key in ("lam", "kl", "tv", "logp", "logt"):
+        traj[key] = np.full((B, max_len), np.nan)
+    if max_len <= 0:
+        traj["done"][:] = DONE_FINISHED
+    return traj
+
+
 def rollout(model, prompts, k, max_len, eps, seed, eos_id=-1, chunk=CHUNK, max_waves=None):
     """Runs waves until every sequence is finished.
 
-    Returns a dict with
-      tokens [B, max_len] (-1 past the end), corrected, lam, kl, tv, logp,
-      logt, teacher_argmax (same shape, token-aligned), length [B], done [B],
-      waves (number of waves run), and min_margin [B]: the smallest decision
-      margin seen in the committed part of each sequence (the accept margin
-      |u - alpha| and the relative key gaps of the draft and correction
-      races), which says how close a sequence came to a different path.
+    Returns the trajectories of commit_wave (tokens, corrected,
+    teacher_argmax, lam, kl, tv, logp, logt [B, max_len], -1 / NaN past the
+    end; length, done [B]), plus waves (the number of waves run) and margin
+    [B, max_len]: the smallest decision margin behind each committed token
+    (the accept margin |u - alpha| and the relative key gap of the draft race
+    at that position, and at a correction the key gaps of the residual race),
+    which says how close the sequence came to a different path there.
     """
     prompts = np.asarray(prompts)
     B = prompts.shape[0]
     state = model.initial(prompts)
-    tokens = np.full((B, max_len), -1, np.int64)
-    corrected = np.zeros((B, max_len), np.int64)
-    teacher_argmax = np.full((B, max_len), -1, np.int64)
-    meta = {key: np.full((B, max_len), np.nan) for key in ("lam", "kl", "tv", "logp", "logt")}
-    length = np.zeros(B, np.int64)
-    done = np.zeros(B, np.int64)
-    min_margin = np.full(B, np.inf)
-    if max_len <= 0:
-        done[:] = DONE_FINISHED
+    traj = new_trajectories(B, max_len)
     wave = 0
     limit = max_waves if max_waves is not None else max_len + 1
-    while (done == DONE_RUNNING).any() and wave < limit:
+    while (traj["done"] == DONE_RUNNING).any() and wave < limit:
         g0 = wave * B * k
         # 1. drafting from the committed prefixes
         H = [state]
-        S = []
         Z = []
         draft_gap = []
         for j in range(k):
             s_j, _ = model.logits(H[j])
             z_j, gc, ge = draft_tokens(s_j, seed, g0 + j, k, chunk)
-            S.append(s_j)
             Z.append(z_j)
             draft_gap.append(np.minimum(gc, ge))
             H.append(model.advance(H[j], np.where(z_j >= 0, z_j, 0)))
@@ -124,47 +169,34 @@ def rollout(model, prompts, k, max_len, eps, seed, eos_id=-1, chunk=CHUNK, max_w
         drafts = np.stack(Z, axis=1).reshape(-1)
         v = verify_blocks(s_bk, t_bk, k, drafts, eps, seed, row_offset=g0, eos_id=eos_id,
                           chunk=chunk)
+        # per-position token and metadata of the verified positions
+        R = B * k
+        token = drafts.copy()
+        margin = np.minimum(v["margin"], np.stack(draft_gap, axis=1).reshape(-1))
+        for b in range(B):
+            if v["correction"][b] >= 0:
+                r = b * k + v["accepted_len"][b]
+                token[r] = v["correction"][b]
+                margin[r] = min(margin[r], v["gaps"][b, 0], v["gaps"][b, 1])
+        idx = np.clip(token, 0, t_bk.shape[1] - 1)
         logpi = np.stack([log_softmax(t_bk[r]) if np.isfinite(t_bk[r]).all()
-                          else np.full(t_bk.shape[1], np.nan) for r in range(B * k)])
-        dgap = np.stack(draft_gap, axis=1).reshape(-1)
+                          else np.full(t_bk.shape[1], np.nan) for r in range(R)])
+        per_pos = dict(token=token, lam=v["lam"], kl=v["kl"], tv=v["tv"],
+                       logp=v["logp"][np.arange(R), idx], logt=logpi[np.arange(R), idx],
+                       teacher_argmax=np.argmax(t_bk, axis=1), margin=margin)
         # 3-4. commit up to the first rejection, token-aligned metadata
+        length0 = traj["length"].copy()
+        n_commit = commit_wave(traj, k, eos_id, v["accepted_len"], v["correction"], per_pos)
         new_state = state.copy()
         for b in range(B):
-            if done[b] != DONE_RUNNING:
-                continue
-            n = int(v["accepted_len"][b])
-            c = int(v["correction"][b])
-            commit = [int(drafts[b * k + j]) for j in range(n)] + ([c] if c >= 0 else [])
-            commit = commit[:max_len - length[b]]
-            if not commit:
-                done[b] = DONE_STOPPED
-                continue
-            for j, y in enumerate(commit):
-                r = b * k + j
-                pos = length[b] + j
-                tokens[b, pos] = y
-                corrected[b, pos] = 1 if j == n else 0
-                meta["lam"][b, pos] = v["lam"][r]
-                meta["kl"][b, pos] = v["kl"][r]
-                meta["tv"][b, pos] = v["tv"][r]
-                meta["logp"][b, pos] = v["logp"][r, y]
-                meta["logt"][b, pos] = logpi[r, y]
-                teacher_argmax[b, pos] = int(np.argmax(t_bk[r]))
-                m = min(v["margin"][r], dgap[r])
-                if j == n:
-                    m = min(m, v["gaps"][b, 0], v["gaps"][b, 1])
-                min_margin[b] = min(min_margin[b], m)
-            m = len(commit)
-            new_state[b] = committed_state(model, H, b, m, commit[-1])
-            length[b] += m
-            if length[b] >= max_len or (eos_id >= 0 and commit[-1] == eos_id):
-                done[b] = DONE_FINISHED
+            m = int(n_commit[b])
+            if m > 0:
+                traj["margin"][b, length0[b]:length0[b] + m] = margin[b * k:b * k + m]
+                new_state[b] = committed_state(model, H, b, m, int(token[b * k + m - 1]))
         state = new_state
         wave += 1
-    out = dict(tokens=tokens, corrected=corrected, teacher_argmax=teacher_argmax, length=length,
-               done=done, waves=wave, min_margin=min_margin)
-    out.update(meta)
-    return out
+    traj["waves"] = wave
+    return traj
 
 
 def sequential_law(model, prompt, V, L, eps):
@@ -190,5 +222,5 @@ def sequential_law(model, prompt, V, L, eps):
     return law
 
 
-__all__ = ["committed_state", "draft_tokens", "rollout", "sequential_law", "DONE_RUNNING", "DONE_FINISHED",
+__all__ = ["commit_wave", "committed_state", "draft_tokens", "new_trajectories", "rollout", "sequential_law", "DONE_RUNNING", "DONE_FINISHED",
            "DONE_STOPPED"]

@@ -26,7 +26,9 @@ STATUS = {0: "SAKI_OK", 1: "SAKI_E_NULLPTR", 2: "SAKI_E_SHAPE", 3: "SAKI_E_VALUE
           8: "SAKI_E_LAUNCH"}
 
 EXPORTED = ["saki_workspace_bytes", "saki_couple", "saki_route_loss", "saki_spec_verify",
-            "saki_select_positions", "saki_probe_metrics", "saki_status_str", "saki_last_error"]
+            "saki_select_positions", "saki_probe_metrics", "saki_sample", "saki_commit",
+            "saki_status_str", "saki_last_error"]
+SEQ_RUNNING, SEQ_FINISHED, SEQ_STOPPED = 0, 1, 2
 SAKI_MAX_PROBE_K = 64
 
 
@@ -54,6 +56,18 @@ class SakiRouteArgs(ctypes.Structure):
                 ("grad_dtype", ctypes.c_int32), ("row_loss", ctypes.c_void_p),
                 ("loss_sum", ctypes.c_void_p), ("grad", ctypes.c_void_p),
                 ("grad_stride", ctypes.c_int64), ("correction_target", ctypes.c_int32)]
+
+
+# struct order of saki_traj after (n_seq, max_len)
+TRAJ_FIELDS = ["tokens", "corrected", "lambda", "kl", "tv", "logp_token", "logt_token",
+               "teacher_argmax", "length", "done"]
+TRAJ_DTYPES = dict(tokens=torch.int32, corrected=torch.uint8, teacher_argmax=torch.int32,
+                   length=torch.int32, done=torch.uint8)
+
+
+class SakiTraj(ctypes.Structure):
+    _fields_ = [("n_seq", ctypes.c_int64), ("max_len", ctypes.c_int64)] + \
+               [(n, ctypes.c_void_p) for n in TRAJ_FIELDS]
 
 
 class SakiError(RuntimeError):
@@ -101,6 +115,13 @@ def load(path=LIB_PATH):
     lib.saki_probe_metrics.argtypes = [ctypes.POINTER(SakiRows), ctypes.c_int32, ctypes.c_void_p,
                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.saki_sample.restype = ctypes.c_int
+    lib.saki_sample.argtypes = [ctypes.POINTER(SakiRows), ctypes.c_int64, ctypes.c_uint64,
+                                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.saki_commit.restype = ctypes.c_int
+    lib.saki_commit.argtypes = [ctypes.POINTER(SakiTraj), ctypes.c_int32, ctypes.c_int32,
+                                ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(SakiCoupleOut),
+                                ctypes.c_void_p, ctypes.c_void_p]
     lib.saki_status_str.restype = ctypes.c_char_p
     lib.saki_status_str.argtypes = [ctypes.c_int]
     lib.saki_last_error.restype = ctypes.c_char_p
@@ -116,6 +137,13 @@ def _check(status):
 
 def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dense(*ts):
+    """Per-row arrays are passed as bare pointers: they must be contiguous."""
+    for t in ts:
+        if t is not None and not t.is_contiguous():
+            raise ValueError("per-row arrays must be contiguous tensors")
 
 
 def _dtype_code(dt):
@@ -328,3 +356,54 @@ def probe_metrics(student, teacher, k=16, stream=None):
                row_status=torch.empty(n, dtype=torch.uint8, device=dev))
     saki_probe_metrics(student, teacher, k, stream=stream, **out)
     return out
+
+
+def saki_sample(student, token, seed, row_offset=0, row_step=1, row_status=None, stream=None):
+    """Call saki_sample: token[r] ~ softmax(student[r]) keyed by row_offset + r * row_step.
+
+    student is a [n_rows, V] tensor whose rows may be strided (stride(1) == 1)."""
+    load()
+    assert student.dim() == 2 and student.stride(1) == 1
+    _dense(token, row_status)
+    rows = SakiRows(_ptr(student), None, _dtype_code(student.dtype), 0, student.shape[0],
+                    student.shape[1], student.stride(0), int(row_offset))
+    st = _lib.saki_sample(ctypes.byref(rows), int(row_step), int(seed) & (2**64 - 1), _ptr(token),
+                          _ptr(row_status), _stream(stream))
+    _check(st)
+
+
+def sample(student, seed, row_offset=0, row_step=1, stream=None):
+    """Draws one token per row; allocates token (int32) and row_status (uint8)."""
+    n = student.shape[0]
+    tok = torch.empty(n, dtype=torch.int32, device=student.device)
+    status = torch.empty(n, dtype=torch.uint8, device=student.device)
+    saki_sample(student, tok, seed, row_offset, row_step, status, stream)
+    return tok, status
+
+
+def alloc_traj(n_seq, max_len, device, fields=TRAJ_FIELDS):
+    """Trajectory buffers: tokens -1, float metadata NaN, length 0, done running."""
+    out = {}
+    for f in fields:
+        dt = TRAJ_DTYPES.get(f, torch.float32)
+        shape = (n_seq,) if f in ("length", "done") else (n_seq, max_len)
+        if f == "tokens" or f == "teacher_argmax":
+            out[f] = torch.full(shape, -1, dtype=dt, device=device)
+        elif dt == torch.float32:
+            out[f] = torch.full(shape, float("nan"), dtype=dt, device=device)
+        else:
+            out[f] = torch.zeros(shape, dtype=dt, device=device)
+    return out
+
+
+def saki_commit(traj, max_len, k, eos_id, accepted_len, correction, per_pos, n_commit=None,
+                stream=None):
+    """Call saki_commit on trajectory buffers `traj` (dict of TRAJ_FIELDS tensors)."""
+    load()
+    _dense(*traj.values(), accepted_len, correction, n_commit, *per_pos.values())
+    n_seq = traj["length"].numel()
+    tr = SakiTraj(n_seq, int(max_len), *[_ptr(traj.get(f)) for f in TRAJ_FIELDS])
+    pp = _couple_struct(per_pos)
+    st = _lib.saki_commit(ctypes.byref(tr), int(k), int(eos_id), _ptr(accepted_len),
+                          _ptr(correction), ctypes.byref(pp), _ptr(n_commit), _stream(stream))
+    _check(st)

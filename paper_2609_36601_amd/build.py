@@ -7,7 +7,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libsaki.so")
 SOURCES = [os.path.join(HERE, "csrc", "saki.hip")]
-DEPS = SOURCES + [os.path.join(HERE, "csrc", f) for f in ("device_util.hpp", "row_engine.hpp", "probe.hpp")] + [
+DEPS = SOURCES + [os.path.join(HERE, "csrc", f) for f in ("device_util.hpp", "row_engine.hpp", "probe.hpp", "rollout.hpp")] + [
     os.path.join(ROOT, "include", "saki.h")]
 
 HIPCC_FLAGS = [

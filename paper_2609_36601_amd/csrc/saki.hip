@@ -324,6 +324,8 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void verify_kernel(VerifyParams P) {
   }
 }
 
+#include "rollout.hpp"
+
 // ---------------------------------------------------------------------------
 // Standalone routed loss and gradient from given events.
 // ---------------------------------------------------------------------------
@@ -591,7 +593,7 @@ saki_status device_cus(int* cus) {
   return SAKI_OK;
 }
 
-saki_status check_rows(const saki_rows* in) {
+saki_status check_rows(const saki_rows* in, bool need_teacher = true) {
   if (!in) return fail(SAKI_E_NULLPTR, "rows descriptor is NULL");
   if (in->dtype != SAKI_F32 && in->dtype != SAKI_BF16) return fail(SAKI_E_DTYPE, "unknown logits dtype");
   if (in->reserved != 0) return fail(SAKI_E_VALUE, "saki_rows.reserved must be 0");
@@ -600,8 +602,9 @@ saki_status check_rows(const saki_rows* in) {
   if (in->row_stride < in->vocab) return fail(SAKI_E_SHAPE, "row_stride < vocab");
   if (in->row_offset < 0) return fail(SAKI_E_VALUE, "row_offset < 0");
   if (in->n_rows == 0) return SAKI_OK;
-  if (!in->student || !in->teacher) return fail(SAKI_E_NULLPTR, "student or teacher pointer is NULL");
-  if (!aligned16(in->student) || !aligned16(in->teacher) ||
+  if (!in->student || (need_teacher && !in->teacher))
+    return fail(SAKI_E_NULLPTR, "student or teacher pointer is NULL");
+  if (!aligned16(in->student) || (need_teacher && !aligned16(in->teacher)) ||
       (in->row_stride * elem_size(in->dtype)) % 16 != 0)
     return fail(SAKI_E_ALIGN, "logit base pointers and row pitch must be 16-byte aligned");
   return SAKI_OK;
@@ -834,6 +837,68 @@ saki_status saki_spec_verify(const saki_rows* in, int32_t k, const int32_t* draf
   else
     hipLaunchKernelGGL(saki::verify_kernel<float>, dim3(grid), dim3(saki::NT), 0, hs, P);
   st = launched("verify_kernel");
+  if (st != SAKI_OK) return st;
+  return ok();
+}
+
+saki_status saki_sample(const saki_rows* in, int64_t row_step, uint64_t seed, int32_t* token,
+                        uint8_t* row_status, saki_stream_t stream) {
+  saki_status st = check_rows(in, false);
+  if (st != SAKI_OK) return st;
+  if (row_step < 1) return fail(SAKI_E_VALUE, "row_step < 1");
+  if (in->n_rows > 0 && (in->n_rows - 1) > (INT64_MAX - in->row_offset) / row_step)
+    return fail(SAKI_E_VALUE, "row_offset + (n_rows - 1) * row_step overflows");
+  if (in->n_rows == 0) return ok();
+  if (!token) return fail(SAKI_E_NULLPTR, "token is required");
+  int cus = 0;
+  st = device_cus(&cus);
+  if (st != SAKI_OK) return st;
+  saki::SampleParams P{};
+  P.s = in->student;
+  P.n_rows = in->n_rows;
+  P.stride = in->row_stride;
+  P.row_offset = in->row_offset;
+  P.row_step = row_step;
+  P.V = static_cast<int>(in->vocab);
+  P.seed = seed;
+  P.token = token;
+  P.status = row_status;
+  const int grid = static_cast<int>(std::min<int64_t>(P.n_rows, static_cast<int64_t>(cus) * saki::WG_PER_CU));
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (in->dtype == SAKI_BF16)
+    hipLaunchKernelGGL(saki::sample_kernel<uint16_t>, dim3(grid), dim3(saki::NT), 0, hs, P);
+  else
+    hipLaunchKernelGGL(saki::sample_kernel<float>, dim3(grid), dim3(saki::NT), 0, hs, P);
+  st = launched("sample_kernel");
+  if (st != SAKI_OK) return st;
+  return ok();
+}
+
+saki_status saki_commit(const saki_traj* traj, int32_t k, int32_t eos_id,
+                        const int32_t* accepted_len, const int32_t* correction,
+                        const saki_couple_out* per_pos, int32_t* n_commit, saki_stream_t stream) {
+  if (!traj) return fail(SAKI_E_NULLPTR, "trajectory descriptor is NULL");
+  if (k < 1 || k > SAKI_MAX_BLOCK_K) return fail(SAKI_E_SHAPE, "k outside [1, SAKI_MAX_BLOCK_K]");
+  if (traj->n_seq < 0) return fail(SAKI_E_SHAPE, "n_seq < 0");
+  if (traj->max_len < 0 || traj->max_len > INT32_MAX) return fail(SAKI_E_SHAPE, "max_len outside [0, 2^31 - 1]");
+  if (traj->n_seq == 0) return ok();
+  if (!traj->tokens || !traj->length || !traj->done)
+    return fail(SAKI_E_NULLPTR, "tokens, length and done are required");
+  if (!accepted_len || !correction || !per_pos || !per_pos->token)
+    return fail(SAKI_E_NULLPTR, "accepted_len, correction and per_pos->token are required");
+  saki::CommitParams P{};
+  P.tr = *traj;
+  P.k = k;
+  P.eos = eos_id;
+  P.accepted_len = accepted_len;
+  P.correction = correction;
+  P.pp = *per_pos;
+  P.n_commit = n_commit;
+  const int64_t grid = (traj->n_seq + 255) / 256;
+  if (grid > INT32_MAX) return fail(SAKI_E_SHAPE, "n_seq too large");
+  hipLaunchKernelGGL(saki::commit_kernel, dim3(static_cast<unsigned>(grid)), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), P);
+  saki_status st = launched("commit_kernel");
   if (st != SAKI_OK) return st;
   return ok();
 }

@@ -137,3 +137,41 @@ def test_probe_metrics_argument_errors(lib):
     assert f(ctypes.byref(_rows(vocab=8, row_stride=8)), 9, None, None, None, None, None, None, None) == 2
     assert f(ctypes.byref(_rows(n_rows=0, student=0, teacher=0)), 4, None, None, None, None, None, None,
              None) == 0
+
+
+def test_sample_argument_errors(lib):
+    f = lib.saki_sample
+    tok = ctypes.c_void_p(64)
+    assert f(None, 1, 0, tok, None, None) == 1
+    assert f(ctypes.byref(_rows()), 0, 0, tok, None, None) == 3            # row_step < 1
+    assert f(ctypes.byref(_rows(row_offset=2 ** 62)), 2 ** 62, 0, tok, None, None) == 3  # g overflows
+    assert f(ctypes.byref(_rows()), 1, 0, None, None, None) == 1           # NULL token
+    assert f(ctypes.byref(_rows(student=0)), 1, 0, tok, None, None) == 1   # NULL student
+    assert f(ctypes.byref(_rows(student=8)), 1, 0, tok, None, None) == 5   # misaligned
+    assert f(ctypes.byref(_rows(vocab=0)), 1, 0, tok, None, None) == 2
+    # the teacher is not read: NULL is fine (zero rows: no device needed)
+    assert f(ctypes.byref(_rows(n_rows=0, teacher=0)), 1, 0, tok, None, None) == 0
+
+
+def _traj(**kw):
+    t = dict(n_seq=4, max_len=8, tokens=16, length=32, done=48)
+    t.update(kw)
+    return binding.SakiTraj(**t)
+
+
+def test_commit_argument_errors(lib):
+    f = lib.saki_commit
+    pp = binding.SakiCoupleOut(token=64)
+    a, c = ctypes.c_void_p(80), ctypes.c_void_p(96)
+    assert f(None, 4, -1, a, c, ctypes.byref(pp), None, None) == 1
+    assert f(ctypes.byref(_traj()), 0, -1, a, c, ctypes.byref(pp), None, None) == 2
+    assert f(ctypes.byref(_traj()), 65, -1, a, c, ctypes.byref(pp), None, None) == 2
+    assert f(ctypes.byref(_traj(n_seq=-1)), 4, -1, a, c, ctypes.byref(pp), None, None) == 2
+    assert f(ctypes.byref(_traj(max_len=-1)), 4, -1, a, c, ctypes.byref(pp), None, None) == 2
+    assert f(ctypes.byref(_traj(max_len=2 ** 31)), 4, -1, a, c, ctypes.byref(pp), None, None) == 2
+    assert f(ctypes.byref(_traj(tokens=0)), 4, -1, a, c, ctypes.byref(pp), None, None) == 1
+    assert f(ctypes.byref(_traj(done=0)), 4, -1, a, c, ctypes.byref(pp), None, None) == 1
+    assert f(ctypes.byref(_traj()), 4, -1, None, c, ctypes.byref(pp), None, None) == 1
+    assert f(ctypes.byref(_traj()), 4, -1, a, c, None, None, None) == 1
+    assert f(ctypes.byref(_traj()), 4, -1, a, c, ctypes.byref(binding.SakiCoupleOut()), None, None) == 1
+    assert f(ctypes.byref(_traj(n_seq=0)), 4, -1, None, None, None, None, None) == 0

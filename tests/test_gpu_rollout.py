@@ -1,0 +1,223 @@
+"""GPU parity of the rollout path against the float64 oracle (oracle/rollout.py):
+draft sampling (saki_sample), the first-rejection commit (saki_commit) and whole
+multi-wave speculative rollouts on the synthetic prefix-hash model (App. I;
+App. F, Prop. spec_exact)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import bridge, coupling, rollout as orollout
+from paper_2609_36601_amd import binding, workloads
+from paper_2609_36601_amd.workloads import SyntheticAR, SyntheticARTorch
+from tests import parity
+from tests.test_gpu_parity import DEV, f64, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _random_rows(n, V, dtype, seed, scale=3.0):
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    x = torch.randn(n, V, generator=g) * scale
+    out = binding.alloc_rows(n, V, dtype, DEV)
+    out.copy_(x.to(dtype))
+    return out
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_sample_matches_oracle(saki_lib, dtype):
+    # 3 full chunks and a ragged tail; strided keys g = 1000 + 3 r
+    n, V, seed = 64, 3 * 1024 + 517, 77
+    s = _random_rows(n, V, dtype, 5)
+    say(f"sample dtype={dtype} n={n} V={V}")
+    tok, status = saki_lib.sample(s, seed, row_offset=1000, row_step=3)
+    torch.cuda.synchronize()
+    z_o, gc, ge = orollout.draft_tokens(f64(s), seed, 1000, 3)
+    tok = tok.cpu().numpy()
+    assert (status.cpu().numpy() == 0).all()
+    near = np.minimum(gc, ge) < parity.MARGIN
+    bad = (tok != z_o) & ~near
+    assert not bad.any(), f"draft differs at rows {np.nonzero(bad)[0][:10]}"
+    assert (tok == z_o).mean() > 0.95
+
+
+def test_sample_equals_couple_proposal(saki_lib):
+    s, t = workloads.rows("mid", 0, 512, device=DEV)
+    seed = workloads.coupling_seed("mid")
+    say("sample vs couple proposal, mid rows 0..512")
+    tok, _ = saki_lib.sample(s, seed, row_offset=0, row_step=1)
+    out = saki_lib.couple(s, t, 0.2, seed)
+    torch.cuda.synchronize()
+    tok = tok.cpu().numpy()
+    prop = out["proposal"].cpu().numpy()
+    diff = np.nonzero(tok != prop)[0]
+    for r in diff:
+        # allowed only where the race itself is a near tie
+        _, gc, ge = orollout.draft_tokens(f64(s[r:r + 1]), seed, int(r), 1)
+        assert min(gc[0], ge[0]) < parity.MARGIN, f"row {r}"
+    assert diff.size <= 2
+
+
+def test_sample_nonfinite_rows(saki_lib):
+    n, V = 8, 2100
+    s = _random_rows(n, V, torch.float32, 9)
+    s[1, 5] = float("nan")
+    s[3, 2099] = float("inf")
+    s[5, 1024] = float("-inf")
+    tok, status = saki_lib.sample(s, 3)
+    torch.cuda.synchronize()
+    tok, status = tok.cpu().numpy(), status.cpu().numpy()
+    bad = [1, 3, 5]
+    assert (tok[bad] == -1).all() and (status[bad] == binding.ROW_NONFINITE).all()
+    good = [0, 2, 4, 6, 7]
+    assert (status[good] == 0).all() and ((tok[good] >= 0) & (tok[good] < V)).all()
+    z_o = np.array([orollout.draft_tokens(f64(s[r:r + 1]), 3, r, 1)[0][0] for r in good])
+    assert (tok[good] == z_o).all()
+
+
+def test_commit_matches_oracle(saki_lib):
+    """saki_commit on hand-made verification outputs, every case of the commit
+    rule: full acceptance, rejection at any position, the max_len cut, EOS as a
+    draft or a correction, finished and stopped sequences, bad lengths."""
+    rng = np.random.default_rng(3)
+    B, k, L, eos = 300, 5, 12, 7
+    length = rng.integers(0, L + 1, B)
+    length[:4] = [-1, L + 3, L, L - 1]
+    done = rng.choice([0, 0, 0, 0, 1, 2], B)
+    done[:4] = 0
+    done[length == L] = 1
+    acc = rng.integers(0, k + 1, B)
+    acc[4:8] = [-2, k + 4, 0, k]
+    corr = np.where(acc < k, rng.integers(0, 20, B), -1)
+    corr[rng.random(B) < 0.1] = -1
+    tok = rng.integers(0, 20, B * k)
+    R = B * k
+    pp = dict(token=tok, lam=rng.random(R), kl=rng.random(R), tv=rng.random(R),
+              logp=-rng.random(R), logt=-rng.random(R), teacher_argmax=rng.integers(0, 20, R))
+    for b in range(B):  # the correction is the committed token at its position
+        if 0 <= acc[b] < k and corr[b] >= 0:
+            pp["token"][b * k + acc[b]] = corr[b]
+    # oracle
+    traj_o = orollout.new_trajectories(B, L)
+    traj_o["length"][:] = length
+    traj_o["done"][:] = done
+    pp32 = {key: (v.astype(np.float32).astype(np.float64) if v.dtype.kind == "f" else v)
+            for key, v in pp.items()}
+    n_o = orollout.commit_wave(traj_o, k, eos, acc, corr, pp32)
+    # GPU
+    traj = binding.alloc_traj(B, L, DEV)
+    traj["length"].copy_(torch.as_tensor(length, dtype=torch.int32))
+    traj["done"].copy_(torch.as_tensor(done, dtype=torch.uint8))
+    ppg = dict(token=torch.as_tensor(tok, dtype=torch.int32, device=DEV),
+               teacher_argmax=torch.as_tensor(pp["teacher_argmax"], dtype=torch.int32, device=DEV))
+    for a, b_ in (("lambda", "lam"), ("kl", "kl"), ("tv", "tv"), ("logp_token", "logp"),
+                  ("logt_token", "logt")):
+        ppg[a] = torch.as_tensor(pp[b_], dtype=torch.float32, device=DEV)
+    n_g = torch.empty(B, dtype=torch.int32, device=DEV)
+    say(f"commit B={B} k={k} L={L}")
+    saki_lib.saki_commit(traj, L, k, eos, torch.as_tensor(acc, dtype=torch.int32, device=DEV),
+                         torch.as_tensor(corr, dtype=torch.int32, device=DEV), ppg, n_g)
+    torch.cuda.synchronize()
+    g = {key: v.cpu().numpy() for key, v in traj.items()}
+    np.testing.assert_array_equal(n_g.cpu().numpy(), n_o)
+    np.testing.assert_array_equal(g["length"], traj_o["length"])
+    np.testing.assert_array_equal(g["done"], traj_o["done"])
+    np.testing.assert_array_equal(g["tokens"], traj_o["tokens"])
+    np.testing.assert_array_equal(g["corrected"], traj_o["corrected"])
+    np.testing.assert_array_equal(g["teacher_argmax"], traj_o["teacher_argmax"])
+    for a, b_ in (("lambda", "lam"), ("kl", "kl"), ("tv", "tv"), ("logp_token", "logp"),
+                  ("logt_token", "logt")):
+        np.testing.assert_array_equal(g[a].astype(np.float64), traj_o[b_], err_msg=a)
+    # every case occurred
+    assert (n_o == 0).any() and (n_o == k).any() and (traj_o["done"] == 2).any()
+    assert ((traj_o["tokens"] == eos).any(axis=1) & (traj_o["done"] == 1)).any()
+
+
+def _compare_rollouts(tr, o, V):
+    """Token by token up to each sequence's first near-tied decision."""
+    g = {key: v.cpu().numpy() for key, v in tr.items()}
+    B = g["length"].shape[0]
+    compared = 0
+    for b in range(B):
+        n_o = int(o["length"][b])
+        near = np.nonzero(o["margin"][b, :n_o] < parity.MARGIN)[0]
+        upto = int(near[0]) if near.size else n_o
+        if near.size:
+            say(f"sequence {b}: near tie at position {upto}")
+        else:
+            assert g["length"][b] == n_o and g["done"][b] == o["done"][b], b
+        sl = slice(0, upto)
+        np.testing.assert_array_equal(g["tokens"][b, sl], o["tokens"][b, sl], err_msg=f"seq {b}")
+        np.testing.assert_array_equal(g["corrected"][b, sl], o["corrected"][b, sl])
+        np.testing.assert_array_equal(g["teacher_argmax"][b, sl], o["teacher_argmax"][b, sl])
+        for a, b_ in (("lambda", "lam"), ("kl", "kl"), ("tv", "tv")):
+            ok = parity.close(g[a][b, sl], o[b_][b, sl])
+            assert ok.all(), (a, b, np.nonzero(~ok)[0][:5], parity.rel_err(g[a][b, sl], o[b_][b, sl]))
+        for a, b_ in (("logp_token", "logp"), ("logt_token", "logt")):
+            assert parity.close(g[a][b, sl], o[b_][b, sl], rtol=1e-5, atol=1e-6).all(), (a, b)
+        compared += upto
+    return compared
+
+
+@pytest.mark.parametrize("dtype,eos,V", [(torch.bfloat16, -1, 3000), (torch.float32, -1, 2100),
+                                         (torch.float32, 11, 64)])
+def test_rollout_matches_oracle(saki_lib, dtype, eos, V):
+    B, k, L, eps, seed = 12, 4, 20, 0.05, 1234
+    m = SyntheticAR(V, seed=9)
+    mt = SyntheticARTorch(V, seed=9, device=DEV)
+    say(f"rollout V={V} B={B} k={k} L={L} dtype={dtype} eos={eos}")
+    tr, waves = saki_lib.rollout(mt, np.arange(B), k, L, eps, seed, eos_id=eos, dtype=dtype)
+    torch.cuda.synchronize()
+    o = orollout.rollout(m, np.arange(B), k, L, eps, seed, eos_id=eos)
+    assert waves == o["waves"] or (o["margin"] < parity.MARGIN).any()
+    n = _compare_rollouts(tr, o, V)
+    say(f"compared {n} committed positions over {waves} waves")
+    assert n >= B * 5
+    assert (o["corrected"] == 1).sum() > 5  # rollbacks happened
+    if eos >= 0:
+        assert (o["length"] < L).any()
+
+
+def test_rollout_one_draft_and_long_blocks(saki_lib):
+    V, B, L, eps, seed = 1100, 6, 10, 0.1, 55
+    for k in (1, 16):
+        m = SyntheticAR(V, seed=k)
+        mt = SyntheticARTorch(V, seed=k, device=DEV)
+        say(f"rollout k={k}")
+        tr, waves = saki_lib.rollout(mt, np.arange(B), k, L, eps, seed, dtype=torch.float32,
+                                     check_every=3)
+        torch.cuda.synchronize()
+        o = orollout.rollout(m, np.arange(B), k, L, eps, seed)
+        _compare_rollouts(tr, o, V)
+
+
+def test_rollout_full_vocab_metadata(saki_lib):
+    """V = 151,936 bf16, 32 sequences x k = 8 x 24 tokens: every committed
+    position is a valid token with finite metadata, and the metadata of two
+    sequences equals the oracle's bridge at the prefixes rebuilt from their
+    committed tokens."""
+    V, B, k, L, eps, seed = 151936, 32, 8, 24, 0.2, 99
+    mt = SyntheticARTorch(V, seed=4, device=DEV)
+    say(f"rollout full vocab B={B} k={k} L={L}")
+    tr, waves = saki_lib.rollout(mt, np.arange(B), k, L, eps, seed)
+    torch.cuda.synchronize()
+    g = {key: v.cpu().numpy() for key, v in tr.items()}
+    assert (g["length"] == L).all() and (g["done"] == binding.SEQ_FINISHED).all()
+    assert ((g["tokens"] >= 0) & (g["tokens"] < V)).all()
+    assert np.isfinite(g["tv"]).all() and np.isfinite(g["lambda"]).all()
+    assert waves < L  # more than one token per wave on average
+    m = SyntheticAR(V, seed=4)
+    for b in (0, B - 1):
+        state = m.initial(np.array([b]))
+        states = []
+        for pos in range(L):
+            states.append(state[0])
+            state = m.advance(state, g["tokens"][b, pos:pos + 1].astype(np.int64))
+        # the model's logits are multiples of 1/8 in [-4, 4]: exact in bf16
+        s, t = m.logits(np.array(states, dtype=np.uint64))
+        s, t = s.astype(np.float64), t.astype(np.float64)
+        br = bridge.bridge_rows(s, t, eps)
+        assert parity.close(g["lambda"][b], br["lam"]).all()
+        assert parity.close(g["tv"][b], br["tv"]).all()
+        assert parity.close(g["kl"][b], br["kl"]).all()
+        np.testing.assert_array_equal(g["teacher_argmax"][b], np.argmax(t, axis=1))
