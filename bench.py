@@ -127,7 +127,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one 1 GiB device copy before timing (counter calibration)")
-    ap.add_argument("--workload", choices=("couple", "verify", "stream"), default="couple",
+    ap.add_argument("--workload", choices=("couple", "verify", "stream", "rollout"), default="couple",
                     help="couple: the headline (coupling + routed loss + fp32 gradient); "
                          "verify: speculative verification of 8,192 blocks of k = 8; "
                          "stream: the long-rollout stress workload, 262,144 rows in 64 chunks")
@@ -145,6 +145,8 @@ def main():
     dev = torch.device("cuda:0")
     if args.workload == "verify":
         return bench_verify(args, saki, workloads, dev)
+    if args.workload == "rollout":
+        return bench_rollout(args, saki, workloads, dev)
     if args.workload == "stream":
         return bench_stream(args, saki, workloads, dev)
     cfg = workloads.CONFIGS["large"]
@@ -330,6 +332,106 @@ def bench_verify(args, saki, workloads, dev):
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "attainable_read": attainable,
                      "frac_attainable": achieved / attainable, "traffic": None},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+ROLLOUT = dict(B=256, k=8, max_len=64, V=151936, eps=0.2, model_seed=4, seed=0x5A4B49 + 6)
+
+
+def _oracle_rollout(job):
+    import numpy as np
+    from oracle import rollout as orollout
+    from paper_2609_36601_amd import workloads
+    B, k, L, V, eps, seed, model_seed = job
+    t0 = time.process_time()
+    o = orollout.rollout(workloads.SyntheticAR(V, seed=model_seed), np.arange(B), k, L, eps, seed)
+    return time.process_time() - t0, int(o["length"].sum())
+
+
+def bench_rollout(args, saki, workloads, dev):
+    """Speculative rollout waves (App. I): 256 sequences x 64 tokens, k = 8 drafts
+    per wave, V = 151,936 bf16, eps 0.2, on the synthetic prefix-hash model.  The
+    timed figure is the library's work per rollout (draft sampling, verification,
+    commit), from events around its calls; the synthetic model's logits (the
+    stand-in for the networks) are reported apart."""
+    import torch
+    R = dict(ROLLOUT)
+    B, k, L, V, eps = R["B"], R["k"], R["max_len"], R["V"], R["eps"]
+    mt = workloads.SyntheticARTorch(V, seed=R["model_seed"], device=dev)
+    prompts = torch.arange(B)
+
+    def run(timing=None):
+        return saki.rollout(mt, prompts, k, L, eps, R["seed"], dtype=torch.bfloat16,
+                            check_every=4, timing=timing)
+
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    lib_ms, wall_ms, tokens, waves_all, evaluated = [], [], 0, [], 0
+    parts = {"sample": 0.0, "verify": 0.0, "commit": 0.0}
+    for _ in range(args.steps):
+        timing = {}
+        t0 = time.perf_counter()
+        tr, waves = run(timing)
+        torch.cuda.synchronize()
+        wall_ms.append((time.perf_counter() - t0) * 1e3)
+        ms = 0.0
+        for name in parts:
+            x = sum(a.elapsed_time(b) for a, b in timing.get(name, []))
+            parts[name] += x
+            ms += x
+        lib_ms.append(ms)
+        tokens += int(tr["length"].sum().item())
+        waves_all.append(waves)
+        for a in timing["accepted_len"]:
+            evaluated += int(torch.clamp(a.long() + 1, max=k).sum().item())
+    n = args.steps
+    ms = sum(lib_ms) / n
+    tok = tokens / n
+    # algorithmic bytes of the library per rollout: each draft step reads the B
+    # student rows once (2 V bytes each), verification reads student and teacher
+    # rows up to each block's first rejection
+    waves_mean = sum(waves_all) / n
+    bytes_per = waves_mean * k * B * V * 2 + (evaluated / n) * 2 * V * 2
+    achieved = bytes_per / (ms * 1e-3) / 1e9
+    print(f"# library ms per rollout {[round(x, 2) for x in lib_ms]}; wall ms {[round(x, 1) for x in wall_ms]}; "
+          f"waves {waves_all}; parts (ms per rollout) "
+          f"{ {k_: round(v / n, 3) for k_, v in parts.items()} }", file=sys.stderr, flush=True)
+    cpu = None
+    if not args.no_cpu_baseline:
+        # the oracle on a bounded sample of the same workload: 2 sequences x 8 tokens
+        job = (2, k, 8, V, eps, R["seed"], R["model_seed"])
+        with mp.get_context("spawn").Pool(1) as pool:
+            pool.map(_noop, range(1))
+            t0 = time.perf_counter()
+            busy, ntok = pool.map(_oracle_rollout, [job])[0]
+            wall = time.perf_counter() - t0
+        cpu = dict(value=ntok / wall, unit="committed tokens/s", cores=1, kind="oracle",
+                   sample=f"oracle rollout of 2 sequences x 8 tokens, k={k}, same V, eps and model "
+                          f"(one single-threaded process, {busy:.1f} s of CPU work)")
+    line = {
+        "metric": "speculative rollout committed tokens/sec (k=8, V=151,936 bf16; library steps)",
+        "value": tok / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 in, f32/f64 accumulation",
+        "data": "synthetic",
+        "config": {"workload": "rollout: 256 sequences x 64 tokens, k=8 drafts per wave, V=151,936 bf16, "
+                               "eps 0.2, synthetic prefix-hash student/teacher",
+                   "tokens_per_rollout": tok, "waves_per_rollout": waves_mean,
+                   "positions_verified_per_rollout": evaluated / n,
+                   "library_ms": {k_: v / n for k_, v in parts.items()},
+                   "wall_ms_with_model": sum(wall_ms) / n},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None},
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -35,12 +35,16 @@ META_FIELDS = ["lambda", "kl", "tv", "logp_token", "logt_token", "teacher_argmax
 
 
 def rollout(model, prompts, k, max_len, eps, seed, eos_id=-1, dtype=torch.bfloat16,
-            check_every=1, max_waves=None, stream=None):
+            check_every=1, max_waves=None, stream=None, timing=None):
     """Runs waves until every sequence is done; returns (trajectories, waves).
 
     trajectories: dict of device tensors as in binding.alloc_traj: tokens,
     corrected, lambda, kl, tv, logp_token, logt_token, teacher_argmax
     [B, max_len] and length, done [B].
+    timing: optional dict; if given, (start, end) event pairs recorded on the
+    current stream around the library calls are appended to timing["sample"],
+    timing["verify"] and timing["commit"], and each wave's accepted lengths
+    (a device tensor) to timing["accepted_len"].
     """
     dev = torch.device(model.device)
     prompts = torch.as_tensor(prompts, dtype=torch.int64, device=dev)
@@ -62,6 +66,17 @@ def rollout(model, prompts, k, max_len, eps, seed, eos_id=-1, dtype=torch.bfloat
     corr = torch.empty(B, dtype=torch.int32, device=dev)
     n_commit = torch.empty(B, dtype=torch.int32, device=dev)
     state = model.initial(prompts)
+
+    def timed(name, fn, *a, **kw):
+        if timing is None:
+            return fn(*a, **kw)
+        st = torch.cuda.current_stream() if stream is None else stream
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        fn(*a, **kw)
+        e1.record(st)
+        timing.setdefault(name, []).append((e0, e1))
+
     limit = max_waves if max_waves is not None else max_len + 1
     wave = 0
     while wave < limit:
@@ -69,13 +84,17 @@ def rollout(model, prompts, k, max_len, eps, seed, eos_id=-1, dtype=torch.bfloat
         H[:, 0] = state
         for j in range(k):
             model.logits_into(H[:, j], S3[:, j], None)
-            _b.saki_sample(S3[:, j], D[j], seed, row_offset=g0 + j, row_step=k, stream=stream)
+            timed("sample", _b.saki_sample, S3[:, j], D[j], seed, row_offset=g0 + j, row_step=k,
+                  stream=stream)
             H[:, j + 1] = model.advance(H[:, j], D[j].clamp(min=0))
         drafts.copy_(D.t())
         model.logits_into(H[:, :k].reshape(-1), None, T)
-        _b.saki_spec_verify(S, T, k, drafts.view(-1), eps, seed, row_offset=g0, eos_id=eos_id,
-                            accepted_len=acc, correction=corr, per_pos=pp, stream=stream)
-        _b.saki_commit(traj, max_len, k, eos_id, acc, corr, pp, n_commit, stream=stream)
+        timed("verify", _b.saki_spec_verify, S, T, k, drafts.view(-1), eps, seed, row_offset=g0,
+              eos_id=eos_id, accepted_len=acc, correction=corr, per_pos=pp, stream=stream)
+        if timing is not None:
+            timing.setdefault("accepted_len", []).append(acc.clone())
+        timed("commit", _b.saki_commit, traj, max_len, k, eos_id, acc, corr, pp, n_commit,
+              stream=stream)
         # the model continues from the committed prefix: the draft state after
         # m - 1 drafts, advanced by the last committed token (rollback of the rest)
         m = n_commit.long()
