@@ -315,26 +315,58 @@ struct StatsBlock {
   float dmin, dmax;
 };
 
+// One exchange through LDS: each wave posts its sums (relative to its own
+// running maxima), maxima, argmax and range of d; every thread then combines
+// the waves in the same fixed order, so all threads hold the same bits.
 template <int NT, typename SH>
 __device__ StatsBlock stats_combine_block(Block<NT, SH>& B, StatsAcc& a) {
+  constexpr int NW = NT / WAVE;
+  double v[8] = {a.Ss, static_cast<double>(a.S1), static_cast<double>(a.S2), static_cast<double>(a.S3),
+                 static_cast<double>(a.S4), a.St, static_cast<double>(a.T1), static_cast<double>(a.T2)};
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = wave_sum(v[i]);
+  const float wdmin = -wave_max(-a.dmin);
+  const float wdmax = wave_max(a.dmax);
+  if (B.lane == 0) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) B.sh.red_d[B.wave][i] = v[i];
+    B.sh.red_f[B.wave][0] = a.Ms;
+    B.sh.red_f[B.wave][1] = a.Mt;
+    B.sh.red_f[B.wave][2] = wdmin;
+    B.sh.red_f[B.wave][3] = wdmax;
+    B.sh.red_i[B.wave][0] = a.tidx;
+  }
+  __syncthreads();
   StatsBlock O;
-  O.ms = B.max(a.Ms);
-  O.mt = B.max(a.Mt);
-  // rescale each wave's sums to the block maxima, then add in a fixed order
-  const double gs = (a.Ms == -finf()) ? 0.0 : (a.Ms == O.ms) ? 1.0 : static_cast<double>(fexp2((a.Ms - O.ms) * LOG2E));
-  const double gt = (a.Mt == -finf()) ? 0.0 : (a.Mt == O.mt) ? 1.0 : static_cast<double>(fexp2((a.Mt - O.mt) * LOG2E));
-  double v[8] = {a.Ss * gs, static_cast<double>(a.S1) * gs, static_cast<double>(a.S2) * gs,
-                 static_cast<double>(a.S3) * gs, static_cast<double>(a.S4) * gs, a.St * gt,
-                 static_cast<double>(a.T1) * gt, static_cast<double>(a.T2) * gt};
-  B.sum(v);
-  O.Ss = v[0]; O.S1 = v[1]; O.S2 = v[2]; O.S3 = v[3]; O.S4 = v[4]; O.St = v[5]; O.T1 = v[6]; O.T2 = v[7];
-  float tb = a.Mt;
-  int ti = a.tidx;
-  B.argmax(tb, ti);
+  O.ms = -finf();
+  O.mt = -finf();
+  O.dmin = finf();
+  O.dmax = -finf();
+  for (int w = 0; w < NW; ++w) {
+    O.ms = fmaxf(O.ms, B.sh.red_f[w][0]);
+    O.mt = fmaxf(O.mt, B.sh.red_f[w][1]);
+    O.dmin = fminf(O.dmin, B.sh.red_f[w][2]);
+    O.dmax = fmaxf(O.dmax, B.sh.red_f[w][3]);
+  }
+  double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  float tb = -finf();
+  int ti = 0x7fffffff;
+  for (int w = 0; w < NW; ++w) {
+    const float wMs = B.sh.red_f[w][0], wMt = B.sh.red_f[w][1];
+    const double gs = (wMs == -finf()) ? 0.0 : (wMs == O.ms) ? 1.0 : static_cast<double>(fexp2((wMs - O.ms) * LOG2E));
+    const double gt = (wMt == -finf()) ? 0.0 : (wMt == O.mt) ? 1.0 : static_cast<double>(fexp2((wMt - O.mt) * LOG2E));
+#pragma unroll
+    for (int i = 0; i < 5; ++i) acc[i] += B.sh.red_d[w][i] * gs;
+#pragma unroll
+    for (int i = 5; i < 8; ++i) acc[i] += B.sh.red_d[w][i] * gt;
+    const int wi = B.sh.red_i[w][0];
+    if (wMt > tb || (wMt == tb && wi < ti)) { tb = wMt; ti = wi; }
+  }
+  __syncthreads();
+  O.Ss = acc[0]; O.S1 = acc[1]; O.S2 = acc[2]; O.S3 = acc[3]; O.S4 = acc[4];
+  O.St = acc[5]; O.T1 = acc[6]; O.T2 = acc[7];
   O.tbest = tb;
   O.tidx = ti;
-  O.dmin = B.min(a.dmin);
-  O.dmax = B.max(a.dmax);
   return O;
 }
 
@@ -584,7 +616,9 @@ __device__ inline double cumulant_start(const RowStats& R, double eps) {
     if (!(fp > 0)) { l = l2; break; }
     const double nl = l - f / fp;
     if (!(nl > 0.25 * l2 && nl < 4.0 * l2)) { l = l2; break; }
+    const bool done = fabs(nl - l) <= 1e-10 * l;
     l = nl;
+    if (done) break;
   }
   return l;
 }
@@ -610,8 +644,9 @@ __device__ inline double two_ended_start(const RowStats& R, double eps) {
     return v * l;
   };
   if (!(kl(1.0) > eps)) return -1.0;
+  // 2^-24 resolution: far below the error of the model itself (~1e-3)
   double lo = 0.0, hi = 1.0;
-  for (int it = 0; it < 50; ++it) {
+  for (int it = 0; it < 24; ++it) {
     const double m = 0.5 * (lo + hi);
     if (kl(m) <= eps) lo = m; else hi = m;
   }
