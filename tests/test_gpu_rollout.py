@@ -221,3 +221,62 @@ def test_rollout_full_vocab_metadata(saki_lib):
         assert parity.close(g["tv"][b], br["tv"]).all()
         assert parity.close(g["kl"][b], br["kl"]).all()
         np.testing.assert_array_equal(g["teacher_argmax"][b], np.argmax(t, axis=1))
+
+
+@pytest.mark.parametrize("V", [1, 5, 1024, 1025, 2 ** 21])
+def test_sample_vocab_edges_and_large_keys(saki_lib, V):
+    """One-entry rows, sub-chunk rows, exactly one chunk, one chunk plus one
+    entry, the largest vocabulary; row keys near 2^40."""
+    n = 4 if V == 2 ** 21 else 16
+    s = _random_rows(n, V, torch.bfloat16, V)
+    off, step, seed = 2 ** 40 + 3, 2 ** 20 + 1, 2 ** 63 + 11
+    say(f"sample edges V={V} n={n}")
+    tok, status = saki_lib.sample(s, seed, row_offset=off, row_step=step)
+    torch.cuda.synchronize()
+    tok = tok.cpu().numpy()
+    assert (status.cpu().numpy() == 0).all() and ((tok >= 0) & (tok < V)).all()
+    if V == 1:
+        assert (tok == 0).all()
+        return
+    z_o, gc, ge = orollout.draft_tokens(f64(s), seed, off, step)
+    near = np.minimum(gc, ge) < parity.MARGIN
+    assert not ((tok != z_o) & ~near).any(), np.nonzero(tok != z_o)[0]
+
+
+@pytest.mark.parametrize("same", [False, True])
+def test_rollout_without_corrections(saki_lib, same):
+    """eps = 0 (q = p), or a teacher equal to the student (q = pi = p): every
+    draft is accepted, so each wave commits k tokens, nothing is corrected, and
+    the tokens are the drafts themselves (the student's own samples)."""
+    V, B, k, L, seed = 700, 5, 4, 10, 8
+    mt = SyntheticARTorch(V, seed=2, device=DEV)
+    if same:
+        class Same:
+            V, device = mt.V, mt.device
+            initial, advance = mt.initial, mt.advance
+
+            def logits_into(self, states, s_out=None, t_out=None):
+                mt.logits_into(states, s_out, None)
+                if t_out is not None:
+                    mt.logits_into(states, t_out, None)
+        model, eps = Same(), 0.3
+    else:
+        model, eps = mt, 0.0
+    say(f"rollout without corrections same={same}")
+    tr, waves = saki_lib.rollout(model, np.arange(B), k, L, eps, seed, dtype=torch.float32)
+    torch.cuda.synchronize()
+    g = {key: v.cpu().numpy() for key, v in tr.items()}
+    assert waves == -(-L // k)
+    assert (g["length"] == L).all() and (g["corrected"] == 0).all()
+    expect_lam = 1.0 if same else 0.0
+    assert (g["lambda"] == expect_lam).all() and (g["tv"] == 0).all()
+    # the committed tokens are the student's samples at their keys
+    m = SyntheticAR(V, seed=2)
+    for b in range(B):
+        state = m.initial(np.array([b]))
+        for pos in range(L):
+            w, j = divmod(pos, k)
+            s, _ = m.logits(state)
+            z, _, _ = orollout.draft_tokens(s, seed, w * B * k + b * k + j, 1)
+            assert g["tokens"][b, pos] == z[0], (b, pos)
+            state = m.advance(state, z)
