@@ -25,10 +25,10 @@ constexpr int RED_MAX = 12;  // widest block reduction (doubles per thread)
 template <int NT>
 struct RowShared {
   static constexpr int NW = NT / WAVE;
-  float chunk_a[MAX_CHUNKS];  // proposal: reference max of s | residual: chunk mass
-  float chunk_b[MAX_CHUNKS];  // proposal: chunk sum of exp(s - reference)
-  float chunk_c[MAX_CHUNKS];  // teacher draw: reference max of t
-  float chunk_d[MAX_CHUNKS];  // teacher draw: chunk sum of exp(t - reference)
+  float chunk_a[MAX_CHUNKS];  // proposal: reference (log2 units) | residual: chunk mass
+  float chunk_b[MAX_CHUNKS];  // proposal: chunk sum of 2^(s log2 e - reference)
+  float chunk_c[MAX_CHUNKS];  // teacher draw: reference (log2 units)
+  float chunk_d[MAX_CHUNKS];  // teacher draw: chunk sum of 2^(t log2 e - reference)
   double red_d[NW][RED_MAX];
   float red_f[NW][4];
   int red_i[NW][4];
@@ -193,15 +193,23 @@ __device__ __forceinline__ void for_chunks(const T* srow, const T* trow, int V, 
 // ---------------------------------------------------------------------------
 // Stats sweep.
 // ---------------------------------------------------------------------------
+// 2^-d0 for d0 = ms log2(e) - msL, the rounding of the float shift msL.
+__device__ __forceinline__ double shift_correction(float ms, float msL) {
+  const double d0 = static_cast<double>(LOG2E) * static_cast<double>(ms) - static_cast<double>(msL);
+  return exp2(-d0);
+}
+
 struct StatsAcc {
   float Ms, Mt;                 // wave-uniform running maxima of s and t
-  double Ss, St;                // per-lane sums of exp(s - Ms), exp(t - Mt)
+  float MsL, MtL;               // Ms log2(e), Mt log2(e) rounded to float
+  double Ss, St;                // per-lane sums of 2^(s log2 e - MsL), 2^(t log2 e - MtL)
   float S1, S2, S3, S4;         // per-lane p-weighted powers of d (relative to Ms)
   float T1, T2;                 // per-lane pi-weighted sums of d, d^2 (relative to Mt)
   int tidx;                     // wave-uniform lowest index of the running max of t
   float dmin, dmax;             // per-lane range of d
   __device__ void init() {
     Ms = -finf(); Mt = -finf();
+    MsL = -finf(); MtL = -finf();
     Ss = St = 0.0;
     S1 = S2 = S3 = S4 = T1 = T2 = 0.f;
     tidx = 0x7fffffff;
@@ -212,9 +220,12 @@ struct StatsAcc {
 // Exponents are taken relative to the wave's running maxima Ms, Mt, so the
 // common chunk needs no cross-lane step before its exp2: only a chunk that
 // raises a running maximum (the wave's first chunk, then rarely) reduces it
-// over the wave and rescales the sums.  The arguments (x - M) log2(e) have
-// an exact subtraction, so the largest terms carry no rounding from the shift.
-// The proposal mass of chunk c is kept as (Ms, sum_c exp(s - Ms)).
+// over the wave and rescales the sums.  Each exponent is one fma,
+// fma(x, log2 e, -ML) with ML = M log2(e) rounded to float, rounded once, so
+// the largest terms carry no rounding from the shift; the rounding of ML itself
+// is one factor for every term sharing it, removed exactly once the row's
+// maxima are known (shift_correction).  The proposal mass of chunk c is kept as
+// (MsL, sum_c 2^(s log2 e - MsL)), i.e. ln W_c = MsL ln 2 + ln(sum).
 template <bool TAIL, typename SH>
 __device__ __forceinline__ void stats_math(const float* s, const float* t, uint32_t vm, int c,
                                            int lane, bool keep_chunks, bool keep_teacher, SH& sh,
@@ -234,10 +245,14 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
   a.dmax = fmaxf(a.dmax, lmax);
   if (wave_any(ls > a.Ms)) {
     const float cms = wave_max(ls);
-    const float f = fexp2((a.Ms - cms) * LOG2E);
+    // rounded product and difference, never contracted into one fma: the sums
+    // so far are relative to exactly the MsL the later terms use
+    const float cmsL = __fmul_rn(cms, LOG2E);
+    const float f = fexp2(__fsub_rn(a.MsL, cmsL));
     a.Ss *= static_cast<double>(f);
     a.S1 *= f; a.S2 *= f; a.S3 *= f; a.S4 *= f;
     a.Ms = cms;
+    a.MsL = cmsL;
   }
   if (wave_any(lt > a.Mt)) {
     // a new running maximum of t: its lowest index in this chunk
@@ -247,11 +262,13 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
     for (int e = EPL - 1; e >= 0; --e)
       if (SAKI_VALID(e) && t[e] == cmt) li = c * CHUNK + elem_offset(lane, e);
     a.tidx = wave_min(li);
-    const float f = fexp2((a.Mt - cmt) * LOG2E);
+    const float cmtL = __fmul_rn(cmt, LOG2E);
+    const float f = fexp2(__fsub_rn(a.MtL, cmtL));
     a.St *= static_cast<double>(f);
     a.T1 *= f;
     a.T2 *= f;
     a.Mt = cmt;
+    a.MtL = cmtL;
   }
   // normalisers: float sums of four entries (within three roundings each),
   // then double
@@ -259,8 +276,8 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
   float gs = 0.f, gt = 0.f, p1 = 0.f, p2 = 0.f, p3 = 0.f, p4 = 0.f, t1 = 0.f, t2 = 0.f;
 #pragma unroll
   for (int e = 0; e < EPL; ++e) {
-    float es = fexp2((s[e] - a.Ms) * LOG2E);
-    float et = fexp2((t[e] - a.Mt) * LOG2E);
+    float es = fexp2(fmaf(s[e], LOG2E, -a.MsL));
+    float et = fexp2(fmaf(t[e], LOG2E, -a.MtL));
     if (TAIL && !SAKI_VALID(e)) { es = 0.f; et = 0.f; }
     const float d = t[e] - s[e];
     const float ed = es * d;
@@ -285,14 +302,14 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
   if (keep_chunks) {
     const float csum = static_cast<float>(wave_sum(ps));
     if (lane == 0) {
-      sh.chunk_a[c] = a.Ms;
+      sh.chunk_a[c] = a.MsL;
       sh.chunk_b[c] = csum;
     }
   }
   if (keep_teacher) {
     const float csum = static_cast<float>(wave_sum(pt));
     if (lane == 0) {
-      sh.chunk_c[c] = a.Mt;
+      sh.chunk_c[c] = a.MtL;
       sh.chunk_d[c] = csum;
     }
   }
@@ -330,6 +347,8 @@ __device__ StatsBlock stats_combine_block(Block<NT, SH>& B, StatsAcc& a) {
   if (B.lane == 0) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) B.sh.red_d[B.wave][i] = v[i];
+    B.sh.red_d[B.wave][8] = static_cast<double>(a.MsL);
+    B.sh.red_d[B.wave][9] = static_cast<double>(a.MtL);
     B.sh.red_f[B.wave][0] = a.Ms;
     B.sh.red_f[B.wave][1] = a.Mt;
     B.sh.red_f[B.wave][2] = wdmin;
@@ -351,10 +370,15 @@ __device__ StatsBlock stats_combine_block(Block<NT, SH>& B, StatsAcc& a) {
   double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   float tb = -finf();
   int ti = 0x7fffffff;
+  // each wave's sums are relative to 2^(its MsL): rescale to the block's
+  // msL = ms log2(e) rounded (the MsL of a wave holding the maximum), then
+  // remove that rounding (shift_correction)
+  const float msL = __fmul_rn(O.ms, LOG2E), mtL = __fmul_rn(O.mt, LOG2E);
   for (int w = 0; w < NW; ++w) {
     const float wMs = B.sh.red_f[w][0], wMt = B.sh.red_f[w][1];
-    const double gs = (wMs == -finf()) ? 0.0 : (wMs == O.ms) ? 1.0 : static_cast<double>(fexp2((wMs - O.ms) * LOG2E));
-    const double gt = (wMt == -finf()) ? 0.0 : (wMt == O.mt) ? 1.0 : static_cast<double>(fexp2((wMt - O.mt) * LOG2E));
+    const float wMsL = static_cast<float>(B.sh.red_d[w][8]), wMtL = static_cast<float>(B.sh.red_d[w][9]);
+    const double gs = (wMs == -finf()) ? 0.0 : (wMs == O.ms) ? 1.0 : static_cast<double>(fexp2(__fsub_rn(wMsL, msL)));
+    const double gt = (wMt == -finf()) ? 0.0 : (wMt == O.mt) ? 1.0 : static_cast<double>(fexp2(__fsub_rn(wMtL, mtL)));
 #pragma unroll
     for (int i = 0; i < 5; ++i) acc[i] += B.sh.red_d[w][i] * gs;
 #pragma unroll
@@ -363,8 +387,9 @@ __device__ StatsBlock stats_combine_block(Block<NT, SH>& B, StatsAcc& a) {
     if (wMt > tb || (wMt == tb && wi < ti)) { tb = wMt; ti = wi; }
   }
   __syncthreads();
-  O.Ss = acc[0]; O.S1 = acc[1]; O.S2 = acc[2]; O.S3 = acc[3]; O.S4 = acc[4];
-  O.St = acc[5]; O.T1 = acc[6]; O.T2 = acc[7];
+  const double cs = shift_correction(O.ms, msL), ct = shift_correction(O.mt, mtL);
+  O.Ss = acc[0] * cs; O.S1 = acc[1] * cs; O.S2 = acc[2] * cs; O.S3 = acc[3] * cs; O.S4 = acc[4] * cs;
+  O.St = acc[5] * ct; O.T1 = acc[6] * ct; O.T2 = acc[7] * ct;
   O.tbest = tb;
   O.tidx = ti;
   return O;
@@ -446,11 +471,6 @@ struct LamEval {
   double lam, A, A1, A2, A3, A4, KL;
 };
 
-// 2^-d0 for d0 = ms log2(e) - msL, the rounding of the float shift msL.
-__device__ __forceinline__ double shift_correction(float ms, float msL) {
-  const double d0 = static_cast<double>(LOG2E) * static_cast<double>(ms) - static_cast<double>(msL);
-  return exp2(-d0);
-}
 
 // a = fma(s, log2 e, -msL) with msL = ms log2 e rounded to float: the rounding
 // of the shift, d0 = ms log2 e - msL (exact in double), is one offset for every

@@ -87,7 +87,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
 
     // z ~ p by the two-level race (chunk masses from the stats sweep)
     const int c0 = chunk_race<NT>(B, nch, P.seed, PROP_CHUNK, g, [&](int c) {
-      return static_cast<double>(sh.chunk_a[c]) + log(static_cast<double>(sh.chunk_b[c]));
+      return static_cast<double>(sh.chunk_a[c]) * LN2_D + log(static_cast<double>(sh.chunk_b[c]));
     });
     int z = elem_race<NT>(B, c0 < nch ? c0 : 0, V, P.seed, PROP_ELEM, g,
                           [&](int v) { return Loader<T>::load1(srow + v); });
@@ -111,7 +111,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
     int hot = C ? R.vstar : z;
     if (sample_target && C) {
       const int ct = chunk_race<NT>(B, nch, P.seed, TS_CHUNK, g, [&](int c) {
-        return static_cast<double>(sh.chunk_c[c]) + log(static_cast<double>(sh.chunk_d[c]));
+        return static_cast<double>(sh.chunk_c[c]) * LN2_D + log(static_cast<double>(sh.chunk_d[c]));
       });
       const int vt = elem_race<NT>(B, ct < nch ? ct : 0, V, P.seed, TS_ELEM, g,
                                    [&](int v) { return Loader<T>::load1(trow + v); });
