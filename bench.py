@@ -130,7 +130,8 @@ def main():
     ap.add_argument("--workload", choices=("couple", "verify", "stream", "rollout"), default="couple",
                     help="couple: the headline (coupling + routed loss + fp32 gradient); "
                          "verify: speculative verification of 8,192 blocks of k = 8; "
-                         "stream: the long-rollout stress workload, 262,144 rows in 64 chunks")
+                         "stream: the long-rollout stress workload, 262,144 rows in 64 chunks; "
+                         "rollout: speculative rollout waves, 256 sequences x 64 tokens, k = 8")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: this build has no multi-GPU path "

@@ -1,0 +1,39 @@
+"""Host-side behaviour of bench.py that needs no GPU."""
+import os
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _run(*args, env=None):
+    return subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *args], cwd=ROOT,
+                          capture_output=True, text=True, timeout=120, env=env)
+
+
+def test_more_than_one_gpu_is_refused():
+    r = _run("--gpus", "2")
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    env = dict(os.environ, WORLD_SIZE="4")
+    r = _run(env=env)
+    assert r.returncode == 2
+
+
+def test_help_lists_the_workloads():
+    r = _run("--help")
+    assert r.returncode == 0
+    for w in ("couple", "verify", "stream", "rollout"):
+        assert w in r.stdout
+
+
+def test_traffic_table_is_keyed_by_source_hash():
+    sys.path.insert(0, ROOT)
+    import bench
+    h = bench.kernel_source_hash()
+    assert len(h) == 64
+    t = bench.measured_traffic_bytes()
+    # either the counters were taken for exactly these sources, or traffic is unknown
+    assert (t is None) == (h not in bench.MEASURED_TRAFFIC)
+    if t is not None:
+        assert 79e9 < t < 400e9  # at least the algorithmic 79.7 GB
