@@ -21,9 +21,14 @@ def _pvalue(obs, law, n):
     """Chi-square p-value with the cells of expected count < 5 pooled."""
     e = law * n
     keep = e >= 5
-    o2 = np.append(obs[keep], obs[~keep].sum())
-    e2 = np.append(e[keep], e[~keep].sum())
-    return chisquare(o2, e2).pvalue
+    o2, e2 = obs[keep], e[keep]
+    if (~keep).any():
+        if e[~keep].sum() > 0:
+            o2 = np.append(o2, obs[~keep].sum())
+            e2 = np.append(e2, e[~keep].sum())
+        elif obs[~keep].sum() > 0:
+            return 0.0  # outcomes the law gives probability 0
+    return chisquare(o2, e2 * (o2.sum() / e2.sum())).pvalue
 
 
 def _empirical(k, seed):
