@@ -230,6 +230,8 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void verify_kernel(VerifyParams P) {
   const int nch = (V + CHUNK - 1) / CHUNK;
   const saki_couple_out& o = P.pp;
   const bool need_tv = P.has_pp && o.tv != nullptr;
+  // outputs that need lambda* at an accepted position
+  const bool need_lam = P.has_pp && (o.lambda || o.kl || o.tv || o.accept_prob || o.margin || o.logq_token);
   for (int64_t b = blockIdx.x; b < P.n_blocks; b += gridDim.x) {
     int n = P.k;
     int corr = -1;
@@ -253,10 +255,35 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void verify_kernel(VerifyParams P) {
         next_unwritten = j + 1;
         break;
       }
-      const LamResult L = lambda_search<T, NT>(B, srow, trow, V, R, P.eps);
       const float sz = Loader<T>::load1(srow + z), tz = Loader<T>::load1(trow + z);
-      const double alpha = exp(fmin(0.0, L.log_ratio(sz, tz)));
       const double u = static_cast<double>(philox_uniform(P.seed, ACCEPT, g, 0));
+      // lam x_z - A(lam) is concave in lam and 0 at lam = 0, so on [0, 1] it lies
+      // above lam (x_z - A(1)) >= min(0, log pi(z) - log p(z)): a draft with u
+      // below that bound is accepted whatever lambda* is, and when no output
+      // needs lambda* its search is skipped
+      if (!need_lam) {
+        const double lr1 = (static_cast<double>(tz) - R.lse_t) - (static_cast<double>(sz) - R.lse_s);
+        if (u < exp(fmin(0.0, lr1))) {
+          if (P.has_pp && B.tid == 0) {
+            if (o.logp_token) o.logp_token[r] = static_cast<float>(static_cast<double>(sz) - R.lse_s);
+            if (o.logt_token) o.logt_token[r] = static_cast<float>(static_cast<double>(tz) - R.lse_t);
+            if (o.proposal) o.proposal[r] = z;
+            if (o.token) o.token[r] = z;
+            if (o.teacher_argmax) o.teacher_argmax[r] = R.vstar;
+            if (o.target) o.target[r] = z;
+            if (o.corrected) o.corrected[r] = 0;
+            if (o.row_status) o.row_status[r] = SAKI_ROW_OK;
+          }
+          if (P.eos >= 0 && z == P.eos) {
+            n = j + 1;
+            next_unwritten = j + 1;
+            break;
+          }
+          continue;
+        }
+      }
+      const LamResult L = lambda_search<T, NT>(B, srow, trow, V, R, P.eps);
+      const double alpha = exp(fmin(0.0, L.log_ratio(sz, tz)));
       const bool accept = u < alpha;
       double TV = __builtin_nan("");
       const FinalConst F = final_const(R, L);

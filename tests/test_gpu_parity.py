@@ -157,6 +157,42 @@ def test_verify_blocks(saki_lib):
     say(f"mean accepted length {al.mean():.3f}")
 
 
+def test_verify_without_per_position_outputs(saki_lib):
+    """Without per-position outputs, drafts whose u lies below min(1, pi(z) / p(z))
+    (a lower bound of the accept probability for every lambda in [0, 1]) are
+    accepted without the lambda search; results equal the full path's and the
+    oracle's."""
+    k = 8
+    n = 4096 * 2
+    s, t = workloads.rows("verify", 0, n, device=DEV)
+    draft = workloads.drafts(s)
+    eps, seed = 0.2, workloads.coupling_seed("verify")
+    say(f"verify without per-position outputs n={n}")
+    full = saki_lib.spec_verify(s, t, k, draft, eps, seed)
+    lean = saki_lib.spec_verify(s, t, k, draft, eps, seed, per_pos=False)
+    torch.cuda.synchronize()
+    gpu = dict(accepted_len=lean["accepted_len"].cpu().numpy(), correction=lean["correction"].cpu().numpy())
+    same = (gpu["accepted_len"] == full["accepted_len"].cpu().numpy()) & \
+           (gpu["correction"] == full["correction"].cpu().numpy())
+    diff = np.nonzero(~same)[0]
+    say(f"blocks differing from the full path: {diff.size}")
+    assert diff.size <= 2
+    blocks = np.unique(np.concatenate([[0, 1, 2, 500, 1023], diff]))
+    idx = np.concatenate([np.arange(b * k, (b + 1) * k) for b in blocks])
+    ii = torch.as_tensor(idx, device=DEV)
+    R = parity.compare_verify(gpu, f64(s[ii]), f64(t[ii]), k, draft[ii].cpu().numpy(), eps, seed, 0,
+                              blocks)
+    say(R.summary())
+    R.check()
+    # EOS through the shortcut: p = pi accepts every draft
+    V = 300
+    s2 = torch.randn(2 * 4, V, generator=torch.Generator(device=DEV).manual_seed(3), device=DEV)
+    d2 = torch.tensor([3, 7, 5, 1, 2, 2, 2, 2], dtype=torch.int32, device=DEV)
+    out = saki_lib.spec_verify(s2, s2.clone(), 4, d2, 0.1, 5, eos_id=7, per_pos=False)
+    torch.cuda.synchronize()
+    assert out["accepted_len"].cpu().tolist() == [2, 4] and out["correction"].cpu().tolist() == [-1, -1]
+
+
 def test_verify_edge_cases(saki_lib):
     k, V = 4, 300
     rng = torch.Generator(device=DEV).manual_seed(1)
