@@ -127,6 +127,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one 1 GiB device copy before timing (counter calibration)")
+    ap.add_argument("--metadata", choices=("full", "objective"), default="full",
+                    help="rollout workload: per-token metadata kept (objective: without lambda, KL, TV)")
     ap.add_argument("--workload", choices=("couple", "verify", "stream", "rollout"), default="couple",
                     help="couple: the headline (coupling + routed loss + fp32 gradient); "
                          "verify: speculative verification of 8,192 blocks of k = 8; "
@@ -365,7 +367,7 @@ def bench_rollout(args, saki, workloads, dev):
 
     def run(timing=None):
         return saki.rollout(mt, prompts, k, L, eps, R["seed"], dtype=torch.bfloat16,
-                            check_every=4, timing=timing)
+                            check_every=4, timing=timing, metadata=args.metadata)
 
     for _ in range(args.warmup):
         run()
@@ -427,6 +429,7 @@ def bench_rollout(args, saki, workloads, dev):
         "data": "synthetic",
         "config": {"workload": "rollout: 256 sequences x 64 tokens, k=8 drafts per wave, V=151,936 bf16, "
                                "eps 0.2, synthetic prefix-hash student/teacher",
+                   "metadata": args.metadata,
                    "tokens_per_rollout": tok, "waves_per_rollout": waves_mean,
                    "positions_verified_per_rollout": evaluated / n,
                    "library_ms": {k_: v / n for k_, v in parts.items()},

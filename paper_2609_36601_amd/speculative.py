@@ -32,15 +32,22 @@ from . import binding as _b
 
 META_FIELDS = ["lambda", "kl", "tv", "logp_token", "logt_token", "teacher_argmax", "token",
                "corrected", "row_status"]
+# what the routed objective needs per committed token: the token, the
+# correction flag, the teacher mode and log p, log pi of the token (for the
+# advantage); without lambda*, KL and TV the verification can accept a draft
+# below its lambda-free accept bound without the lambda search
+OBJECTIVE_FIELDS = ["logp_token", "logt_token", "teacher_argmax", "token", "corrected", "row_status"]
 
 
 def rollout(model, prompts, k, max_len, eps, seed, eos_id=-1, dtype=torch.bfloat16,
-            check_every=1, max_waves=None, stream=None, timing=None):
+            check_every=1, max_waves=None, stream=None, timing=None, metadata="full"):
     """Runs waves until every sequence is done; returns (trajectories, waves).
 
     trajectories: dict of device tensors as in binding.alloc_traj: tokens,
     corrected, lambda, kl, tv, logp_token, logt_token, teacher_argmax
     [B, max_len] and length, done [B].
+    metadata: "full" (every field above) or "objective" (lambda, kl and tv are
+    left NaN: the fields the routed objective needs, and a faster verification).
     timing: optional dict; if given, (start, end) event pairs recorded on the
     current stream around the library calls are appended to timing["sample"],
     timing["verify"] and timing["commit"], and each wave's accepted lengths
@@ -61,7 +68,10 @@ def rollout(model, prompts, k, max_len, eps, seed, eos_id=-1, dtype=torch.bfloat
     H = torch.empty(B, k + 1, dtype=torch.int64, device=dev)
     D = torch.empty(k, B, dtype=torch.int32, device=dev)       # drafts, position-major
     drafts = torch.empty(B, k, dtype=torch.int32, device=dev)  # block-major for verification
-    pp = _b.alloc_couple_out(B * k, dev, fields=[f for f in _b.COUPLE_FIELDS if f in META_FIELDS])
+    if metadata not in ("full", "objective"):
+        raise ValueError("metadata must be 'full' or 'objective'")
+    wanted = META_FIELDS if metadata == "full" else OBJECTIVE_FIELDS
+    pp = _b.alloc_couple_out(B * k, dev, fields=[f for f in _b.COUPLE_FIELDS if f in wanted])
     acc = torch.empty(B, dtype=torch.int32, device=dev)
     corr = torch.empty(B, dtype=torch.int32, device=dev)
     n_commit = torch.empty(B, dtype=torch.int32, device=dev)

@@ -280,3 +280,22 @@ def test_rollout_without_corrections(saki_lib, same):
             z, _, _ = orollout.draft_tokens(s, seed, w * B * k + b * k + j, 1)
             assert g["tokens"][b, pos] == z[0], (b, pos)
             state = m.advance(state, z)
+
+
+def test_rollout_objective_metadata(saki_lib):
+    """metadata='objective' commits the same trajectories as 'full' (the
+    verification's lambda-free accept bound only skips work) and leaves
+    lambda, KL and TV unset."""
+    V, B, k, L, eps, seed = 3000, 12, 4, 20, 0.2, 31
+    mt = SyntheticARTorch(V, seed=9, device=DEV)
+    say("rollout objective metadata")
+    full, w1 = saki_lib.rollout(mt, np.arange(B), k, L, eps, seed)
+    obj, w2 = saki_lib.rollout(mt, np.arange(B), k, L, eps, seed, metadata="objective")
+    torch.cuda.synchronize()
+    assert w1 == w2
+    for key in ("tokens", "corrected", "teacher_argmax", "length", "done", "logp_token", "logt_token"):
+        a, b = full[key], obj[key]
+        if a.is_floating_point():
+            a, b = torch.nan_to_num(a, nan=-7.0), torch.nan_to_num(b, nan=-7.0)
+        assert torch.equal(a, b), key
+    assert torch.isnan(obj["tv"]).all() and torch.isnan(obj["lambda"]).all()
