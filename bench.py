@@ -127,7 +127,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one 1 GiB device copy before timing (counter calibration)")
-    ap.add_argument("--metadata", choices=("full", "objective"), default="full",
+    ap.add_argument("--metadata", choices=("full", "objective"), default="objective",
                     help="rollout workload: per-token metadata kept (objective: without lambda, KL, TV)")
     ap.add_argument("--workload", choices=("couple", "verify", "stream", "rollout"), default="couple",
                     help="couple: the headline (coupling + routed loss + fp32 gradient); "
