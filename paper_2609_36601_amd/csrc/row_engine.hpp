@@ -155,25 +155,27 @@ __device__ __forceinline__ void for_chunks(const T* srow, const T* trow, int V, 
   };
   if (wave < nfull) {
     // two fragment buffers used in turn: chunk c is processed while the
-    // loads of the wave's next chunk are in flight, without register copies
+    // loads of the wave's next chunk are in flight, without register copies.
+    // The next loads are issued on every path (on the wave's last chunk they
+    // re-read chunk c, unused): a load under a branch leaves a join where
+    // the compiler's wait counters must assume no younger loads, and it then
+    // waits for the next chunk's first load before processing chunk c.
     Frag<T> as, at, bs, bt;
     frag_load<LAST>(as, srow, wave, lane);
     frag_load<LAST>(at, trow, wave, lane);
     int c = wave;
     for (;;) {
       const bool more_b = c + NW < nfull;
-      if (more_b) {
-        frag_load<LAST>(bs, srow, c + NW, lane);
-        frag_load<LAST>(bt, trow, c + NW, lane);
-      }
+      const int cb = more_b ? c + NW : c;
+      frag_load<LAST>(bs, srow, cb, lane);
+      frag_load<LAST>(bt, trow, cb, lane);
       run(as, at, c);
       if (!more_b) break;
       c += NW;
       const bool more_a = c + NW < nfull;
-      if (more_a) {
-        frag_load<LAST>(as, srow, c + NW, lane);
-        frag_load<LAST>(at, trow, c + NW, lane);
-      }
+      const int ca = more_a ? c + NW : c;
+      frag_load<LAST>(as, srow, ca, lane);
+      frag_load<LAST>(at, trow, ca, lane);
       run(bs, bt, c);
       if (!more_a) break;
       c += NW;
@@ -830,11 +832,26 @@ __device__ __forceinline__ float res_weight(float s, float t, const FinalConst& 
   return p * fmaxf(em1, 0.0f);
 }
 
-template <typename T, typename G, int NT, bool GRAD, bool ACC>
-__device__ double final_sweep(Block<NT>& B, const T* srow, const T* trow, G* grow, int V,
-                              const FinalConst& F, bool keep_res, float coef, int hot) {
+// Thread of a workgroup of NT threads that holds entry v in the chunk sweeps
+// (wave c % NW of chunk c = v / CHUNK, lane and slot by elem_offset).
+template <int NT>
+__device__ __forceinline__ int entry_owner(int v) {
   constexpr int NW = NT / WAVE;
-  const int hot_chunk = hot >= 0 ? hot / CHUNK : -1;
+  const int o = v % CHUNK;
+  const int lane = (o < 512) ? (o >> 3) : ((o - 512) >> 3);
+  return ((v / CHUNK) % NW) * WAVE + lane;
+}
+
+// F is taken by value: the loop then holds its fields in registers, with no
+// reloads through a pointer that the gradient stores might alias.  The
+// gradient's indicator entry (hot) is not special-cased inside the loop: after
+// the sweep the thread that stored coef * p_hot overwrites it with
+// coef * (p_hot - 1), p_hot computed by the same expression (same thread,
+// same address, so the later store is the one that stays).
+template <typename T, typename G, int NT, bool GRAD, bool ACC>
+__device__ __forceinline__ double final_sweep(Block<NT>& B, const T* srow, const T* trow, G* grow, int V,
+                              const FinalConst F, bool keep_res, float coef, int hot) {
+  constexpr int NW = NT / WAVE;
   double TV = 0;
   for_chunks<T, NW, true>(srow, trow, V, B.wave, B.lane,
                     [&](auto tail, const float* s, const float* t, uint32_t vm, int c) {
@@ -847,17 +864,6 @@ __device__ double final_sweep(Block<NT>& B, const T* srow, const T* trow, G* gro
                         if (SAKI_VALID(e)) tv += w;
                         if (GRAD) g[e] = coef * p;
                       }
-                      if (GRAD && c == hot_chunk) {
-                        // the one entry with the indicator (wave-uniform branch)
-#pragma unroll
-                        for (int e = 0; e < EPL; ++e) {
-                          if (c * CHUNK + elem_offset(B.lane, e) == hot) {
-                            float p;
-                            res_weight<ACC>(s[e], t[e], F, &p);
-                            g[e] = coef * (p - 1.0f);
-                          }
-                        }
-                      }
                       if (keep_res) {
                         const float m = wave_sum(tv);
                         if (B.lane == 0) B.sh.chunk_a[c] = m;
@@ -865,6 +871,11 @@ __device__ double final_sweep(Block<NT>& B, const T* srow, const T* trow, G* gro
                       TV += static_cast<double>(tv);
                       if (GRAD) store_lane<G, TAIL>(grow, c, B.lane, V, g);
                     });
+  if (GRAD && hot >= 0 && hot < V && B.tid == entry_owner<NT>(hot)) {
+    const float sh_ = Loader<T>::load1(srow + hot);
+    const float p = fexp2(fmaf(sh_, LOG2E, -F.msL)) * F.invS;
+    Storer<G>::store1(grow + hot, coef * (p - 1.0f));
+  }
   double v[1] = {TV};
   B.sum(v);
   return v[0];
