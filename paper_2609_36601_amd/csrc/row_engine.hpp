@@ -22,16 +22,22 @@ namespace saki {
 
 constexpr int RED_MAX = 12;  // widest block reduction (doubles per thread)
 
-template <int NT>
+// MAXC: chunk capacity (rows of up to MAXC * CHUNK entries).  KC > 0 adds a
+// row cache of KC chunks per wave (bf16 rows): the stats sweep stores the
+// wave's last KC full chunks there and the later sweeps of the row read them
+// from LDS instead of memory (4 KiB per chunk: 1 KiB each of s and t per half).
+template <int NT, int MAXC = MAX_CHUNKS, int KC = 0>
 struct RowShared {
   static constexpr int NW = NT / WAVE;
-  float chunk_a[MAX_CHUNKS];  // proposal: reference (log2 units) | residual: chunk mass
-  float chunk_b[MAX_CHUNKS];  // proposal: chunk sum of 2^(s log2 e - reference)
-  float chunk_c[MAX_CHUNKS];  // teacher draw: reference (log2 units)
-  float chunk_d[MAX_CHUNKS];  // teacher draw: chunk sum of 2^(t log2 e - reference)
+  static constexpr int CACHE_CHUNKS = KC;
+  float chunk_a[MAXC];  // proposal: reference (log2 units) | residual: chunk mass
+  float chunk_b[MAXC];  // proposal: chunk sum of 2^(s log2 e - reference)
+  float chunk_c[MAXC];  // teacher draw: reference (log2 units)
+  float chunk_d[MAXC];  // teacher draw: chunk sum of 2^(t log2 e - reference)
   double red_d[NW][RED_MAX];
   float red_f[NW][4];
   int red_i[NW][4];
+  uint4 cache[KC > 0 ? NW * KC * 4 * WAVE : 1];  // [wave][slot][s0, s1, t0, t1][lane]
 };
 
 // Row-uniform results of the stats sweep.
@@ -116,6 +122,38 @@ struct Block {
     idx = bi;
   }
 
+  // (key, index) minimum over the block, ties to the lower index, carrying
+  // two floats of the winner along.
+  __device__ void argmin_with(float& key, int& idx, float& pa, float& pb) {
+#pragma unroll
+    for (int o = WAVE / 2; o > 0; o >>= 1) {
+      const float k2 = __shfl_xor(key, o, WAVE);
+      const int i2 = __shfl_xor(idx, o, WAVE);
+      const float a2 = __shfl_xor(pa, o, WAVE);
+      const float b2 = __shfl_xor(pb, o, WAVE);
+      if (k2 < key || (k2 == key && i2 < idx)) { key = k2; idx = i2; pa = a2; pb = b2; }
+    }
+    if (lane == 0) {
+      sh.red_f[wave][0] = key;
+      sh.red_f[wave][1] = pa;
+      sh.red_f[wave][2] = pb;
+      sh.red_i[wave][0] = idx;
+    }
+    __syncthreads();
+    float bk = sh.red_f[0][0], ba = sh.red_f[0][1], bb = sh.red_f[0][2];
+    int bi = sh.red_i[0][0];
+    for (int w = 1; w < NW; ++w) {
+      const float k2 = sh.red_f[w][0];
+      const int i2 = sh.red_i[w][0];
+      if (k2 < bk || (k2 == bk && i2 < bi)) { bk = k2; bi = i2; ba = sh.red_f[w][1]; bb = sh.red_f[w][2]; }
+    }
+    __syncthreads();
+    key = bk;
+    idx = bi;
+    pa = ba;
+    pb = bb;
+  }
+
   __device__ void argmax(float& val, int& idx) {
     wave_argmax(val, idx);
     if (lane == 0) {
@@ -142,37 +180,82 @@ struct Block {
 // std::integral_constant<bool, TAIL> (TAIL: the ragged last chunk).  Full
 // chunks are visited with the next chunk's loads already issued.  LAST marks
 // the row's last pass: its loads do not allocate in the caches.
+//
+// Row cache (bf16 rows, cache != nullptr): the wave's full chunks are
+// i = 0 .. nw-1 (chunk wave + i NW); the last kc of them are cached.
+// CACHE_FILL (stats sweep) visits every chunk from memory and stores the
+// cached ones in LDS; CACHE_USE visits the cached chunks from LDS first (while
+// the first memory chunk's loads are in flight), then the others from memory.
+// Each wave uses only its own slots, so no barrier is needed between sweeps.
 // ---------------------------------------------------------------------------
-template <typename T, int NW, bool LAST = false, typename Body>
+enum CacheMode { CACHE_NONE = 0, CACHE_FILL = 1, CACHE_USE = 2 };
+
+struct RowCache {
+  uint4* lds;  // RowShared::cache, or nullptr
+  int kc;      // cached chunks per wave
+};
+
+template <typename T, int NW, bool LAST = false, int CM = CACHE_NONE, typename Body>
 __device__ __forceinline__ void for_chunks(const T* srow, const T* trow, int V, int wave, int lane,
-                                           Body&& body) {
+                                           Body&& body, RowCache rc = RowCache{nullptr, 0}) {
+  static_assert(CM == CACHE_NONE || sizeof(T) == 2, "the row cache holds bf16 chunks");
   const int nfull = V / CHUNK;
+  const int nw = wave < nfull ? (nfull - 1 - wave) / NW + 1 : 0;  // this wave's full chunks
+  const int ncache = (CM == CACHE_NONE || rc.lds == nullptr) ? 0 : min(rc.kc, nw);
+  const int first_cached = nw - ncache;
+  const int nmem = (CM == CACHE_USE) ? first_cached : nw;  // chunks read from memory
+  auto slot = [&](int i, int part) { return rc.lds + ((wave * rc.kc + (i - first_cached)) * 4 + part) * WAVE + lane; };
   auto run = [&](const Frag<T>& fs, const Frag<T>& ft, int c) {
+    if constexpr (CM == CACHE_FILL) {
+      const int i = (c - wave) / NW;
+      if (i >= first_cached) {
+        *slot(i, 0) = fs.q[0];
+        *slot(i, 1) = fs.q[1];
+        *slot(i, 2) = ft.q[0];
+        *slot(i, 3) = ft.q[1];
+      }
+    }
     float s[EPL], t[EPL];
     frag_unpack(fs, s);
     frag_unpack(ft, t);
     body(std::integral_constant<bool, false>(), s, t, 0xffffu, c);
   };
-  if (wave < nfull) {
-    // two fragment buffers used in turn: chunk c is processed while the
-    // loads of the wave's next chunk are in flight, without register copies.
-    // The next loads are issued on every path (on the wave's last chunk they
-    // re-read chunk c, unused): a load under a branch leaves a join where
-    // the compiler's wait counters must assume no younger loads, and it then
-    // waits for the next chunk's first load before processing chunk c.
-    Frag<T> as, at, bs, bt;
+  // two fragment buffers used in turn: chunk c is processed while the
+  // loads of the wave's next chunk are in flight, without register copies.
+  // The next loads are issued on every path (on the wave's last chunk they
+  // re-read chunk c, unused): a load under a branch leaves a join where
+  // the compiler's wait counters must assume no younger loads, and it then
+  // waits for the next chunk's first load before processing chunk c.
+  Frag<T> as, at, bs, bt;
+  if (nmem > 0) {
     frag_load<LAST>(as, srow, wave, lane);
     frag_load<LAST>(at, trow, wave, lane);
+  }
+  if constexpr (CM == CACHE_USE) {
+    for (int i = first_cached; i < nw; ++i) {
+      Frag<T> cs, ct;
+      cs.q[0] = *slot(i, 0);
+      cs.q[1] = *slot(i, 1);
+      ct.q[0] = *slot(i, 2);
+      ct.q[1] = *slot(i, 3);
+      float s[EPL], t[EPL];
+      frag_unpack(cs, s);
+      frag_unpack(ct, t);
+      body(std::integral_constant<bool, false>(), s, t, 0xffffu, wave + i * NW);
+    }
+  }
+  if (nmem > 0) {
+    const int clast = wave + (nmem - 1) * NW;  // the wave's last chunk read from memory
     int c = wave;
     for (;;) {
-      const bool more_b = c + NW < nfull;
+      const bool more_b = c < clast;
       const int cb = more_b ? c + NW : c;
       frag_load<LAST>(bs, srow, cb, lane);
       frag_load<LAST>(bt, trow, cb, lane);
       run(as, at, c);
       if (!more_b) break;
       c += NW;
-      const bool more_a = c + NW < nfull;
+      const bool more_a = c < clast;
       const int ca = more_a ? c + NW : c;
       frag_load<LAST>(as, srow, ca, lane);
       frag_load<LAST>(at, trow, ca, lane);
@@ -189,6 +272,18 @@ __device__ __forceinline__ void for_chunks(const T* srow, const T* trow, int V, 
     body(std::integral_constant<bool, true>(), s, t, vm, nfull);
   }
 }
+
+// The row cache of a workgroup's shared state (none when SH has no slots or
+// the rows are not bf16).
+template <typename T, typename SH>
+__device__ __forceinline__ RowCache row_cache(SH& sh) {
+  if constexpr (SH::CACHE_CHUNKS > 0 && sizeof(T) == 2) return RowCache{sh.cache, SH::CACHE_CHUNKS};
+  return RowCache{nullptr, 0};
+}
+template <typename T, typename SH>
+constexpr int fill_mode() { return (SH::CACHE_CHUNKS > 0 && sizeof(T) == 2) ? CACHE_FILL : CACHE_NONE; }
+template <typename T, typename SH>
+constexpr int use_mode() { return (SH::CACHE_CHUNKS > 0 && sizeof(T) == 2) ? CACHE_USE : CACHE_NONE; }
 
 #define SAKI_VALID(e) (!TAIL || ((vm >> (e)) & 1u))
 
@@ -426,17 +521,17 @@ __device__ inline RowStats row_stats_from(const StatsBlock& O) {
 }
 
 // keep_chunks: store the proposal chunk masses (of p); keep_teacher: those of pi.
-template <typename T, int NT>
-__device__ RowStats stats_sweep(Block<NT>& B, const T* srow, const T* trow, int V, bool keep_chunks,
+template <typename T, int NT, typename SH>
+__device__ RowStats stats_sweep(Block<NT, SH>& B, const T* srow, const T* trow, int V, bool keep_chunks,
                                 bool keep_teacher = false) {
   constexpr int NW = NT / WAVE;
   StatsAcc a;
   a.init();
-  for_chunks<T, NW>(srow, trow, V, B.wave, B.lane,
+  for_chunks<T, NW, false, fill_mode<T, SH>()>(srow, trow, V, B.wave, B.lane,
                     [&](auto tail, const float* s, const float* t, uint32_t vm, int c) {
                       constexpr bool TAIL = decltype(tail)::value;
                       stats_math<TAIL>(s, t, vm, c, B.lane, keep_chunks, keep_teacher, B.sh, a);
-                    });
+                    }, row_cache<T>(B.sh));
   return row_stats_from(stats_combine_block(B, a));
 }
 
@@ -545,17 +640,17 @@ __device__ inline LamEval lam_finish(const double (&v)[5], double b0, float lam,
   return E;
 }
 
-template <typename T, int NT, int MODE>
-__device__ LamEval lam_sweep_mode(Block<NT>& B, const T* srow, const T* trow, int V, const RowStats& R,
+template <typename T, int NT, int MODE, typename SH>
+__device__ LamEval lam_sweep_mode(Block<NT, SH>& B, const T* srow, const T* trow, int V, const RowStats& R,
                                   float lam, float sigl) {
   constexpr int NW = NT / WAVE;
   double v[5] = {0, 0, 0, 0, 0};
   const float msL = R.ms * LOG2E;
-  for_chunks<T, NW>(srow, trow, V, B.wave, B.lane,
+  for_chunks<T, NW, false, use_mode<T, SH>()>(srow, trow, V, B.wave, B.lane,
                     [&](auto tail, const float* s, const float* t, uint32_t vm, int c) {
                       constexpr bool TAIL = decltype(tail)::value;
                       lam_math<MODE, TAIL>(s, t, vm, msL, R.cL, lam, sigl, v);
-                    });
+                    }, row_cache<T>(B.sh));
   B.sum(v);
   const double corr = shift_correction(R.ms, msL);
 #pragma unroll
@@ -565,8 +660,8 @@ __device__ LamEval lam_sweep_mode(Block<NT>& B, const T* srow, const T* trow, in
 
 // Evaluates A and its derivatives at lam over the whole row; acc selects the
 // expm1 form.  Every thread gets the same result.
-template <typename T, int NT>
-__device__ LamEval lam_sweep(Block<NT>& B, const T* srow, const T* trow, int V, const RowStats& R,
+template <typename T, int NT, typename SH>
+__device__ LamEval lam_sweep(Block<NT, SH>& B, const T* srow, const T* trow, int V, const RowStats& R,
                              float lam, bool acc) {
   const double top = static_cast<double>(lam) * (static_cast<double>(R.dmax) - R.c);  // largest lam x
   if (acc) return lam_sweep_mode<T, NT, LAM_ACC>(B, srow, trow, V, R, lam, 0.0f);
@@ -789,8 +884,8 @@ __device__ LamResult lambda_search_with(const RowStats& R, double eps, Sweep1&& 
   return out;
 }
 
-template <typename T, int NT>
-__device__ LamResult lambda_search(Block<NT>& B, const T* srow, const T* trow, int V,
+template <typename T, int NT, typename SH>
+__device__ LamResult lambda_search(Block<NT, SH>& B, const T* srow, const T* trow, int V,
                                    const RowStats& R, double eps) {
   return lambda_search_with(R, eps, [&](float lam, bool acc) {
     return lam_sweep<T, NT>(B, srow, trow, V, R, lam, acc);
@@ -844,16 +939,17 @@ __device__ __forceinline__ int entry_owner(int v) {
 
 // F is taken by value: the loop then holds its fields in registers, with no
 // reloads through a pointer that the gradient stores might alias.  The
-// gradient's indicator entry (hot) is not special-cased inside the loop: after
-// the sweep the thread that stored coef * p_hot overwrites it with
-// coef * (p_hot - 1), p_hot computed by the same expression (same thread,
-// same address, so the later store is the one that stays).
-template <typename T, typename G, int NT, bool GRAD, bool ACC>
-__device__ __forceinline__ double final_sweep(Block<NT>& B, const T* srow, const T* trow, G* grow, int V,
-                              const FinalConst F, bool keep_res, float coef, int hot) {
+// gradient's indicator entry (hot, whose logit s_hot the caller already holds)
+// is not special-cased inside the loop: after the sweep the thread that
+// stored coef * p_hot overwrites it with coef * (p_hot - 1), p_hot computed by
+// the same expression (same thread, same address, so the later store is the
+// one that stays).
+template <typename T, typename G, int NT, bool GRAD, bool ACC, typename SH>
+__device__ __forceinline__ double final_sweep(Block<NT, SH>& B, const T* srow, const T* trow, G* grow, int V,
+                              const FinalConst F, bool keep_res, float coef, int hot, float s_hot) {
   constexpr int NW = NT / WAVE;
   double TV = 0;
-  for_chunks<T, NW, true>(srow, trow, V, B.wave, B.lane,
+  for_chunks<T, NW, true, use_mode<T, SH>()>(srow, trow, V, B.wave, B.lane,
                     [&](auto tail, const float* s, const float* t, uint32_t vm, int c) {
                       constexpr bool TAIL = decltype(tail)::value;
                       float tv = 0.f, g[EPL];
@@ -870,10 +966,9 @@ __device__ __forceinline__ double final_sweep(Block<NT>& B, const T* srow, const
                       }
                       TV += static_cast<double>(tv);
                       if (GRAD) store_lane<G, TAIL>(grow, c, B.lane, V, g);
-                    });
+                    }, row_cache<T>(B.sh));
   if (GRAD && hot >= 0 && hot < V && B.tid == entry_owner<NT>(hot)) {
-    const float sh_ = Loader<T>::load1(srow + hot);
-    const float p = fexp2(fmaf(sh_, LOG2E, -F.msL)) * F.invS;
+    const float p = fexp2(fmaf(s_hot, LOG2E, -F.msL)) * F.invS;
     Storer<G>::store1(grow + hot, coef * (p - 1.0f));
   }
   double v[1] = {TV};
@@ -901,8 +996,8 @@ __device__ __forceinline__ void grad_chunk(const T* srow, G* grow, int V, int c,
   store_lane<G, TAIL>(grow, c, lane, V, g);
 }
 
-template <typename T, typename G, int NT>
-__device__ void grad_sweep(Block<NT>& B, const T* srow, G* grow, int V, float ms, double sum_s,
+template <typename T, typename G, int NT, typename SH>
+__device__ void grad_sweep(Block<NT, SH>& B, const T* srow, G* grow, int V, float ms, double sum_s,
                            float coef, int hot, bool nan_row) {
   constexpr int NW = NT / WAVE;
   const int nchunks = (V + CHUNK - 1) / CHUNK;
@@ -926,8 +1021,8 @@ __device__ void grad_sweep(Block<NT>& B, const T* srow, G* grow, int V, float ms
 
 // Chunk level.  logw(c) returns ln W_c up to a row constant, or -inf.  One
 // chunk per thread: the double-precision logs dominate, not the Philox block.
-template <int NT, typename F>
-__device__ int chunk_race(Block<NT>& B, int nchunks, uint64_t seed, uint32_t stream, uint64_t g,
+template <int NT, typename SH, typename F>
+__device__ int chunk_race(Block<NT, SH>& B, int nchunks, uint64_t seed, uint32_t stream, uint64_t g,
                           F logw) {
   double best = __builtin_huge_val();
   int bi = 0x7fffffff;
@@ -944,8 +1039,8 @@ __device__ int chunk_race(Block<NT>& B, int nchunks, uint64_t seed, uint32_t str
 }
 
 // Entry level inside chunk c.  logw(v) returns ln w_v up to a row constant, or -inf.
-template <int NT, typename F>
-__device__ int elem_race(Block<NT>& B, int c, int V, uint64_t seed, uint32_t stream, uint64_t g,
+template <int NT, typename SH, typename F>
+__device__ int elem_race(Block<NT, SH>& B, int c, int V, uint64_t seed, uint32_t stream, uint64_t g,
                          F logw) {
   float best = finf();
   int bi = 0x7fffffff;
@@ -969,6 +1064,77 @@ __device__ int elem_race(Block<NT>& B, int c, int V, uint64_t seed, uint32_t str
     }
   }
   B.argmin(best, bi);
+  return bi;
+}
+
+// The entry-level race in two halves.  elem_fetch loads this thread's four
+// consecutive entries of s and t in chunk c (one vector load per array), so
+// that a caller can issue it before a long step and hide its latency;
+// elem_pick then runs the race of elem_race on them (same uniforms, keys and
+// ties) and returns the winner with its s and t, so no later load is needed.
+// logw(s, t, v) returns ln w_v up to a row constant, or -inf.
+struct ElemFetch {
+  float s[4], t[4];
+  int v0;  // first of this thread's entries
+};
+
+template <typename T, int NT>
+__device__ __forceinline__ ElemFetch elem_fetch(const T* srow, const T* trow, int c, int V, int tid) {
+  static_assert(4 * NT >= CHUNK, "four entries per thread cover a chunk");
+  ElemFetch f;
+  const int hi = min(V, c * CHUNK + CHUNK);
+  f.v0 = c * CHUNK + 4 * tid;
+  if (f.v0 + 4 <= hi) {
+    if constexpr (sizeof(T) == 2) {
+      const uint2 qs = *reinterpret_cast<const uint2*>(srow + f.v0);
+      const uint2 qt = *reinterpret_cast<const uint2*>(trow + f.v0);
+      f.s[0] = __uint_as_float(qs.x << 16); f.s[1] = __uint_as_float(qs.x & 0xffff0000u);
+      f.s[2] = __uint_as_float(qs.y << 16); f.s[3] = __uint_as_float(qs.y & 0xffff0000u);
+      f.t[0] = __uint_as_float(qt.x << 16); f.t[1] = __uint_as_float(qt.x & 0xffff0000u);
+      f.t[2] = __uint_as_float(qt.y << 16); f.t[3] = __uint_as_float(qt.y & 0xffff0000u);
+    } else {
+      const float4 qs = *reinterpret_cast<const float4*>(srow + f.v0);
+      const float4 qt = *reinterpret_cast<const float4*>(trow + f.v0);
+      f.s[0] = qs.x; f.s[1] = qs.y; f.s[2] = qs.z; f.s[3] = qs.w;
+      f.t[0] = qt.x; f.t[1] = qt.y; f.t[2] = qt.z; f.t[3] = qt.w;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const bool in = f.v0 + k < hi;
+      f.s[k] = in ? Loader<T>::load1(srow + f.v0 + k) : 0.0f;
+      f.t[k] = in ? Loader<T>::load1(trow + f.v0 + k) : 0.0f;
+    }
+  }
+  return f;
+}
+
+template <int NT, typename SH, typename F>
+__device__ int elem_pick(Block<NT, SH>& B, const ElemFetch& f, int c, int V, uint64_t seed, uint32_t stream,
+                         uint64_t g, F logw, float* s_win, float* t_win) {
+  float best = finf(), bs = 0.0f, bt = 0.0f;
+  int bi = 0x7fffffff;
+  const int hi = min(V, c * CHUNK + CHUNK);
+  if (f.v0 < hi) {
+    const uint4 w = philox_block(seed, stream, g, static_cast<uint32_t>(f.v0 >> 2));
+    const uint32_t words[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int v = f.v0 + k;
+      if (v < hi) {
+        const float lw = logw(f.s[k], f.t[k], v);
+        if (lw > -finf()) {
+          const float u = word_to_uniform(words[k]);
+          const float E = -flog2(u) * LN2;
+          const float key = flog2(E) * LN2 - lw;
+          if (key < best) { best = key; bi = v; bs = f.s[k]; bt = f.t[k]; }
+        }
+      }
+    }
+  }
+  B.argmin_with(best, bi, bs, bt);
+  *s_win = bs;
+  *t_win = bt;
   return bi;
 }
 

@@ -20,6 +20,14 @@ namespace saki {
 
 constexpr int NT = 256;
 constexpr int WG_PER_CU = 2;
+// bf16 rows of up to CACHED_MAXC chunks (262,144 entries) use the variant with
+// a row cache of CACHE_KC chunks per wave: 4 KiB of chunk masses and 64 KiB of
+// cached chunks per workgroup, two workgroups in the 160 KiB of LDS of a CU.
+// The cached chunks are read once per row instead of three times.
+constexpr int CACHED_MAXC = 256;
+constexpr int CACHE_KC = 4;
+template <int KC>
+using RowSharedK = RowShared<NT, (KC > 0 ? CACHED_MAXC : MAX_CHUNKS), KC>;
 
 struct CoupleParams {
   const void* s;
@@ -43,10 +51,10 @@ struct CoupleParams {
 
 __device__ __forceinline__ float nanf_() { return __builtin_nanf(""); }
 
-template <typename T, typename G, bool ROUTE, bool GRAD>
+template <typename T, typename G, bool ROUTE, bool GRAD, int KC>
 __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
-  __shared__ RowShared<NT> sh;
-  Block<NT> B(sh);
+  __shared__ RowSharedK<KC> sh;
+  Block<NT, RowSharedK<KC>> B(sh);
   const int V = P.V;
   const int nch = (V + CHUNK - 1) / CHUNK;
   for (int64_t r = blockIdx.x; r < P.n_rows; r += gridDim.x) {
@@ -85,18 +93,29 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
       continue;
     }
 
-    // z ~ p by the two-level race (chunk masses from the stats sweep)
+    // z ~ p by the two-level race (chunk masses from the stats sweep): the
+    // chunk race now; the winning chunk's entries are loaded before the lambda
+    // search, which hides their latency, and raced after it.  The logit of the
+    // teacher mode (the loss and gradient at a correction) is loaded early too.
     const int c0 = chunk_race<NT>(B, nch, P.seed, PROP_CHUNK, g, [&](int c) {
       return static_cast<double>(sh.chunk_a[c]) * LN2_D + log(static_cast<double>(sh.chunk_b[c]));
     });
-    int z = elem_race<NT>(B, c0 < nch ? c0 : 0, V, P.seed, PROP_ELEM, g,
-                          [&](int v) { return Loader<T>::load1(srow + v); });
-    if (z >= V) z = R.vstar;  // unreachable for finite rows: every chunk has a winner
+    const int cz = c0 < nch ? c0 : 0;
+    const ElemFetch fz = elem_fetch<T, NT>(srow, trow, cz, V, B.tid);
+    const float s_vstar = Loader<T>::load1(srow + R.vstar);
 
     const LamResult L = lambda_search<T, NT>(B, srow, trow, V, R, P.eps);
 
+    float sz, tz;
+    int z = elem_pick<NT>(B, fz, cz, V, P.seed, PROP_ELEM, g,
+                          [&](float sv, float, int) { return sv; }, &sz, &tz);
+    if (z >= V) {  // unreachable for finite rows: every chunk has a winner
+      z = R.vstar;
+      sz = s_vstar;
+      tz = Loader<T>::load1(trow + z);
+    }
+
     // accept test, Eq. accept in the log form exp(min(0, log q(z) - log p(z)))
-    const float sz = Loader<T>::load1(srow + z), tz = Loader<T>::load1(trow + z);
     const double alpha = exp(fmin(0.0, L.log_ratio(sz, tz)));
     const double u = static_cast<double>(philox_uniform(P.seed, ACCEPT, g, 0));
     const bool C = !(u < alpha);
@@ -109,20 +128,28 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
     // the teacher mode, or a draw from pi by the same two-level race on its
     // own streams (teacher chunk masses from the stats sweep)
     int hot = C ? R.vstar : z;
+    float s_hot = C ? s_vstar : sz;
     if (sample_target && C) {
       const int ct = chunk_race<NT>(B, nch, P.seed, TS_CHUNK, g, [&](int c) {
         return static_cast<double>(sh.chunk_c[c]) * LN2_D + log(static_cast<double>(sh.chunk_d[c]));
       });
-      const int vt = elem_race<NT>(B, ct < nch ? ct : 0, V, P.seed, TS_ELEM, g,
-                                   [&](int v) { return Loader<T>::load1(trow + v); });
-      if (vt < V) hot = vt;
+      const int cc = ct < nch ? ct : 0;
+      const ElemFetch ft = elem_fetch<T, NT>(srow, trow, cc, V, B.tid);
+      float sv, tv;
+      const int vt = elem_pick<NT>(B, ft, cc, V, P.seed, TS_ELEM, g,
+                                   [&](float, float tl, int) { return tl; }, &sv, &tv);
+      if (vt < V) {
+        hot = vt;
+        s_hot = sv;
+      }
     }
 
     const FinalConst F = final_const(R, L);
-    const double TV = F.acc ? final_sweep<T, G, NT, GRAD, true>(B, srow, trow, grow, V, F, C, coef, hot)
-                            : final_sweep<T, G, NT, GRAD, false>(B, srow, trow, grow, V, F, C, coef, hot);
+    const double TV = F.acc ? final_sweep<T, G, NT, GRAD, true>(B, srow, trow, grow, V, F, C, coef, hot, s_hot)
+                            : final_sweep<T, G, NT, GRAD, false>(B, srow, trow, grow, V, F, C, coef, hot, s_hot);
 
     int y = z;
+    float sy = sz, ty = tz;
     if (C) {
       const int c1 = chunk_race<NT>(B, nch, P.seed, RES_CHUNK, g, [&](int c) {
         const float m = sh.chunk_a[c];
@@ -131,18 +158,22 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
       // a residual that rounds to zero everywhere in float (lambda* x within
       // rounding of A*) leaves no chunk with mass; the proposal is kept then
       if (c1 < nch) {
-        const int yc = elem_race<NT>(B, c1, V, P.seed, RES_ELEM, g, [&](int v) {
+        const ElemFetch fr = elem_fetch<T, NT>(srow, trow, c1, V, B.tid);
+        float sw, tw;
+        const int yc = elem_pick<NT>(B, fr, c1, V, P.seed, RES_ELEM, g, [&](float sv, float tv, int) {
           float p;
-          const float sv = Loader<T>::load1(srow + v), tv = Loader<T>::load1(trow + v);
           const float w = F.acc ? res_weight<true>(sv, tv, F, &p) : res_weight<false>(sv, tv, F, &p);
           return w > 0.0f ? flog2(w) * LN2 : -finf();
-        });
-        if (yc < V) y = yc;
+        }, &sw, &tw);
+        if (yc < V) {
+          y = yc;
+          sy = sw;
+          ty = tw;
+        }
       }
     }
 
     if (B.tid == 0) {
-      const float sy = Loader<T>::load1(srow + y), ty = Loader<T>::load1(trow + y);
       const double logp_y = static_cast<double>(sy) - R.lse_s;
       const double logt_y = static_cast<double>(ty) - R.lse_t;
       const double logq_y = logp_y + L.log_ratio(sy, ty);
@@ -165,7 +196,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
         double l = 0.0;
         if (M != 0.0f) {
           if (C) {
-            const double logp_v = static_cast<double>(Loader<T>::load1(srow + hot)) - R.lse_s;
+            const double logp_v = static_cast<double>(s_hot) - R.lse_s;
             l = -logp_v;
           } else {
             l = -adv * logp_z;
@@ -222,10 +253,10 @@ __device__ void write_skipped(const saki_couple_out& o, int64_t r, int32_t draft
   if (o.row_status) o.row_status[r] = status;
 }
 
-template <typename T>
+template <typename T, int KC>
 __global__ __launch_bounds__(NT, WG_PER_CU) void verify_kernel(VerifyParams P) {
-  __shared__ RowShared<NT> sh;
-  Block<NT> B(sh);
+  __shared__ RowSharedK<KC> sh;
+  Block<NT, RowSharedK<KC>> B(sh);
   const int V = P.V;
   const int nch = (V + CHUNK - 1) / CHUNK;
   const saki_couple_out& o = P.pp;
@@ -288,26 +319,31 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void verify_kernel(VerifyParams P) {
       double TV = __builtin_nan("");
       const FinalConst F = final_const(R, L);
       if (need_tv || !accept)
-        TV = F.acc ? final_sweep<T, float, NT, false, true>(B, srow, trow, nullptr, V, F, !accept, 0.0f, -1)
-                   : final_sweep<T, float, NT, false, false>(B, srow, trow, nullptr, V, F, !accept, 0.0f, -1);
+        TV = F.acc ? final_sweep<T, float, NT, false, true>(B, srow, trow, nullptr, V, F, !accept, 0.0f, -1, 0.0f)
+                   : final_sweep<T, float, NT, false, false>(B, srow, trow, nullptr, V, F, !accept, 0.0f, -1, 0.0f);
       int y = z;
+      float sy = sz, ty = tz;
       if (!accept) {
         const int c1 = chunk_race<NT>(B, nch, P.seed, RES_CHUNK, g, [&](int c) {
           const float m = sh.chunk_a[c];
           return m > 0.0f ? log(static_cast<double>(m)) : -__builtin_huge_val();
         });
         if (c1 < nch) {
-          const int yc = elem_race<NT>(B, c1, V, P.seed, RES_ELEM, g, [&](int v) {
+          const ElemFetch fr = elem_fetch<T, NT>(srow, trow, c1, V, B.tid);
+          float sw, tw;
+          const int yc = elem_pick<NT>(B, fr, c1, V, P.seed, RES_ELEM, g, [&](float sv, float tv, int) {
             float p;
-            const float sv = Loader<T>::load1(srow + v), tv = Loader<T>::load1(trow + v);
             const float w = F.acc ? res_weight<true>(sv, tv, F, &p) : res_weight<false>(sv, tv, F, &p);
             return w > 0.0f ? flog2(w) * LN2 : -finf();
-          });
-          if (yc < V) y = yc;
+          }, &sw, &tw);
+          if (yc < V) {
+            y = yc;
+            sy = sw;
+            ty = tw;
+          }
         }
       }
       if (P.has_pp && B.tid == 0) {
-        const float sy = Loader<T>::load1(srow + y), ty = Loader<T>::load1(trow + y);
         const double logp_y = static_cast<double>(sy) - R.lse_s;
         const double logt_y = static_cast<double>(ty) - R.lse_t;
         if (o.lambda) o.lambda[r] = L.lam;
@@ -666,7 +702,13 @@ saki_status launched(const char* what) {
 
 template <typename T, typename G, bool ROUTE, bool GRAD>
 saki_status launch_couple(const saki::CoupleParams& P, int grid, hipStream_t st) {
-  hipLaunchKernelGGL((saki::couple_kernel<T, G, ROUTE, GRAD>), dim3(grid), dim3(saki::NT), 0, st, P);
+  if constexpr (sizeof(T) == 2) {
+    if ((P.V + saki::CHUNK - 1) / saki::CHUNK <= saki::CACHED_MAXC) {
+      hipLaunchKernelGGL((saki::couple_kernel<T, G, ROUTE, GRAD, saki::CACHE_KC>), dim3(grid), dim3(saki::NT), 0, st, P);
+      return launched("couple_kernel");
+    }
+  }
+  hipLaunchKernelGGL((saki::couple_kernel<T, G, ROUTE, GRAD, 0>), dim3(grid), dim3(saki::NT), 0, st, P);
   return launched("couple_kernel");
 }
 
@@ -859,10 +901,12 @@ saki_status saki_spec_verify(const saki_rows* in, int32_t k, const int32_t* draf
   }
   const int grid = static_cast<int>(std::min<int64_t>(P.n_blocks, static_cast<int64_t>(cus) * saki::WG_PER_CU));
   hipStream_t hs = static_cast<hipStream_t>(stream);
-  if (in->dtype == SAKI_BF16)
-    hipLaunchKernelGGL(saki::verify_kernel<uint16_t>, dim3(grid), dim3(saki::NT), 0, hs, P);
+  if (in->dtype == SAKI_BF16 && (P.V + saki::CHUNK - 1) / saki::CHUNK <= saki::CACHED_MAXC)
+    hipLaunchKernelGGL((saki::verify_kernel<uint16_t, saki::CACHE_KC>), dim3(grid), dim3(saki::NT), 0, hs, P);
+  else if (in->dtype == SAKI_BF16)
+    hipLaunchKernelGGL((saki::verify_kernel<uint16_t, 0>), dim3(grid), dim3(saki::NT), 0, hs, P);
   else
-    hipLaunchKernelGGL(saki::verify_kernel<float>, dim3(grid), dim3(saki::NT), 0, hs, P);
+    hipLaunchKernelGGL((saki::verify_kernel<float, 0>), dim3(grid), dim3(saki::NT), 0, hs, P);
   st = launched("verify_kernel");
   if (st != SAKI_OK) return st;
   return ok();
