@@ -239,6 +239,33 @@ def test_edge_vocab_sizes_and_special_rows(saki_lib):
             run_and_compare(saki_lib, s, t, eps, 99, row_offset=10, valid=valid)
 
 
+@pytest.mark.parametrize("V", [16 * 1024, 17 * 1024 + 5, 256 * 1024, 256 * 1024 + 1])
+def test_row_cache_boundaries(saki_lib, V):
+    """bf16 rows of up to 256 chunks keep each wave's last four full chunks in
+    LDS: every chunk cached (16 chunks), one chunk per wave past that plus a
+    ragged tail, the largest cached row (256 chunks), and one entry more (the
+    variant without the cache).  Coupling, loss and gradient against the
+    oracle on every row; the verify kernel on the same rows, whose blocks
+    stop at their first rejection."""
+    g = torch.Generator(device=DEV).manual_seed(V)
+    n = 8
+    s = (3.0 * torch.randn(n, V, generator=g, device=DEV) / 0.7).to(torch.bfloat16)
+    t = (0.7 * s.float() + 0.7 * 3.0 * torch.randn(n, V, generator=g, device=DEV)).to(torch.bfloat16)
+    s, t = padded(s), padded(t)
+    run_and_compare(saki_lib, s, t, 0.2, 4242, row_offset=3)
+    k = 4
+    draft = workloads.drafts(s)
+    out = saki_lib.spec_verify(s, t, k, draft, 0.2, 4242, 3)
+    torch.cuda.synchronize()
+    gpu = dict(accepted_len=out["accepted_len"].cpu().numpy(),
+               correction=out["correction"].cpu().numpy(),
+               per_pos=np_out(out["per_pos"]))
+    R = parity.compare_verify(gpu, f64(s), f64(t), k, draft.cpu().numpy(), 0.2, 4242, 3,
+                              np.arange(n // k))
+    say(R.summary())
+    R.check()
+
+
 def test_bf16_gradient_and_masks(saki_lib):
     s, t = workloads.rows("mid", 0, 64, device=DEV)
     valid = (np.arange(64) % 3 != 0).astype(np.uint8)
