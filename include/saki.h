@@ -189,7 +189,12 @@ saki_status saki_route_loss(const void *student, int32_t dtype, int64_t n_rows, 
  *   per_pos      optional per-position outputs ([n_rows], fields may be NULL):
  *                positions after the end of the committed prefix get NaN / -1
  *                and row_status SAKI_ROW_SKIPPED; proposal = the draft, token =
- *                the committed token. */
+ *                the committed token.
+ *   ws           required: ws_bytes >= saki_workspace_bytes(SAKI_OP_VERIFY, n_rows,
+ *                vocab) (256 bytes), 4-byte aligned; it holds the counter from
+ *                which workgroups take blocks, cleared by the call on `stream`.
+ *                Calls that may run at the same time need separate workspaces.
+ * More than 2^31 - 1 blocks is SAKI_E_SHAPE. */
 saki_status saki_spec_verify(const saki_rows *in, int32_t k, const int32_t *draft, double eps,
                              uint64_t seed, int32_t eos_id, int32_t *accepted_len,
                              int32_t *correction, const saki_couple_out *per_pos, void *ws,

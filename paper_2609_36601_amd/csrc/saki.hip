@@ -234,7 +234,14 @@ struct VerifyParams {
   int32_t* correction;
   saki_couple_out pp;  // per-position outputs (fields may be NULL)
   int has_pp;
+  unsigned int* next_block;  // work counter in the caller's workspace, zero at launch
 };
+
+// Clears the verify work counter (a kernel rather than a memset node, so that a
+// captured graph replays it correctly).
+__global__ void clear_counter_kernel(unsigned int* c) {
+  if (threadIdx.x == 0) *c = 0u;
+}
 
 __device__ void write_skipped(const saki_couple_out& o, int64_t r, int32_t draft, uint8_t status) {
   if (o.lambda) o.lambda[r] = nanf_();
@@ -263,7 +270,21 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void verify_kernel(VerifyParams P) {
   const bool need_tv = P.has_pp && o.tv != nullptr;
   // outputs that need lambda* at an accepted position
   const bool need_lam = P.has_pp && (o.lambda || o.kl || o.tv || o.accept_prob || o.margin || o.logq_token);
-  for (int64_t b = blockIdx.x; b < P.n_blocks; b += gridDim.x) {
+  // Blocks cost one to k positions, so workgroups take them from a counter
+  // (dynamic scheduling) rather than with a fixed stride.  Thread 0 takes the
+  // next index and posts it in LDS; readfirstlane makes the index, and so the
+  // loop's exit, uniform in every wave, so all threads reach the same
+  // barriers.  Each iteration takes a new block or ends the loop, so at most
+  // n_blocks + 1 iterations run.
+  __shared__ unsigned int next_b;
+  for (int64_t it = 0; it <= P.n_blocks; ++it) {
+    if (threadIdx.x == 0) next_b = atomicAdd(P.next_block, 1u);
+    __syncthreads();
+    const unsigned int bu = static_cast<unsigned int>(__builtin_amdgcn_readfirstlane(static_cast<int>(next_b)));
+    __syncthreads();
+    // unsigned: n_blocks < 2^31 and the counter stays below n_blocks + grid
+    if (bu >= static_cast<unsigned int>(P.n_blocks)) break;
+    const int64_t b = static_cast<int64_t>(bu);
     int n = P.k;
     int corr = -1;
     int next_unwritten = P.k;  // first position whose per-position outputs are not yet written
@@ -739,7 +760,7 @@ size_t saki_workspace_bytes(int op, int64_t n_rows, int64_t vocab) {
     case SAKI_OP_ROUTE:
       return loss_ws_bytes(n_rows);
     case SAKI_OP_VERIFY:
-      return 0;
+      return 256;  // the work counter
     case SAKI_OP_SELECT:
       return loss_ws_bytes(n_rows);
     default:
@@ -868,8 +889,6 @@ saki_status saki_spec_verify(const saki_rows* in, int32_t k, const int32_t* draf
                              uint64_t seed, int32_t eos_id, int32_t* accepted_len,
                              int32_t* correction, const saki_couple_out* per_pos, void* ws,
                              size_t ws_bytes, saki_stream_t stream) {
-  (void)ws;
-  (void)ws_bytes;
   saki_status st = check_rows(in);
   if (st != SAKI_OK) return st;
   if (k < 1 || k > SAKI_MAX_BLOCK_K) return fail(SAKI_E_SHAPE, "k outside [1, SAKI_MAX_BLOCK_K]");
@@ -878,6 +897,10 @@ saki_status saki_spec_verify(const saki_rows* in, int32_t k, const int32_t* draf
   if (in->n_rows == 0) return ok();
   if (!draft || !accepted_len || !correction)
     return fail(SAKI_E_NULLPTR, "draft, accepted_len and correction are required");
+  if (in->n_rows / k >= (int64_t{1} << 31)) return fail(SAKI_E_SHAPE, "more than 2^31 - 1 blocks");
+  if (!ws || ws_bytes < saki_workspace_bytes(SAKI_OP_VERIFY, in->n_rows, in->vocab))
+    return fail(SAKI_E_WORKSPACE, "workspace NULL or smaller than saki_workspace_bytes(SAKI_OP_VERIFY)");
+  if ((reinterpret_cast<uintptr_t>(ws) & 3u) != 0) return fail(SAKI_E_ALIGN, "workspace must be 4-byte aligned");
   int cus = 0;
   st = device_cus(&cus);
   if (st != SAKI_OK) return st;
@@ -899,8 +922,12 @@ saki_status saki_spec_verify(const saki_rows* in, int32_t k, const int32_t* draf
     P.pp = *per_pos;
     P.has_pp = 1;
   }
+  P.next_block = static_cast<unsigned int*>(ws);
   const int grid = static_cast<int>(std::min<int64_t>(P.n_blocks, static_cast<int64_t>(cus) * saki::WG_PER_CU));
   hipStream_t hs = static_cast<hipStream_t>(stream);
+  hipLaunchKernelGGL(saki::clear_counter_kernel, dim3(1), dim3(64), 0, hs, P.next_block);
+  st = launched("clear_counter_kernel");
+  if (st != SAKI_OK) return st;
   if (in->dtype == SAKI_BF16 && (P.V + saki::CHUNK - 1) / saki::CHUNK <= saki::CACHED_MAXC)
     hipLaunchKernelGGL((saki::verify_kernel<uint16_t, saki::CACHE_KC>), dim3(grid), dim3(saki::NT), 0, hs, P);
   else if (in->dtype == SAKI_BF16)

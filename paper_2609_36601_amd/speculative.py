@@ -75,6 +75,7 @@ def rollout(model, prompts, k, max_len, eps, seed, eos_id=-1, dtype=torch.bfloat
     acc = torch.empty(B, dtype=torch.int32, device=dev)
     corr = torch.empty(B, dtype=torch.int32, device=dev)
     n_commit = torch.empty(B, dtype=torch.int32, device=dev)
+    ws = torch.empty(max(_b.workspace_bytes(_b.SAKI_OP_VERIFY, B * k, V), 8), dtype=torch.uint8, device=dev)
     state = model.initial(prompts)
 
     def timed(name, fn, *a, **kw):
@@ -100,7 +101,7 @@ def rollout(model, prompts, k, max_len, eps, seed, eos_id=-1, dtype=torch.bfloat
         drafts.copy_(D.t())
         model.logits_into(H[:, :k].reshape(-1), None, T)
         timed("verify", _b.saki_spec_verify, S, T, k, drafts.view(-1), eps, seed, row_offset=g0,
-              eos_id=eos_id, accepted_len=acc, correction=corr, per_pos=pp, stream=stream)
+              eos_id=eos_id, accepted_len=acc, correction=corr, per_pos=pp, workspace=ws, stream=stream)
         if timing is not None:
             timing.setdefault("accepted_len", []).append(acc.clone())
         timed("commit", _b.saki_commit, traj, max_len, k, eos_id, acc, corr, pp, n_commit,
