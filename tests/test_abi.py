@@ -92,6 +92,15 @@ def test_verify_and_route_argument_errors(lib):
     assert not_multiple == 2
     no_draft = lib.saki_spec_verify(ctypes.byref(rows), 3, None, 0.1, 1, -1, acc, acc, None, None, 0, None)
     assert no_draft == 1
+    # the block work counter lives in the caller's workspace: required, sized, aligned
+    assert lib.saki_workspace_bytes(binding.SAKI_OP_VERIFY, 6, 32) == 256
+    assert lib.saki_workspace_bytes(binding.SAKI_OP_VERIFY, 0, 32) == 0
+    no_ws = lib.saki_spec_verify(ctypes.byref(rows), 3, 64, 0.1, 1, -1, acc, acc, None, None, 0, None)
+    assert no_ws == 6 and b"workspace" in lib.saki_last_error()
+    small_ws = lib.saki_spec_verify(ctypes.byref(rows), 3, 64, 0.1, 1, -1, acc, acc, None, 256, 128, None)
+    assert small_ws == 6
+    odd_ws = lib.saki_spec_verify(ctypes.byref(rows), 3, 64, 0.1, 1, -1, acc, acc, None, 258, 256, None)
+    assert odd_ws == 5
 
     rt = binding.SakiRouteArgs(None, 1.0, 0, None, None, None, 0)
     assert lib.saki_route_loss(16, 9, 4, 64, 64, 64, 64, 64, 64, ctypes.byref(rt), None, 0, None) == 4
