@@ -158,7 +158,13 @@ size_t saki_workspace_bytes(int op, int64_t n_rows, int64_t vocab);
  *   seed   64-bit Philox key
  *   out    per-row outputs (any field may be NULL); out itself may not be NULL
  *   route  NULL for coupling only
- *   ws     workspace of ws_bytes >= saki_workspace_bytes(SAKI_OP_COUPLE, ...) */
+ *   ws     required when n_rows > 0: ws_bytes >= saki_workspace_bytes(SAKI_OP_COUPLE,
+ *          n_rows, vocab), 8-byte aligned.  Its first 256 bytes hold the counter from
+ *          which workgroups take rows (cleared by the call on `stream`); with
+ *          route->loss_sum the scaled row losses follow.  Calls that may run at the
+ *          same time need separate workspaces.
+ * More than 2^31 - 1 rows in one call is SAKI_E_SHAPE (split the rows into calls
+ * with row_offset; results do not change). */
 saki_status saki_couple(const saki_rows *in, double eps, uint64_t seed, const saki_couple_out *out,
                         const saki_route_args *route, void *ws, size_t ws_bytes,
                         saki_stream_t stream);

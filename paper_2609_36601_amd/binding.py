@@ -262,7 +262,6 @@ def couple(student, teacher, eps, seed, row_offset=0, route=False, grad_dtype=No
     dev = student.device
     out = alloc_couple_out(n, dev)
     rargs = None
-    ws = None
     if route:
         rargs = dict(valid_mask=valid_mask, grad_scale=grad_scale,
                      row_loss=torch.empty(n, dtype=torch.float32, device=dev),
@@ -270,8 +269,7 @@ def couple(student, teacher, eps, seed, row_offset=0, route=False, grad_dtype=No
                      correction_target=correction_target)
         if grad_dtype is not None:
             rargs["grad"] = alloc_rows(n, V, grad_dtype, dev)
-        nb = workspace_bytes(SAKI_OP_COUPLE, n, V)
-        ws = torch.empty(max(nb, 8), dtype=torch.uint8, device=dev)
+    ws = torch.empty(max(workspace_bytes(SAKI_OP_COUPLE, n, V), 8), dtype=torch.uint8, device=dev)
     saki_couple(student, teacher, eps, seed, row_offset, out, rargs, ws, stream)
     if rargs is not None:
         out.update({k: v for k, v in rargs.items() if k in ("row_loss", "loss_sum", "grad")})

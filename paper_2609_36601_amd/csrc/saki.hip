@@ -47,9 +47,28 @@ struct CoupleParams {
   void* grad;
   int64_t grad_stride;
   int target_mode;      // SAKI_TARGET_MODE or SAKI_TARGET_SAMPLE
+  unsigned int* next_row;  // work counter in the caller's workspace, zero at launch
 };
 
 __device__ __forceinline__ float nanf_() { return __builtin_nanf(""); }
+
+// Clears a work counter (a kernel rather than a memset node, so that a
+// captured graph replays it correctly).
+__global__ void clear_counter_kernel(unsigned int* c) {
+  if (threadIdx.x == 0) *c = 0u;
+}
+
+// Takes the next work item (row or block) for the whole workgroup: thread 0
+// takes it from the counter with a device atomic and posts it in LDS, and
+// readfirstlane makes the index, and so the caller's loop exit, uniform in
+// every wave, so all threads reach the same barriers.
+__device__ __forceinline__ unsigned int take_next(unsigned int* counter, unsigned int* slot) {
+  if (threadIdx.x == 0) *slot = atomicAdd(counter, 1u);
+  __syncthreads();
+  const unsigned int v = static_cast<unsigned int>(__builtin_amdgcn_readfirstlane(static_cast<int>(*slot)));
+  __syncthreads();
+  return v;
+}
 
 template <typename T, typename G, bool ROUTE, bool GRAD, int KC>
 __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
@@ -57,7 +76,16 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
   Block<NT, RowSharedK<KC>> B(sh);
   const int V = P.V;
   const int nch = (V + CHUNK - 1) / CHUNK;
-  for (int64_t r = blockIdx.x; r < P.n_rows; r += gridDim.x) {
+  // Workgroups take rows from a counter: their speeds differ (the two
+  // workgroups of a CU, and CUs, get unequal shares of the memory system), so
+  // a fixed stride left the slowest ones finishing ~15% after the median.
+  // Each iteration takes a new row or ends the loop: at most n_rows + 1.
+  __shared__ unsigned int next_r;
+  for (int64_t it = 0; it <= P.n_rows; ++it) {
+    const unsigned int ru = take_next(P.next_row, &next_r);
+    // unsigned: n_rows < 2^31 and the counter stays below n_rows + grid
+    if (ru >= static_cast<unsigned int>(P.n_rows)) break;
+    const int64_t r = static_cast<int64_t>(ru);
     const T* srow = static_cast<const T*>(P.s) + r * P.stride;
     const T* trow = static_cast<const T*>(P.t) + r * P.stride;
     G* grow = GRAD ? static_cast<G*>(P.grad) + r * P.grad_stride : nullptr;
@@ -237,12 +265,6 @@ struct VerifyParams {
   unsigned int* next_block;  // work counter in the caller's workspace, zero at launch
 };
 
-// Clears the verify work counter (a kernel rather than a memset node, so that a
-// captured graph replays it correctly).
-__global__ void clear_counter_kernel(unsigned int* c) {
-  if (threadIdx.x == 0) *c = 0u;
-}
-
 __device__ void write_skipped(const saki_couple_out& o, int64_t r, int32_t draft, uint8_t status) {
   if (o.lambda) o.lambda[r] = nanf_();
   if (o.kl) o.kl[r] = nanf_();
@@ -271,17 +293,11 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void verify_kernel(VerifyParams P) {
   // outputs that need lambda* at an accepted position
   const bool need_lam = P.has_pp && (o.lambda || o.kl || o.tv || o.accept_prob || o.margin || o.logq_token);
   // Blocks cost one to k positions, so workgroups take them from a counter
-  // (dynamic scheduling) rather than with a fixed stride.  Thread 0 takes the
-  // next index and posts it in LDS; readfirstlane makes the index, and so the
-  // loop's exit, uniform in every wave, so all threads reach the same
-  // barriers.  Each iteration takes a new block or ends the loop, so at most
-  // n_blocks + 1 iterations run.
+  // (dynamic scheduling) rather than with a fixed stride.  Each iteration
+  // takes a new block or ends the loop, so at most n_blocks + 1 iterations run.
   __shared__ unsigned int next_b;
   for (int64_t it = 0; it <= P.n_blocks; ++it) {
-    if (threadIdx.x == 0) next_b = atomicAdd(P.next_block, 1u);
-    __syncthreads();
-    const unsigned int bu = static_cast<unsigned int>(__builtin_amdgcn_readfirstlane(static_cast<int>(next_b)));
-    __syncthreads();
+    const unsigned int bu = take_next(P.next_block, &next_b);
     // unsigned: n_blocks < 2^31 and the counter stays below n_blocks + grid
     if (bu >= static_cast<unsigned int>(P.n_blocks)) break;
     const int64_t b = static_cast<int64_t>(bu);
@@ -757,6 +773,7 @@ size_t saki_workspace_bytes(int op, int64_t n_rows, int64_t vocab) {
   if (n_rows <= 0) return 0;
   switch (op) {
     case SAKI_OP_COUPLE:
+      return 256 + loss_ws_bytes(n_rows);  // the row counter, then the scaled row losses
     case SAKI_OP_ROUTE:
       return loss_ws_bytes(n_rows);
     case SAKI_OP_VERIFY:
@@ -777,12 +794,13 @@ saki_status saki_couple(const saki_rows* in, double eps, uint64_t seed, const sa
   bool want_sum = false;
   st = check_route(route, in->vocab, &want_sum);
   if (st != SAKI_OK) return st;
-  if (want_sum) {
-    if (!ws) return fail(SAKI_E_WORKSPACE, "workspace is NULL but loss_sum is requested");
-    if (ws_bytes < loss_ws_bytes(in->n_rows)) return fail(SAKI_E_WORKSPACE, "workspace too small");
-    if ((reinterpret_cast<uintptr_t>(ws) & 7u) != 0) return fail(SAKI_E_ALIGN, "workspace must be 8-byte aligned");
-  }
   if (in->n_rows == 0) return ok();
+  if (in->n_rows >= (int64_t{1} << 31)) return fail(SAKI_E_SHAPE, "more than 2^31 - 1 rows in one call");
+  if (!ws) return fail(SAKI_E_WORKSPACE, "workspace is NULL");
+  if (ws_bytes < saki_workspace_bytes(SAKI_OP_COUPLE, in->n_rows, in->vocab))
+    return fail(SAKI_E_WORKSPACE, "workspace smaller than saki_workspace_bytes(SAKI_OP_COUPLE)");
+  if ((reinterpret_cast<uintptr_t>(ws) & 7u) != 0) return fail(SAKI_E_ALIGN, "workspace must be 8-byte aligned");
+  double* const row_losses = reinterpret_cast<double*>(static_cast<char*>(ws) + 256);
   int cus = 0;
   st = device_cus(&cus);
   if (st != SAKI_OK) return st;
@@ -800,13 +818,17 @@ saki_status saki_couple(const saki_rows* in, double eps, uint64_t seed, const sa
     P.valid = route->valid_mask;
     P.grad_scale = route->grad_scale;
     P.row_loss = route->row_loss;
-    P.scaled_loss = want_sum ? static_cast<double*>(ws) : nullptr;
+    P.scaled_loss = want_sum ? row_losses : nullptr;
     P.grad = route->grad;
     P.grad_stride = route->grad_stride;
     P.target_mode = route->correction_target;
   }
+  P.next_row = static_cast<unsigned int*>(ws);
   const int grid = static_cast<int>(std::min<int64_t>(in->n_rows, static_cast<int64_t>(cus) * saki::WG_PER_CU));
   hipStream_t hs = static_cast<hipStream_t>(stream);
+  hipLaunchKernelGGL(saki::clear_counter_kernel, dim3(1), dim3(64), 0, hs, P.next_row);
+  st = launched("clear_counter_kernel");
+  if (st != SAKI_OK) return st;
   const bool grad = route && route->grad;
   st = (in->dtype == SAKI_BF16)
            ? dispatch_couple<uint16_t>(P, route != nullptr, grad, route ? route->grad_dtype : 0, grid, hs)
@@ -814,7 +836,7 @@ saki_status saki_couple(const saki_rows* in, double eps, uint64_t seed, const sa
   if (st != SAKI_OK) return st;
   if (want_sum) {
     hipLaunchKernelGGL(saki::loss_sum_kernel, dim3(1), dim3(1024), 0, hs,
-                       static_cast<const double*>(ws), in->n_rows, route->loss_sum);
+                       static_cast<const double*>(row_losses), in->n_rows, route->loss_sum);
     st = launched("loss_sum_kernel");
     if (st != SAKI_OK) return st;
   }

@@ -71,6 +71,13 @@ def test_argument_errors_without_launch(lib):
     rt = binding.SakiRouteArgs(None, 1.0, 0, None, 64, None, 0)     # loss_sum, no workspace
     assert _couple(lib, _rows(), route=rt) == 6
     assert _couple(lib, _rows(), route=rt, ws=256, ws_bytes=8) == 6  # too small
+    # the row work counter needs a workspace on every call with rows
+    assert _couple(lib, _rows()) == 6
+    need = lib.saki_workspace_bytes(binding.SAKI_OP_COUPLE, 4, 64)
+    assert need == 256 + 256                                         # counter + 4 doubles, rounded
+    assert _couple(lib, _rows(), ws=256, ws_bytes=need - 1) == 6
+    assert _couple(lib, _rows(), ws=260, ws_bytes=need) == 5         # not 8-byte aligned
+    assert _couple(lib, _rows(n_rows=1 << 31), ws=256, ws_bytes=1 << 40) == 2
     rt = binding.SakiRouteArgs(None, float("inf"), 0, None, None, None, 0)
     assert _couple(lib, _rows(), route=rt) == 3
     rt = binding.SakiRouteArgs(None, 1.0, 0, None, None, 48, 32)    # grad stride < vocab
