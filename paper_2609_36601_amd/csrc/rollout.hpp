@@ -23,11 +23,10 @@ struct SampleParams {
   uint8_t* status;
 };
 
-template <typename T, bool TAIL>
-__device__ __forceinline__ bool chunk_mass(const T* srow, int V, int c, int lane, float* ref, float* sum) {
-  float s[EPL];
-  uint32_t vm;
-  load_lane<T, TAIL>(srow, c, lane, V, s, &vm);
+// Mass of one chunk from this lane's 16 entries s (valid mask vm): the chunk's
+// maximum and the sum of 2^((s - max) log2 e) over the wave.
+template <bool TAIL>
+__device__ __forceinline__ bool chunk_mass(const float* s, uint32_t vm, float* ref, float* sum) {
   float m = -finf();
   bool fin = true;
 #pragma unroll
@@ -46,37 +45,42 @@ __device__ __forceinline__ bool chunk_mass(const T* srow, int V, int c, int lane
   return fin;
 }
 
+// One workgroup of SNT = 512 threads (eight waves) per row and one workgroup
+// per CU: rollout batches are a few hundred rows, so a row's sweep is spread
+// over more waves, each streaming its chunks with the next chunk's loads in
+// flight (the row engine's chunk loop, on the one array).
+constexpr int SAMPLE_NT = 512;
+
 template <typename T>
-__global__ __launch_bounds__(NT, WG_PER_CU) void sample_kernel(SampleParams P) {
-  __shared__ RowShared<NT> sh;
-  Block<NT> B(sh);
-  constexpr int NW = NT / WAVE;
+__global__ __launch_bounds__(SAMPLE_NT, 1) void sample_kernel(SampleParams P) {
+  constexpr int SNT = SAMPLE_NT;
+  __shared__ RowShared<SNT> sh;
+  Block<SNT> B(sh);
+  constexpr int NW = SNT / WAVE;
   const int V = P.V;
   const int nch = (V + CHUNK - 1) / CHUNK;
-  const bool ragged = (V % CHUNK) != 0;
   for (int64_t r = blockIdx.x; r < P.n_rows; r += gridDim.x) {
     const T* srow = static_cast<const T*>(P.s) + r * P.stride;
     const uint64_t g = static_cast<uint64_t>(P.row_offset + r * P.row_step);
     bool fin = true;
-    for (int c = B.wave; c < nch; c += NW) {
+    for_chunks1<T, NW>(srow, V, B.wave, B.lane, [&](auto tail, const float* s, uint32_t vm, int c) {
+      constexpr bool TAIL = decltype(tail)::value;
       float ref, sum;
-      const bool f = (ragged && c == nch - 1) ? chunk_mass<T, true>(srow, V, c, B.lane, &ref, &sum)
-                                              : chunk_mass<T, false>(srow, V, c, B.lane, &ref, &sum);
-      fin = fin && f;
+      fin = chunk_mass<TAIL>(s, vm, &ref, &sum) && fin;
       if (B.lane == 0) {
         sh.chunk_a[c] = ref;
         sh.chunk_b[c] = sum;
       }
-    }
+    });
     // the block max is also the barrier that publishes the chunk masses
     const bool finite = B.max(fin ? 0.0f : 1.0f) == 0.0f;
     int z = -1;
     if (finite) {
-      const int c0 = chunk_race<NT>(B, nch, P.seed, PROP_CHUNK, g, [&](int c) {
+      const int c0 = chunk_race<SNT>(B, nch, P.seed, PROP_CHUNK, g, [&](int c) {
         return static_cast<double>(sh.chunk_a[c]) + log(static_cast<double>(sh.chunk_b[c]));
       });
-      z = elem_race<NT>(B, c0 < nch ? c0 : 0, V, P.seed, PROP_ELEM, g,
-                        [&](int v) { return Loader<T>::load1(srow + v); });
+      z = elem_race<SNT>(B, c0 < nch ? c0 : 0, V, P.seed, PROP_ELEM, g,
+                         [&](int v) { return Loader<T>::load1(srow + v); });
       if (z >= V) z = -1;  // unreachable for finite rows: every chunk has a winner
     }
     if (B.tid == 0) {

@@ -273,6 +273,45 @@ __device__ __forceinline__ void for_chunks(const T* srow, const T* trow, int V, 
   }
 }
 
+// The chunk loop over one array: body(tail, x, vm, c) gets this lane's 16
+// entries of chunk c; full chunks with the next chunk's loads in flight.
+template <typename T, int NW, typename Body>
+__device__ __forceinline__ void for_chunks1(const T* row, int V, int wave, int lane, Body&& body) {
+  const int nfull = V / CHUNK;
+  if (wave < nfull) {
+    const int clast = wave + ((nfull - 1 - wave) / NW) * NW;  // the wave's last full chunk
+    Frag<T> fa, fb;
+    frag_load<false>(fa, row, wave, lane);
+    int c = wave;
+    for (;;) {
+      const bool more_b = c < clast;
+      frag_load<false>(fb, row, more_b ? c + NW : c, lane);
+      {
+        float x[EPL];
+        frag_unpack(fa, x);
+        body(std::integral_constant<bool, false>(), x, 0xffffu, c);
+      }
+      if (!more_b) break;
+      c += NW;
+      const bool more_a = c < clast;
+      frag_load<false>(fa, row, more_a ? c + NW : c, lane);
+      {
+        float x[EPL];
+        frag_unpack(fb, x);
+        body(std::integral_constant<bool, false>(), x, 0xffffu, c);
+      }
+      if (!more_a) break;
+      c += NW;
+    }
+  }
+  if ((V % CHUNK) != 0 && (nfull % NW) == wave) {
+    float x[EPL];
+    uint32_t vm;
+    load_lane<T, true>(row, nfull, lane, V, x, &vm);
+    body(std::integral_constant<bool, true>(), x, vm, nfull);
+  }
+}
+
 // The row cache of a workgroup's shared state (none when SH has no slots or
 // the rows are not bf16).
 template <typename T, typename SH>

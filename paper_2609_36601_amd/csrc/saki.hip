@@ -983,12 +983,12 @@ saki_status saki_sample(const saki_rows* in, int64_t row_step, uint64_t seed, in
   P.seed = seed;
   P.token = token;
   P.status = row_status;
-  const int grid = static_cast<int>(std::min<int64_t>(P.n_rows, static_cast<int64_t>(cus) * saki::WG_PER_CU));
+  const int grid = static_cast<int>(std::min<int64_t>(P.n_rows, static_cast<int64_t>(cus)));
   hipStream_t hs = static_cast<hipStream_t>(stream);
   if (in->dtype == SAKI_BF16)
-    hipLaunchKernelGGL(saki::sample_kernel<uint16_t>, dim3(grid), dim3(saki::NT), 0, hs, P);
+    hipLaunchKernelGGL(saki::sample_kernel<uint16_t>, dim3(grid), dim3(saki::SAMPLE_NT), 0, hs, P);
   else
-    hipLaunchKernelGGL(saki::sample_kernel<float>, dim3(grid), dim3(saki::NT), 0, hs, P);
+    hipLaunchKernelGGL(saki::sample_kernel<float>, dim3(grid), dim3(saki::SAMPLE_NT), 0, hs, P);
   st = launched("sample_kernel");
   if (st != SAKI_OK) return st;
   return ok();
