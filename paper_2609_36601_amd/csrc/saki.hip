@@ -282,10 +282,14 @@ __device__ void write_skipped(const saki_couple_out& o, int64_t r, int32_t draft
   if (o.row_status) o.row_status[r] = status;
 }
 
-template <typename T, int KC>
-__global__ __launch_bounds__(NT, WG_PER_CU) void verify_kernel(VerifyParams P) {
-  __shared__ RowSharedK<KC> sh;
-  Block<NT, RowSharedK<KC>> B(sh);
+// VNT threads per workgroup: 256 (two workgroups per CU) for large batches,
+// 512 (one per CU) when a call has no more blocks than CUs, as in rollouts,
+// so that each position's sweeps are spread over eight waves.
+template <typename T, int KC, int VNT>
+__global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyParams P) {
+  using SH = RowShared<VNT, (KC > 0 ? CACHED_MAXC : MAX_CHUNKS), KC>;
+  __shared__ SH sh;
+  Block<VNT, SH> B(sh);
   const int V = P.V;
   const int nch = (V + CHUNK - 1) / CHUNK;
   const saki_couple_out& o = P.pp;
@@ -316,7 +320,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void verify_kernel(VerifyParams P) {
         next_unwritten = j + 1;
         break;
       }
-      const RowStats R = stats_sweep<T, NT>(B, srow, trow, V, false);
+      const RowStats R = stats_sweep<T, VNT>(B, srow, trow, V, false);
       if (!R.finite) {
         if (P.has_pp && B.tid == 0) write_skipped(o, r, z, SAKI_ROW_NONFINITE);
         n = j;
@@ -350,25 +354,25 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void verify_kernel(VerifyParams P) {
           continue;
         }
       }
-      const LamResult L = lambda_search<T, NT>(B, srow, trow, V, R, P.eps);
+      const LamResult L = lambda_search<T, VNT>(B, srow, trow, V, R, P.eps);
       const double alpha = exp(fmin(0.0, L.log_ratio(sz, tz)));
       const bool accept = u < alpha;
       double TV = __builtin_nan("");
       const FinalConst F = final_const(R, L);
       if (need_tv || !accept)
-        TV = F.acc ? final_sweep<T, float, NT, false, true>(B, srow, trow, nullptr, V, F, !accept, 0.0f, -1, 0.0f)
-                   : final_sweep<T, float, NT, false, false>(B, srow, trow, nullptr, V, F, !accept, 0.0f, -1, 0.0f);
+        TV = F.acc ? final_sweep<T, float, VNT, false, true>(B, srow, trow, nullptr, V, F, !accept, 0.0f, -1, 0.0f)
+                   : final_sweep<T, float, VNT, false, false>(B, srow, trow, nullptr, V, F, !accept, 0.0f, -1, 0.0f);
       int y = z;
       float sy = sz, ty = tz;
       if (!accept) {
-        const int c1 = chunk_race<NT>(B, nch, P.seed, RES_CHUNK, g, [&](int c) {
+        const int c1 = chunk_race<VNT>(B, nch, P.seed, RES_CHUNK, g, [&](int c) {
           const float m = sh.chunk_a[c];
           return m > 0.0f ? log(static_cast<double>(m)) : -__builtin_huge_val();
         });
         if (c1 < nch) {
-          const ElemFetch fr = elem_fetch<T, NT>(srow, trow, c1, V, B.tid);
+          const ElemFetch fr = elem_fetch<T, VNT>(srow, trow, c1, V, B.tid);
           float sw, tw;
-          const int yc = elem_pick<NT>(B, fr, c1, V, P.seed, RES_ELEM, g, [&](float sv, float tv, int) {
+          const int yc = elem_pick<VNT>(B, fr, c1, V, P.seed, RES_ELEM, g, [&](float sv, float tv, int) {
             float p;
             const float w = F.acc ? res_weight<true>(sv, tv, F, &p) : res_weight<false>(sv, tv, F, &p);
             return w > 0.0f ? flog2(w) * LN2 : -finf();
@@ -950,12 +954,23 @@ saki_status saki_spec_verify(const saki_rows* in, int32_t k, const int32_t* draf
   hipLaunchKernelGGL(saki::clear_counter_kernel, dim3(1), dim3(64), 0, hs, P.next_block);
   st = launched("clear_counter_kernel");
   if (st != SAKI_OK) return st;
-  if (in->dtype == SAKI_BF16 && (P.V + saki::CHUNK - 1) / saki::CHUNK <= saki::CACHED_MAXC)
-    hipLaunchKernelGGL((saki::verify_kernel<uint16_t, saki::CACHE_KC>), dim3(grid), dim3(saki::NT), 0, hs, P);
-  else if (in->dtype == SAKI_BF16)
-    hipLaunchKernelGGL((saki::verify_kernel<uint16_t, 0>), dim3(grid), dim3(saki::NT), 0, hs, P);
-  else
-    hipLaunchKernelGGL((saki::verify_kernel<float, 0>), dim3(grid), dim3(saki::NT), 0, hs, P);
+  const bool cached = in->dtype == SAKI_BF16 && (P.V + saki::CHUNK - 1) / saki::CHUNK <= saki::CACHED_MAXC;
+  if (P.n_blocks <= cus) {
+    // no more blocks than CUs: one 512-thread workgroup per block
+    const dim3 g1(static_cast<unsigned>(P.n_blocks)), b1(512);
+    if (cached)
+      hipLaunchKernelGGL((saki::verify_kernel<uint16_t, saki::CACHE_KC, 512>), g1, b1, 0, hs, P);
+    else if (in->dtype == SAKI_BF16)
+      hipLaunchKernelGGL((saki::verify_kernel<uint16_t, 0, 512>), g1, b1, 0, hs, P);
+    else
+      hipLaunchKernelGGL((saki::verify_kernel<float, 0, 512>), g1, b1, 0, hs, P);
+  } else if (cached) {
+    hipLaunchKernelGGL((saki::verify_kernel<uint16_t, saki::CACHE_KC, 256>), dim3(grid), dim3(256), 0, hs, P);
+  } else if (in->dtype == SAKI_BF16) {
+    hipLaunchKernelGGL((saki::verify_kernel<uint16_t, 0, 256>), dim3(grid), dim3(256), 0, hs, P);
+  } else {
+    hipLaunchKernelGGL((saki::verify_kernel<float, 0, 256>), dim3(grid), dim3(256), 0, hs, P);
+  }
   st = launched("verify_kernel");
   if (st != SAKI_OK) return st;
   return ok();
