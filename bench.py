@@ -3,7 +3,7 @@
 One step = one saki_couple call with fused routing and an fp32 gradient over
 the whole 'large' workload: 64 sequences x 1024 positions = 65,536 rows of
 V = 151,936 bf16 student and teacher logits, resident in HBM.  Prints one
-JSON line.  --gpus N with N > 1 exits: this build runs on one GPU.
+JSON line.  --gpus N with N > 1 exits: the library runs on one GPU.
 """
 import argparse
 import json
@@ -136,8 +136,8 @@ def main():
                          "rollout: speculative rollout waves, 256 sequences x 64 tokens, k = 8")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
-              "(rows shard across GPUs without communication; see DESIGN.md)", file=sys.stderr)
+        print("bench.py runs on exactly one GPU: the library has no multi-GPU path "
+              "(rows shard across GPUs without communication: each GPU takes a row range with its own row_offset)", file=sys.stderr)
         sys.exit(2)
 
     import torch
