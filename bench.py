@@ -123,7 +123,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--eps", type=float, default=0.2)
     ap.add_argument("--rows", type=int, default=None, help="override the row count (debug)")
-    ap.add_argument("--cpu-sample", type=int, default=256)
+    ap.add_argument("--cpu-sample", type=int, default=128,
+                    help="rows timed on the CPU oracle (about 25 s of CPU work at V = 151,936)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one 1 GiB device copy before timing (counter calibration)")
