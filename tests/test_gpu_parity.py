@@ -193,6 +193,39 @@ def test_verify_without_per_position_outputs(saki_lib):
     assert out["accepted_len"].cpu().tolist() == [2, 4] and out["correction"].cpu().tolist() == [-1, -1]
 
 
+def test_verify_full_size_sampled(saki_lib):
+    """The verify workload at full size (8,192 blocks of k = 8, V = 151,936
+    bf16) in the configuration the benchmark times (accepted lengths and
+    corrections only): sampled blocks against the oracle, and the first-
+    rejection structure on every block."""
+    cfg = workloads.CONFIGS["verify"]
+    k, n, V = cfg["k"], cfg["rows"], cfg["V"]
+    nb = n // k
+    say(f"generate verify {n}x{V}")
+    s = torch.empty(n, V, dtype=torch.bfloat16, device=DEV)
+    t = torch.empty_like(s)
+    workloads.fill("verify", s, t)
+    draft = workloads.drafts(s)
+    eps, seed = 0.2, workloads.coupling_seed("verify")
+    out = saki_lib.spec_verify(s, t, k, draft, eps, seed, per_pos=False)
+    torch.cuda.synchronize()
+    gpu = dict(accepted_len=out["accepted_len"].cpu().numpy(), correction=out["correction"].cpu().numpy())
+    al, co = gpu["accepted_len"], gpu["correction"]
+    assert al.shape == (nb,) and al.min() >= 0 and al.max() <= k
+    assert np.all((co >= 0) == (al < k)) and co.max() < V
+    rng = np.random.default_rng(11)
+    blocks = np.unique(np.concatenate([[0, 1, nb // 2, nb - 1], rng.choice(nb, 4, replace=False)]))
+    idx = np.concatenate([np.arange(b * k, (b + 1) * k) for b in blocks])
+    ii = torch.as_tensor(idx, device=DEV)
+    say(f"oracle on blocks {blocks.tolist()}")
+    R = parity.compare_verify(gpu, f64(s[ii]), f64(t[ii]), k, draft[ii].cpu().numpy(), eps, seed, 0,
+                              blocks)
+    say(R.summary())
+    R.check()
+    del s, t, draft, out
+    torch.cuda.empty_cache()
+
+
 def test_verify_edge_cases(saki_lib):
     k, V = 4, 300
     rng = torch.Generator(device=DEV).manual_seed(1)
