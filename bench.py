@@ -130,9 +130,10 @@ def main():
                     help="run one 1 GiB device copy before timing (counter calibration)")
     ap.add_argument("--metadata", choices=("full", "objective"), default="objective",
                     help="rollout workload: per-token metadata kept (objective: without lambda, KL, TV)")
-    ap.add_argument("--workload", choices=("couple", "verify", "stream", "rollout"), default="couple",
+    ap.add_argument("--workload", choices=("couple", "verify", "stream", "rollout", "route"), default="couple",
                     help="couple: the headline (coupling + routed loss + fp32 gradient); "
                          "verify: speculative verification of 8,192 blocks of k = 8; "
+                         "route: saki_route_loss alone on the large workload's coupled rows; "
                          "stream: the long-rollout stress workload, 262,144 rows in 64 chunks; "
                          "rollout: speculative rollout waves, 256 sequences x 64 tokens, k = 8")
     args = ap.parse_args()
@@ -153,6 +154,8 @@ def main():
         return bench_rollout(args, saki, workloads, dev)
     if args.workload == "stream":
         return bench_stream(args, saki, workloads, dev)
+    if args.workload == "route":
+        return bench_route(args, saki, workloads, dev)
     cfg = workloads.CONFIGS["large"]
     n = args.rows or cfg["rows"]
     V = cfg["V"]
@@ -337,6 +340,77 @@ def bench_verify(args, saki, workloads, dev):
                      "frac": achieved / HBM_PEAK_GBS, "attainable_read": attainable,
                      "frac_attainable": achieved / attainable, "traffic": None},
         "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def bench_route(args, saki, workloads, dev):
+    """saki_route_loss on its own: the routed loss (Eq. general_objective) and its
+    f32 gradient over the large workload's 65,536 rows (V = 151,936 bf16), with
+    the coupling outputs of one saki_couple call (made before timing) as input."""
+    import torch
+    cfg = workloads.CONFIGS["large"]
+    n = args.rows or cfg["rows"]
+    V = cfg["V"]
+    seed = workloads.coupling_seed("large")
+    print(f"# generating {n} x {V} bf16 rows and their coupling", file=sys.stderr, flush=True)
+    s = torch.empty(n, V, dtype=torch.bfloat16, device=dev)
+    t = torch.empty_like(s)
+    workloads.fill("large", s, t)
+    out = saki.alloc_couple_out(n, dev)
+    ws_c = torch.empty(max(saki.workspace_bytes(saki.SAKI_OP_COUPLE, n, V), 8), dtype=torch.uint8, device=dev)
+    saki.saki_couple(s, t, args.eps, seed, 0, out, None, ws_c)
+    torch.cuda.synchronize()
+    del t, ws_c
+    torch.cuda.empty_cache()
+    adv = (out["logt_token"] - out["logp_token"]).contiguous()
+    grad = torch.empty(n, V, dtype=torch.float32, device=dev)
+    row_loss = torch.empty(n, dtype=torch.float32, device=dev)
+    loss_sum = torch.empty(1, dtype=torch.float64, device=dev)
+    ws = torch.empty(max(saki.workspace_bytes(saki.SAKI_OP_ROUTE, n, V), 8), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+
+    def step():
+        saki.saki_route_loss(s, out["token"], out["corrected"], out["teacher_argmax"], adv,
+                             grad_scale=1.0 / n, row_loss=row_loss, loss_sum=loss_sum, grad=grad,
+                             workspace=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    ev[0].record(stream)
+    for i in range(args.steps):
+        step()
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+    ms = sum(per) / len(per)
+    print(f"# per-step ms: {[round(x, 3) for x in per]}", file=sys.stderr, flush=True)
+    achieved = n * (2 * V + 4 * V) / (ms * 1e-3) / 1e9  # s read once (bf16), f32 gradient written once
+    attainable = attainable_read_gbs(dev)
+    line = {
+        "metric": "routed-loss positions/sec at V=151,936 bf16 (saki_route_loss, f32 gradient)",
+        "value": n / (ms * 1e-3),
+        "unit": "positions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 in, f32/f64 accumulation, f32 gradient",
+        "data": "synthetic",
+        "config": {"workload": "route: the large workload's 65,536 coupled rows, V=151,936 bf16, "
+                               "routed loss + loss sum + fp32 grad",
+                   "rows": n, "vocab": V, "eps": args.eps, "grad_dtype": "f32",
+                   "loss_sum": float(loss_sum.item())},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "attainable_read": attainable,
+                     "frac_attainable": achieved / attainable, "traffic": None},
+        "cpu_baseline": None,
     }
     print(json.dumps(line), flush=True)
 

@@ -174,7 +174,13 @@ saki_status saki_couple(const saki_rows *in, double eps, uint64_t seed, const sa
  * pi_theta (= p).  token y, corrected C, teacher_argmax v* and advantage A
  * (= log pi_T(y) - log p(y), read only at rows with C = 0) are [n_rows] device
  * arrays.  A token or v* outside [0, vocab) at a valid row gives that row a NaN
- * loss and a NaN gradient row. */
+ * loss and a NaN gradient row.
+ *   ws  required when n_rows > 0: ws_bytes >= saki_workspace_bytes(SAKI_OP_ROUTE,
+ *       n_rows, vocab), 8-byte aligned.  Its first 256 bytes hold the counter from
+ *       which workgroups take rows (cleared by the call on `stream`); with
+ *       route->loss_sum the scaled row losses follow.  Calls that may run at the
+ *       same time need separate workspaces.
+ * More than 2^31 - 1 rows in one call is SAKI_E_SHAPE. */
 saki_status saki_route_loss(const void *student, int32_t dtype, int64_t n_rows, int64_t vocab,
                             int64_t row_stride, const int32_t *token, const uint8_t *corrected,
                             const int32_t *teacher_argmax, const float *advantage,

@@ -1015,6 +1015,74 @@ __device__ __forceinline__ double final_sweep(Block<NT, SH>& B, const T* srow, c
   return v[0];
 }
 
+// Standalone routed loss, first sweep: the log-sum-exp of one array, with the
+// next chunk's loads in flight.  Exponents are taken against the wave's
+// running maximum as one fma, fma(s, log2 e, -MsL) with MsL = Ms log2(e)
+// rounded once; a chunk that raises the maximum rescales the sum.  Returns S
+// with sum_v e^(s_v) = 2^msL S for the block's msL (written to *msL_out), so
+// that lse = msL ln 2 + ln S and p_v = 2^(s_v log2 e - msL) / S, the form the
+// gradient sweep evaluates.
+template <typename T, int NT, typename SH>
+__device__ double lse_sweep(Block<NT, SH>& B, const T* srow, int V, float* msL_out) {
+  constexpr int NW = NT / WAVE;
+  float Ms = -finf(), MsL = -finf();
+  double Ss = 0.0;
+  for_chunks1<T, NW>(srow, V, B.wave, B.lane, [&](auto tail, const float* s, uint32_t vm, int c) {
+    constexpr bool TAIL = decltype(tail)::value;
+    float ls = -finf();
+#pragma unroll
+    for (int e = 0; e < EPL; ++e)
+      if (SAKI_VALID(e)) ls = fmaxf(ls, s[e]);
+    if (wave_any(ls > Ms)) {
+      const float cms = wave_max(ls);
+      const float cmsL = __fmul_rn(cms, LOG2E);
+      Ss *= static_cast<double>(fexp2(__fsub_rn(MsL, cmsL)));
+      Ms = cms;
+      MsL = cmsL;
+    }
+    double ps = 0.0;
+    float gs = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+      float es = fexp2(fmaf(s[e], LOG2E, -MsL));
+      if (TAIL && !SAKI_VALID(e)) es = 0.f;
+      gs += es;
+      if ((e & 3) == 3) {
+        ps += static_cast<double>(gs);
+        gs = 0.f;
+      }
+    }
+    Ss += ps;
+  });
+  const float ms = B.max(Ms);
+  const float msL = __fmul_rn(ms, LOG2E);
+  double v[1] = {(Ms == -finf()) ? 0.0 : (Ms == ms) ? Ss : Ss * static_cast<double>(fexp2(__fsub_rn(MsL, msL)))};
+  B.sum(v);
+  *msL_out = msL;
+  return v[0];
+}
+
+// Standalone routed loss, second sweep: grad_v = coef * p_v with the
+// indicator entry (hot, logit s_hot) rewritten after the loop by the thread
+// that stored it, as in the final sweep; a row flagged nan_row is all NaN.
+template <typename T, typename G, int NT, typename SH>
+__device__ void route_grad_sweep(Block<NT, SH>& B, const T* srow, G* grow, int V, float msL, float invS,
+                                 float coef, int hot, float s_hot, bool nan_row) {
+  constexpr int NW = NT / WAVE;
+  const float cf = nan_row ? __builtin_nanf("") : coef;
+  for_chunks1<T, NW>(srow, V, B.wave, B.lane, [&](auto tail, const float* s, uint32_t vm, int c) {
+    constexpr bool TAIL = decltype(tail)::value;
+    float g[EPL];
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) g[e] = cf * (fexp2(fmaf(s[e], LOG2E, -msL)) * invS);
+    store_lane<G, TAIL>(grow, c, B.lane, V, g);
+  });
+  if (!nan_row && hot >= 0 && hot < V && B.tid == entry_owner<NT>(hot)) {
+    const float p = fexp2(fmaf(s_hot, LOG2E, -msL)) * invS;
+    Storer<G>::store1(grow + hot, coef * (p - 1.0f));
+  }
+}
+
 #undef SAKI_VALID
 
 // Gradient-only sweep for rows that carry no coupling (non-finite rows, or

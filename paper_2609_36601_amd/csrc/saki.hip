@@ -448,64 +448,47 @@ struct RouteParams {
   double* scaled_loss;
   void* grad;
   int64_t grad_stride;
+  unsigned int* next_row;  // work counter in the caller's workspace, zero at launch
 };
 
-template <typename T, bool TAIL>
-__device__ __forceinline__ void lse_chunk(const T* srow, int V, int c, int lane, float& Ms, double& Ss) {
-  float s[EPL];
-  uint32_t vm;
-  load_lane<T, TAIL>(srow, c, lane, V, s, &vm);
-  float ls = -finf();
-#pragma unroll
-  for (int e = 0; e < EPL; ++e)
-    if (!TAIL || ((vm >> e) & 1u)) ls = fmaxf(ls, s[e]);
-  const float cms = wave_max(ls);
-  double ps = 0.0;
-#pragma unroll
-  for (int e = 0; e < EPL; ++e)
-    if (!TAIL || ((vm >> e) & 1u)) ps += static_cast<double>(fexp2((s[e] - cms) * LOG2E));
-  if (cms > Ms) {
-    Ss *= static_cast<double>(fexp2((Ms - cms) * LOG2E));
-    Ms = cms;
-  }
-  Ss += ps * ((cms == Ms) ? 1.0 : static_cast<double>(fexp2((cms - Ms) * LOG2E)));
-}
-
+// Standalone routed loss: two sweeps over s per row (log-sum-exp, then the
+// gradient), the loss from the logit of the supervised entry.  Workgroups take
+// rows from a counter, as in the coupling kernel.
 template <typename T, typename G, bool GRAD>
 __global__ __launch_bounds__(NT, WG_PER_CU) void route_kernel(RouteParams P) {
   __shared__ RowShared<NT> sh;
   Block<NT> B(sh);
-  constexpr int NW = NT / WAVE;
   const int V = P.V;
-  const int nch = (V + CHUNK - 1) / CHUNK;
-  const bool ragged = (V % CHUNK) != 0;
-  for (int64_t r = blockIdx.x; r < P.n_rows; r += gridDim.x) {
+  __shared__ unsigned int next_r;
+  for (int64_t it = 0; it <= P.n_rows; ++it) {
+    const unsigned int ru = take_next(P.next_row, &next_r);
+    // unsigned: n_rows < 2^31 and the counter stays below n_rows + grid
+    if (ru >= static_cast<unsigned int>(P.n_rows)) break;
+    const int64_t r = static_cast<int64_t>(ru);
     const T* srow = static_cast<const T*>(P.s) + r * P.stride;
     G* grow = GRAD ? static_cast<G*>(P.grad) + r * P.grad_stride : nullptr;
-    float Ms = -finf();
-    double Ss = 0.0;
-    for (int c = B.wave; c < nch; c += NW) {
-      if (ragged && c == nch - 1) lse_chunk<T, true>(srow, V, c, B.lane, Ms, Ss);
-      else lse_chunk<T, false>(srow, V, c, B.lane, Ms, Ss);
-    }
-    const float ms = B.max(Ms);
-    double v[1] = {(Ms == -finf()) ? 0.0 : (Ms == ms) ? Ss : Ss * static_cast<double>(fexp2((Ms - ms) * LOG2E))};
-    B.sum(v);
-    const double lse = static_cast<double>(ms) + log(v[0]);
     const bool M = P.valid ? (P.valid[r] != 0) : true;
     const bool C = P.corrected[r] != 0;
     const int hot = C ? P.vstar[r] : P.token[r];
-    const bool bad = M && (hot < 0 || hot >= V || !isfinite(lse));
+    const bool hot_ok = hot >= 0 && hot < V;
+    // the supervised entry's logit, loaded before the sweeps
+    const float s_hot = hot_ok ? Loader<T>::load1(srow + hot) : 0.0f;
+    float msL;
+    const double S = lse_sweep<T, NT>(B, srow, V, &msL);
+    const double lse = static_cast<double>(msL) * LN2_D + log(S);
+    const bool bad = M && (!hot_ok || !isfinite(lse));
     const double A = C ? 0.0 : static_cast<double>(P.advantage[r]);
     float coef = 0.0f;
     if (M && !bad) coef = static_cast<float>(static_cast<double>(P.grad_scale) * (C ? 1.0 : A));
-    if (GRAD) grad_sweep<T, G, NT>(B, srow, grow, V, ms, v[0], coef, bad ? -1 : hot, bad);
+    if (GRAD)
+      route_grad_sweep<T, G, NT>(B, srow, grow, V, msL, static_cast<float>(1.0 / S), coef, hot_ok ? hot : -1,
+                                 s_hot, bad);
     if (B.tid == 0) {
       double l = 0.0;
       if (bad) {
         l = __builtin_nan("");
       } else if (M) {
-        const double logp_h = static_cast<double>(Loader<T>::load1(srow + hot)) - lse;
+        const double logp_h = static_cast<double>(s_hot) - lse;
         l = C ? -logp_h : -A * logp_h;
       }
       if (P.row_loss) P.row_loss[r] = static_cast<float>(l);
@@ -779,7 +762,7 @@ size_t saki_workspace_bytes(int op, int64_t n_rows, int64_t vocab) {
     case SAKI_OP_COUPLE:
       return 256 + loss_ws_bytes(n_rows);  // the row counter, then the scaled row losses
     case SAKI_OP_ROUTE:
-      return loss_ws_bytes(n_rows);
+      return 256 + loss_ws_bytes(n_rows);  // the row counter, then the scaled row losses
     case SAKI_OP_VERIFY:
       return 256;  // the work counter
     case SAKI_OP_SELECT:
@@ -860,14 +843,14 @@ saki_status saki_route_loss(const void* student, int32_t dtype, int64_t n_rows, 
   bool want_sum = false;
   saki_status st = check_route(route, vocab, &want_sum);
   if (st != SAKI_OK) return st;
-  if (want_sum) {
-    if (!ws) return fail(SAKI_E_WORKSPACE, "workspace is NULL but loss_sum is requested");
-    if (ws_bytes < loss_ws_bytes(n_rows)) return fail(SAKI_E_WORKSPACE, "workspace too small");
-    if ((reinterpret_cast<uintptr_t>(ws) & 7u) != 0) return fail(SAKI_E_ALIGN, "workspace must be 8-byte aligned");
-  }
+  if (n_rows >= (int64_t{1} << 31)) return fail(SAKI_E_SHAPE, "more than 2^31 - 1 rows in one call");
   if (n_rows == 0) return ok();
   if (!student || !token || !corrected || !teacher_argmax || !advantage)
     return fail(SAKI_E_NULLPTR, "student, token, corrected, teacher_argmax and advantage are required");
+  if (!ws) return fail(SAKI_E_WORKSPACE, "workspace is NULL");
+  if (ws_bytes < saki_workspace_bytes(SAKI_OP_ROUTE, n_rows, vocab)) return fail(SAKI_E_WORKSPACE, "workspace too small");
+  if ((reinterpret_cast<uintptr_t>(ws) & 7u) != 0) return fail(SAKI_E_ALIGN, "workspace must be 8-byte aligned");
+  double* row_losses = reinterpret_cast<double*>(static_cast<char*>(ws) + 256);
   if (!aligned16(student) || (row_stride * elem_size(dtype)) % 16 != 0)
     return fail(SAKI_E_ALIGN, "student base pointer and row pitch must be 16-byte aligned");
   int cus = 0;
@@ -885,11 +868,15 @@ saki_status saki_route_loss(const void* student, int32_t dtype, int64_t n_rows, 
   P.valid = route->valid_mask;
   P.grad_scale = route->grad_scale;
   P.row_loss = route->row_loss;
-  P.scaled_loss = want_sum ? static_cast<double*>(ws) : nullptr;
+  P.scaled_loss = want_sum ? row_losses : nullptr;
   P.grad = route->grad;
   P.grad_stride = route->grad_stride;
+  P.next_row = static_cast<unsigned int*>(ws);
   const int grid = static_cast<int>(std::min<int64_t>(n_rows, static_cast<int64_t>(cus) * saki::WG_PER_CU));
   hipStream_t hs = static_cast<hipStream_t>(stream);
+  hipLaunchKernelGGL(saki::clear_counter_kernel, dim3(1), dim3(64), 0, hs, P.next_row);
+  st = launched("clear_counter_kernel");
+  if (st != SAKI_OK) return st;
   const bool grad = route->grad != nullptr;
   const bool gbf = route->grad_dtype == SAKI_BF16;
   if (dtype == SAKI_BF16) {
@@ -903,8 +890,8 @@ saki_status saki_route_loss(const void* student, int32_t dtype, int64_t n_rows, 
   }
   if (st != SAKI_OK) return st;
   if (want_sum) {
-    hipLaunchKernelGGL(saki::loss_sum_kernel, dim3(1), dim3(1024), 0, hs,
-                       static_cast<const double*>(ws), n_rows, route->loss_sum);
+    hipLaunchKernelGGL(saki::loss_sum_kernel, dim3(1), dim3(1024), 0, hs, row_losses, n_rows,
+                       route->loss_sum);
     st = launched("loss_sum_kernel");
     if (st != SAKI_OK) return st;
   }

@@ -113,6 +113,14 @@ def test_verify_and_route_argument_errors(lib):
     assert lib.saki_route_loss(16, 9, 4, 64, 64, 64, 64, 64, 64, ctypes.byref(rt), None, 0, None) == 4
     assert lib.saki_route_loss(16, 1, 4, 64, 64, None, 64, 64, 64, ctypes.byref(rt), None, 0, None) == 1
     assert lib.saki_route_loss(16, 1, 4, 64, 64, 64, 64, 64, 64, None, None, 0, None) == 1
+    # the row counter (and loss slots) live in the caller's workspace
+    need = lib.saki_workspace_bytes(binding.SAKI_OP_ROUTE, 4, 64)
+    assert need == 512
+    assert lib.saki_route_loss(16, 1, 4, 64, 64, 64, 64, 64, 64, ctypes.byref(rt), None, 0, None) == 6
+    assert lib.saki_route_loss(16, 1, 4, 64, 64, 64, 64, 64, 64, ctypes.byref(rt), 256, need - 8, None) == 6
+    assert lib.saki_route_loss(16, 1, 4, 64, 64, 64, 64, 64, 64, ctypes.byref(rt), 260, need, None) == 5
+    assert lib.saki_route_loss(16, 1, 1 << 31, 64, 64, 64, 64, 64, 64, ctypes.byref(rt), 256, 1 << 40, None) == 2
+    assert lib.saki_route_loss(16, 1, 0, 64, 64, None, None, None, None, ctypes.byref(rt), None, 0, None) == 0
 
 
 def test_workspace_sizes(lib):
