@@ -274,32 +274,55 @@ __device__ __forceinline__ void for_chunks(const T* srow, const T* trow, int V, 
 }
 
 // The chunk loop over one array: body(tail, x, vm, c) gets this lane's 16
-// entries of chunk c; full chunks with the next chunk's loads in flight.
-template <typename T, int NW, typename Body>
-__device__ __forceinline__ void for_chunks1(const T* row, int V, int wave, int lane, Body&& body) {
+// entries of chunk c; full chunks with the next chunk's loads in flight.  The
+// row cache works as in for_chunks, with two slots (the two halves of the
+// array) per cached chunk: the wave's last kc full chunks.
+template <typename T, int NW, int CM = CACHE_NONE, typename Body>
+__device__ __forceinline__ void for_chunks1(const T* row, int V, int wave, int lane, Body&& body,
+                                            RowCache rc = RowCache{nullptr, 0}) {
+  static_assert(CM == CACHE_NONE || sizeof(T) == 2, "the row cache holds bf16 chunks");
   const int nfull = V / CHUNK;
-  if (wave < nfull) {
-    const int clast = wave + ((nfull - 1 - wave) / NW) * NW;  // the wave's last full chunk
-    Frag<T> fa, fb;
-    frag_load<false>(fa, row, wave, lane);
+  const int nw = wave < nfull ? (nfull - 1 - wave) / NW + 1 : 0;  // this wave's full chunks
+  const int ncache = (CM == CACHE_NONE || rc.lds == nullptr) ? 0 : min(rc.kc, nw);
+  const int first_cached = nw - ncache;
+  const int nmem = (CM == CACHE_USE) ? first_cached : nw;  // chunks read from memory
+  auto slot = [&](int i, int part) { return rc.lds + ((wave * rc.kc + (i - first_cached)) * 2 + part) * WAVE + lane; };
+  auto run = [&](const Frag<T>& f, int c) {
+    if constexpr (CM == CACHE_FILL) {
+      const int i = (c - wave) / NW;
+      if (i >= first_cached) {
+        *slot(i, 0) = f.q[0];
+        *slot(i, 1) = f.q[1];
+      }
+    }
+    float x[EPL];
+    frag_unpack(f, x);
+    body(std::integral_constant<bool, false>(), x, 0xffffu, c);
+  };
+  Frag<T> fa, fb;
+  if (nmem > 0) frag_load<false>(fa, row, wave, lane);
+  if constexpr (CM == CACHE_USE) {
+    for (int i = first_cached; i < nw; ++i) {
+      Frag<T> cf;
+      cf.q[0] = *slot(i, 0);
+      cf.q[1] = *slot(i, 1);
+      float x[EPL];
+      frag_unpack(cf, x);
+      body(std::integral_constant<bool, false>(), x, 0xffffu, wave + i * NW);
+    }
+  }
+  if (nmem > 0) {
+    const int clast = wave + (nmem - 1) * NW;  // the wave's last chunk read from memory
     int c = wave;
     for (;;) {
       const bool more_b = c < clast;
       frag_load<false>(fb, row, more_b ? c + NW : c, lane);
-      {
-        float x[EPL];
-        frag_unpack(fa, x);
-        body(std::integral_constant<bool, false>(), x, 0xffffu, c);
-      }
+      run(fa, c);
       if (!more_b) break;
       c += NW;
       const bool more_a = c < clast;
       frag_load<false>(fa, row, more_a ? c + NW : c, lane);
-      {
-        float x[EPL];
-        frag_unpack(fb, x);
-        body(std::integral_constant<bool, false>(), x, 0xffffu, c);
-      }
+      run(fb, c);
       if (!more_a) break;
       c += NW;
     }
@@ -1027,7 +1050,7 @@ __device__ double lse_sweep(Block<NT, SH>& B, const T* srow, int V, float* msL_o
   constexpr int NW = NT / WAVE;
   float Ms = -finf(), MsL = -finf();
   double Ss = 0.0;
-  for_chunks1<T, NW>(srow, V, B.wave, B.lane, [&](auto tail, const float* s, uint32_t vm, int c) {
+  for_chunks1<T, NW, fill_mode<T, SH>()>(srow, V, B.wave, B.lane, [&](auto tail, const float* s, uint32_t vm, int c) {
     constexpr bool TAIL = decltype(tail)::value;
     float ls = -finf();
 #pragma unroll
@@ -1053,7 +1076,7 @@ __device__ double lse_sweep(Block<NT, SH>& B, const T* srow, int V, float* msL_o
       }
     }
     Ss += ps;
-  });
+  }, row_cache<T>(B.sh));
   const float ms = B.max(Ms);
   const float msL = __fmul_rn(ms, LOG2E);
   double v[1] = {(Ms == -finf()) ? 0.0 : (Ms == ms) ? Ss : Ss * static_cast<double>(fexp2(__fsub_rn(MsL, msL)))};
@@ -1070,13 +1093,13 @@ __device__ void route_grad_sweep(Block<NT, SH>& B, const T* srow, G* grow, int V
                                  float coef, int hot, float s_hot, bool nan_row) {
   constexpr int NW = NT / WAVE;
   const float cf = nan_row ? __builtin_nanf("") : coef;
-  for_chunks1<T, NW>(srow, V, B.wave, B.lane, [&](auto tail, const float* s, uint32_t vm, int c) {
+  for_chunks1<T, NW, use_mode<T, SH>()>(srow, V, B.wave, B.lane, [&](auto tail, const float* s, uint32_t vm, int c) {
     constexpr bool TAIL = decltype(tail)::value;
     float g[EPL];
 #pragma unroll
     for (int e = 0; e < EPL; ++e) g[e] = cf * (fexp2(fmaf(s[e], LOG2E, -msL)) * invS);
     store_lane<G, TAIL>(grow, c, B.lane, V, g);
-  });
+  }, row_cache<T>(B.sh));
   if (!nan_row && hot >= 0 && hot < V && B.tid == entry_owner<NT>(hot)) {
     const float p = fexp2(fmaf(s_hot, LOG2E, -msL)) * invS;
     Storer<G>::store1(grow + hot, coef * (p - 1.0f));

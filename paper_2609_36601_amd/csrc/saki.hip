@@ -451,13 +451,29 @@ struct RouteParams {
   unsigned int* next_row;  // work counter in the caller's workspace, zero at launch
 };
 
+// Shared state of the standalone routed loss: the block reductions and, for
+// bf16 rows, a row cache of KC chunks of s per wave (the log-sum-exp sweep
+// stores the wave's last KC full chunks, the gradient sweep reads them).
+template <int NT_, int KC>
+struct RouteShared {
+  static constexpr int NW = NT_ / WAVE;
+  static constexpr int CACHE_CHUNKS = KC;
+  double red_d[NW][RED_MAX];
+  float red_f[NW][4];
+  int red_i[NW][4];
+  uint4 cache[KC > 0 ? NW * KC * 2 * WAVE : 1];  // [wave][slot][half][lane]
+};
+// 9 chunks per wave: 72 KiB, two workgroups per CU
+constexpr int ROUTE_KC = 9;
+
 // Standalone routed loss: two sweeps over s per row (log-sum-exp, then the
 // gradient), the loss from the logit of the supervised entry.  Workgroups take
 // rows from a counter, as in the coupling kernel.
 template <typename T, typename G, bool GRAD>
 __global__ __launch_bounds__(NT, WG_PER_CU) void route_kernel(RouteParams P) {
-  __shared__ RowShared<NT> sh;
-  Block<NT> B(sh);
+  using SH = RouteShared<NT, (sizeof(T) == 2 ? ROUTE_KC : 0)>;
+  __shared__ SH sh;
+  Block<NT, SH> B(sh);
   const int V = P.V;
   __shared__ unsigned int next_r;
   for (int64_t it = 0; it <= P.n_rows; ++it) {

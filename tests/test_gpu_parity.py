@@ -344,6 +344,34 @@ def test_route_loss_standalone(saki_lib):
     assert np.max(np.abs(out["grad"].cpu().numpy() - grad)) <= parity.GRAD_ATOL
 
 
+@pytest.mark.parametrize("V", [36 * 1024, 37 * 1024 + 5, 151936])
+def test_route_loss_row_cache(saki_lib, V):
+    """bf16 rows keep each wave's last nine full chunks of s in LDS between the
+    routed loss's two sweeps: every chunk cached (nine per wave), one chunk per
+    wave past that plus a ragged tail, and the large vocabulary (36 of its 148
+    full chunks cached).  Loss and gradient against the oracle on every row,
+    with a masked row and a bf16 gradient."""
+    g = torch.Generator(device=DEV).manual_seed(V)
+    n = 12
+    s = padded((3.0 * torch.randn(n, V, generator=g, device=DEV) / 0.7).to(torch.bfloat16))
+    token = torch.randint(0, V, (n,), generator=g, device=DEV, dtype=torch.int32)
+    vstar = torch.randint(0, V, (n,), generator=g, device=DEV, dtype=torch.int32)
+    corrected = (torch.arange(n, device=DEV) % 3 == 0).to(torch.uint8)
+    adv = torch.randn(n, generator=g, device=DEV).float()
+    valid = torch.as_tensor((np.arange(n) != 4).astype(np.uint8), device=DEV)
+    say(f"route_loss V={V}")
+    rl, ls, grad = routing.route_rows(f64(s), token.cpu().numpy(), corrected.cpu().numpy(),
+                                      vstar.cpu().numpy(), adv.double().cpu().numpy(), valid.cpu().numpy(), 1.0)
+    for gd in (torch.float32, torch.bfloat16):
+        out = saki_lib.route_loss(s, token, corrected, vstar, adv, valid_mask=valid, grad_scale=1.0,
+                                  grad_dtype=gd)
+        torch.cuda.synchronize()
+        assert np.all(parity.close(out["row_loss"].cpu().numpy(), rl, atol=1e-6))
+        assert abs(out["loss_sum"].item() - ls) <= 1e-5 * np.abs(rl).sum()
+        tol = parity.GRAD_ATOL if gd == torch.float32 else parity.GRAD_ATOL + 2.0 ** -8 * np.abs(grad)
+        assert np.all(np.abs(out["grad"].float().cpu().numpy() - grad) <= tol)
+
+
 def test_determinism_and_row_split_invariance(saki_lib):
     s, t = workloads.rows("mid", 0, 512, device=DEV)
     a = saki_lib.couple(s, t, 0.2, 5, 1000, route=True, grad_dtype=torch.float32)
