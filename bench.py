@@ -22,15 +22,19 @@ KERNEL_SOURCES = ["paper_2609_36601_amd/csrc/saki.hip", "paper_2609_36601_amd/cs
                   "paper_2609_36601_amd/csrc/device_util.hpp", "paper_2609_36601_amd/csrc/probe.hpp",
                   "paper_2609_36601_amd/csrc/rollout.hpp"]
 
-# HBM traffic of one couple-kernel launch on the large workload (eps 0.2), from
-# two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch;
-# profiles/couple_kernel_large.md).  A plain 1 GiB device copy reads
-# FETCH_SIZE = 524,309 KiB and WRITE_SIZE = 1,048,576 KiB on the same box, so
-# FETCH_SIZE is scaled by 2.0 and WRITE_SIZE by 1.0.  Keyed by the SHA-256 of
-# the kernel sources: a changed kernel reports traffic = null until re-measured.
+# HBM traffic of one launch of the dominant kernel, from two rocprofv3 --pmc
+# runs (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch): the couple kernel on the
+# large workload at eps 0.2 (profiles/couple_kernel_large.md) and the route
+# kernel on the same rows (profiles/route_kernel_large.md).  A plain 1 GiB
+# device copy reads FETCH_SIZE = 524,309 KiB and WRITE_SIZE = 1,048,576 KiB on
+# the same box, so FETCH_SIZE is scaled by 2.0 and WRITE_SIZE by 1.0.  Keyed by
+# the SHA-256 of the kernel sources: a changed kernel reports traffic = null
+# until re-measured.
 MEASURED_TRAFFIC = {
-    "af0d437abd3678eb92dc3beec8c0c69b14bb2e4412b20933fe7fe8608a236869":
-        dict(fetch_kib=55397265.8, write_kib=41639121.1, fetch_scale=2.0, write_scale=1.0),
+    "aaec593421b90b830193beb8a8518477eb30b93e0b384dc3afb04d7426f17105": {
+        "couple": dict(fetch_kib=55343079.9, write_kib=41529901.6, fetch_scale=2.0, write_scale=1.0),
+        "route": dict(fetch_kib=17096676.1, write_kib=42635141.7, fetch_scale=2.0, write_scale=1.0),
+    },
 }
 
 
@@ -43,8 +47,8 @@ def kernel_source_hash():
     return h.hexdigest()
 
 
-def measured_traffic_bytes():
-    m = MEASURED_TRAFFIC.get(kernel_source_hash())
+def measured_traffic_bytes(workload="couple"):
+    m = MEASURED_TRAFFIC.get(kernel_source_hash(), {}).get(workload)
     if m is None:
         return None
     return (m["fetch_kib"] * m["fetch_scale"] + m["write_kib"] * m["write_scale"]) * 1024.0
@@ -409,7 +413,8 @@ def bench_route(args, saki, workloads, dev):
                    "loss_sum": float(loss_sum.item())},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "attainable_read": attainable,
-                     "frac_attainable": achieved / attainable, "traffic": None},
+                     "frac_attainable": achieved / attainable,
+                     "traffic": measured_traffic_bytes("route") if n == cfg["rows"] and args.eps == 0.2 else None},
         "cpu_baseline": None,
     }
     print(json.dumps(line), flush=True)
