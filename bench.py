@@ -232,9 +232,9 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16 in, f32/f64 accumulation, f32 gradient",
+        "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": "large: 64 seq x 1024 pos = 65,536 rows, V=151,936 bf16, "
+        "config": {"logits": "bf16", "arithmetic": "f32, row sums and the lambda solve in f64", "workload": "large: 64 seq x 1024 pos = 65,536 rows, V=151,936 bf16, "
                                "rho~U(0.3,0.95), coupling + routed loss + fp32 grad",
                    "rows": n, "vocab": V, "eps": args.eps, "grad_dtype": "f32"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -334,9 +334,9 @@ def bench_verify(args, saki, workloads, dev):
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16 in, f32/f64 accumulation",
+        "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": "verify: 256 seq x 32 blocks x k=8 = 65,536 rows, V=151,936 bf16, "
+        "config": {"logits": "bf16", "arithmetic": "f32, row sums and the lambda solve in f64", "workload": "verify: 256 seq x 32 blocks x k=8 = 65,536 rows, V=151,936 bf16, "
                                "rho~U(0.2,0.99) per block, drafts z~softmax(s)",
                    "blocks": nb, "k": k, "vocab": V, "eps": args.eps,
                    "mean_accepted_length": float(al.mean()), "positions_evaluated": evaluated},
@@ -405,9 +405,9 @@ def bench_route(args, saki, workloads, dev):
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16 in, f32/f64 accumulation, f32 gradient",
+        "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": "route: the large workload's 65,536 coupled rows, V=151,936 bf16, "
+        "config": {"logits": "bf16", "arithmetic": "f32, row sums in f64", "workload": "route: the large workload's 65,536 coupled rows, V=151,936 bf16, "
                                "routed loss + loss sum + fp32 grad",
                    "rows": n, "vocab": V, "eps": args.eps, "grad_dtype": "f32",
                    "loss_sum": float(loss_sum.item())},
@@ -505,9 +505,9 @@ def bench_rollout(args, saki, workloads, dev):
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16 in, f32/f64 accumulation",
+        "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": "rollout: 256 sequences x 64 tokens, k=8 drafts per wave, V=151,936 bf16, "
+        "config": {"logits": "bf16", "arithmetic": "f32, row sums and the lambda solve in f64", "workload": "rollout: 256 sequences x 64 tokens, k=8 drafts per wave, V=151,936 bf16, "
                                "eps 0.2, synthetic prefix-hash student/teacher",
                    "metadata": args.metadata,
                    "tokens_per_rollout": tok, "waves_per_rollout": waves_mean,
@@ -578,9 +578,9 @@ def bench_stream(args, saki, workloads, dev):
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16 in, f32/f64 accumulation, f32 gradient",
+        "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": "stream: 32 seq x 8192 pos = 262,144 rows in 64 chunks of 4,096, "
+        "config": {"logits": "bf16", "arithmetic": "f32, row sums and the lambda solve in f64", "workload": "stream: 32 seq x 8192 pos = 262,144 rows in 64 chunks of 4,096, "
                                "V=151,936 bf16, peaked rows, eps 0.02, coupling + routed loss + fp32 grad",
                    "rows": rows, "vocab": V, "eps": eps, "chunks": n_chunks},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
