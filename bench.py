@@ -55,39 +55,49 @@ def measured_traffic_bytes(workload="couple"):
 
 
 def _oracle_rows(args):
-    """CPU oracle on a batch of rows (runs in a worker process)."""
+    """CPU oracle on rows, in order, until `budget` seconds of work (a worker process)."""
     os.environ.setdefault("OMP_NUM_THREADS", "1")
     import numpy as np
     from oracle import coupling, routing
-    s, t, eps, seed, offsets = args
+    s, t, eps, seed, offsets, budget = args
     t0 = time.perf_counter()
+    done = 0
     for i in range(s.shape[0]):
-        ev = coupling.couple_rows(s[i:i + 1], t[i:i + 1], eps, seed, int(offsets[i]))
-        routing.couple_and_route(ev, s[i:i + 1], None, 1.0, want_grad=True)
-    return time.perf_counter() - t0
+        si = s[i:i + 1].astype(np.float64)
+        ti = t[i:i + 1].astype(np.float64)
+        ev = coupling.couple_rows(si, ti, eps, seed, int(offsets[i]))
+        routing.couple_and_route(ev, si, None, 1.0, want_grad=True)
+        done += 1
+        if time.perf_counter() - t0 >= budget:
+            break
+    return done, time.perf_counter() - t0
 
 
-def cpu_baseline(s, t, eps, seed, n_sample, workers):
-    """The float64 oracle (as it stands) on a bounded sample of the same rows."""
+def cpu_baseline(s, t, eps, seed, n_sample, workers, budget=20.0):
+    """The float64 oracle (as it stands) on a bounded sample of the same rows:
+    each worker takes its share of n_sample evenly spaced rows in order and
+    stops after budget / workers seconds of work."""
     import numpy as np
     import torch
     n = s.shape[0]
     rows = np.linspace(0, n - 1, n_sample).astype(np.int64)
     idx = torch.as_tensor(rows, device=s.device)
-    S = s[idx].float().cpu().numpy().astype(np.float64)
-    T = t[idx].float().cpu().numpy().astype(np.float64)
-    parts = np.array_split(np.arange(n_sample), workers)
-    jobs = [(S[p], T[p], eps, seed, rows[p]) for p in parts if len(p)]
+    S = s[idx].float().cpu().numpy()
+    T = t[idx].float().cpu().numpy()
+    parts = [np.arange(w, n_sample, workers) for w in range(workers)]
+    jobs = [(S[p], T[p], eps, seed, rows[p], budget / workers) for p in parts if len(p)]
     ctx = mp.get_context("spawn")
     with ctx.Pool(len(jobs)) as pool:
         pool.map(_noop, range(len(jobs)))  # start the workers before timing
         t0 = time.perf_counter()
-        busy = pool.map(_oracle_rows, jobs)
+        res = pool.map(_oracle_rows, jobs)
         wall = time.perf_counter() - t0
-    return dict(value=n_sample / wall, unit="positions/s", cores=len(jobs), kind="oracle",
-                sample=f"{n_sample} rows of the same workload (evenly spaced), coupling + routed "
-                       f"loss + gradient, {len(jobs)} single-threaded worker processes; "
-                       f"{sum(busy):.1f} s of CPU work in {wall:.1f} s wall")
+    done = sum(r[0] for r in res)
+    busy = sum(r[1] for r in res)
+    return dict(value=done / wall, unit="positions/s", cores=len(jobs), kind="oracle",
+                sample=f"{done} rows of the same workload (from {n_sample} evenly spaced), coupling + "
+                       f"routed loss + gradient, {len(jobs)} single-threaded worker processes each "
+                       f"stopping after {budget / len(jobs):.2f} s; {busy:.1f} s of CPU work in {wall:.1f} s wall")
 
 
 def _noop(x):
@@ -127,8 +137,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--eps", type=float, default=0.2)
     ap.add_argument("--rows", type=int, default=None, help="override the row count (debug)")
-    ap.add_argument("--cpu-sample", type=int, default=128,
-                    help="rows timed on the CPU oracle (about 25 s of CPU work at V = 151,936)")
+    ap.add_argument("--cpu-sample", type=int, default=256,
+                    help="rows offered to the CPU oracle (it stops after about 20 s of CPU work)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one 1 GiB device copy before timing (counter calibration)")
@@ -248,14 +258,19 @@ def main():
 
 
 def _oracle_blocks(args):
+    """CPU oracle on blocks, in order, until `budget` seconds of work (a worker process)."""
     os.environ.setdefault("OMP_NUM_THREADS", "1")
     from oracle import verify
-    s, t, draft, k, eps, seed, offsets = args
+    s, t, draft, k, eps, seed, offsets, budget = args
     t0 = time.perf_counter()
+    done = 0
     for i in range(len(offsets)):
         sl = slice(i * k, (i + 1) * k)
         verify.verify_blocks(s[sl], t[sl], k, draft[sl], eps, seed, int(offsets[i]))
-    return time.perf_counter() - t0
+        done += 1
+        if time.perf_counter() - t0 >= budget:
+            break
+    return done, time.perf_counter() - t0
 
 
 def bench_verify(args, saki, workloads, dev):
@@ -310,19 +325,23 @@ def bench_verify(args, saki, workloads, dev):
         T = t[idx].float().cpu().numpy().astype(np.float64)
         D = draft[idx].cpu().numpy()
         workers = max(1, min(16, os.cpu_count() or 1))
-        parts = np.array_split(np.arange(n_sample), workers)
+        budget = 20.0
+        parts = [np.arange(w, n_sample, workers) for w in range(workers)]
         jobs = [(np.concatenate([S[b * k:(b + 1) * k] for b in p]), np.concatenate([T[b * k:(b + 1) * k] for b in p]),
-                 np.concatenate([D[b * k:(b + 1) * k] for b in p]), k, args.eps, seed, blocks[p] * k)
+                 np.concatenate([D[b * k:(b + 1) * k] for b in p]), k, args.eps, seed, blocks[p] * k,
+                 budget / workers)
                 for p in parts if len(p)]
         ctx = mp.get_context("spawn")
         with ctx.Pool(len(jobs)) as pool:
             pool.map(_noop, range(len(jobs)))
             t0 = time.perf_counter()
-            busy = pool.map(_oracle_blocks, jobs)
+            res = pool.map(_oracle_blocks, jobs)
             wall = time.perf_counter() - t0
-        cpu = dict(value=n_sample / wall, unit="blocks/s", cores=len(jobs), kind="oracle",
-                   sample=f"{n_sample} blocks of the same workload (evenly spaced), {len(jobs)} "
-                          f"single-threaded worker processes; {sum(busy):.1f} s of CPU work in {wall:.1f} s wall")
+        done = sum(r[0] for r in res)
+        cpu = dict(value=done / wall, unit="blocks/s", cores=len(jobs), kind="oracle",
+                   sample=f"{done} blocks of the same workload (from {n_sample} evenly spaced), {len(jobs)} "
+                          f"single-threaded worker processes each stopping after {budget / len(jobs):.2f} s; "
+                          f"{sum(r[1] for r in res):.1f} s of CPU work in {wall:.1f} s wall")
     line = {
         "metric": "speculative-verify blocks/sec (k=8, V=151,936 bf16)",
         "value": nb / (ms * 1e-3),

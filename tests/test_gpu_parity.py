@@ -372,6 +372,38 @@ def test_route_loss_row_cache(saki_lib, V):
         assert np.all(np.abs(out["grad"].float().cpu().numpy() - grad) <= tol)
 
 
+def test_route_loss_f32_ragged_and_bad_rows(saki_lib):
+    """f32 rows of a ragged vocabulary (no row cache), with a supervised index
+    outside [0, V) at a valid row and a non-finite logit (both: NaN loss and a
+    NaN gradient row), and a masked row with an invalid index (loss 0, gradient
+    row 0); the other rows against the oracle."""
+    g = torch.Generator(device=DEV).manual_seed(5)
+    n, V = 10, 3000
+    s = padded(2.0 * torch.randn(n, V, generator=g, device=DEV))
+    token = torch.randint(0, V, (n,), generator=g, device=DEV, dtype=torch.int32)
+    vstar = torch.randint(0, V, (n,), generator=g, device=DEV, dtype=torch.int32)
+    corrected = (torch.arange(n, device=DEV) % 2 == 1).to(torch.uint8)
+    adv = torch.randn(n, generator=g, device=DEV).float()
+    valid = torch.ones(n, dtype=torch.uint8, device=DEV)
+    good = np.ones(n, bool)
+    token[2], corrected[2] = V, 0                  # index outside the row
+    vstar[3], corrected[3], valid[3] = -1, 1, 0    # masked, invalid index
+    s[5, 17] = float("inf")                        # non-finite logit
+    good[[2, 3, 5]] = False
+    out = saki_lib.route_loss(s, token, corrected, vstar, adv, valid_mask=valid, grad_scale=1.0)
+    torch.cuda.synchronize()
+    rl_g, gr_g = out["row_loss"].cpu().numpy(), out["grad"].cpu().numpy()
+    for r in (2, 5):
+        assert np.isnan(rl_g[r]) and np.isnan(gr_g[r]).all()
+    assert rl_g[3] == 0 and np.all(gr_g[3] == 0)
+    ii = np.nonzero(good)[0]
+    it = torch.as_tensor(ii, device=DEV)
+    rl, _, grad = routing.route_rows(f64(s[it]), token[it].cpu().numpy(), corrected[it].cpu().numpy(),
+                                     vstar[it].cpu().numpy(), adv[it].double().cpu().numpy(), None, 1.0)
+    assert np.all(parity.close(rl_g[ii], rl, atol=1e-6))
+    assert np.max(np.abs(gr_g[ii] - grad)) <= parity.GRAD_ATOL
+
+
 def test_determinism_and_row_split_invariance(saki_lib):
     s, t = workloads.rows("mid", 0, 512, device=DEV)
     a = saki_lib.couple(s, t, 0.2, 5, 1000, route=True, grad_dtype=torch.float32)
