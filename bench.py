@@ -144,10 +144,11 @@ def main():
                     help="run one 1 GiB device copy before timing (counter calibration)")
     ap.add_argument("--metadata", choices=("full", "objective"), default="objective",
                     help="rollout workload: per-token metadata kept (objective: without lambda, KL, TV)")
-    ap.add_argument("--workload", choices=("couple", "verify", "stream", "rollout", "route"), default="couple",
+    ap.add_argument("--workload", choices=("couple", "verify", "stream", "rollout", "route", "probe"), default="couple",
                     help="couple: the headline (coupling + routed loss + fp32 gradient); "
                          "verify: speculative verification of 8,192 blocks of k = 8; "
                          "route: saki_route_loss alone on the large workload's coupled rows; "
+                         "probe: probe metrics (Top-16) on 4,096 rows of the large workload; "
                          "stream: the long-rollout stress workload, 262,144 rows in 64 chunks; "
                          "rollout: speculative rollout waves, 256 sequences x 64 tokens, k = 8")
     args = ap.parse_args()
@@ -170,6 +171,8 @@ def main():
         return bench_stream(args, saki, workloads, dev)
     if args.workload == "route":
         return bench_route(args, saki, workloads, dev)
+    if args.workload == "probe":
+        return bench_probe(args, saki, workloads, dev)
     cfg = workloads.CONFIGS["large"]
     n = args.rows or cfg["rows"]
     V = cfg["V"]
@@ -434,6 +437,62 @@ def bench_route(args, saki, workloads, dev):
                      "frac": achieved / HBM_PEAK_GBS, "attainable_read": attainable,
                      "frac_attainable": achieved / attainable,
                      "traffic": measured_traffic_bytes("route") if n == cfg["rows"] and args.eps == 0.2 else None},
+        "cpu_baseline": None,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def bench_probe(args, saki, workloads, dev):
+    """Probe metrics (C_1, C_16, KL(T || S), H(S) and the teacher's Top-16) on
+    4,096 rows of the large workload (V = 151,936 bf16)."""
+    import torch
+    cfg = workloads.CONFIGS["large"]
+    n = args.rows or 4096
+    V, k = cfg["V"], 16
+    s, t = workloads.rows("large", 0, n, device=dev)
+    out = dict(c1=torch.empty(n, dtype=torch.float32, device=dev),
+               ck=torch.empty(n, dtype=torch.float32, device=dev),
+               kl_ts=torch.empty(n, dtype=torch.float32, device=dev),
+               entropy=torch.empty(n, dtype=torch.float32, device=dev),
+               topk=torch.empty(n, k, dtype=torch.int32, device=dev),
+               row_status=torch.empty(n, dtype=torch.uint8, device=dev))
+    torch.cuda.synchronize()
+
+    def step():
+        saki.saki_probe_metrics(s, t, k, **out)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    ev[0].record(stream)
+    for i in range(args.steps):
+        step()
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+    ms = sum(per) / len(per)
+    print(f"# per-step ms: {[round(x, 3) for x in per]}", file=sys.stderr, flush=True)
+    achieved = n * (2 * V * 2) / (ms * 1e-3) / 1e9  # s and t read once (bf16)
+    line = {
+        "metric": "probe positions/sec at V=151,936 bf16 (C_1, C_16, KL(T||S), H(S), teacher Top-16)",
+        "value": n / (ms * 1e-3),
+        "unit": "positions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"logits": "bf16", "arithmetic": "f32, row sums in f64",
+                   "workload": "probe: 4,096 rows of the large workload, V=151,936 bf16, k=16",
+                   "rows": n, "vocab": V, "k": k, "mean_c16": float(out["ck"].mean())},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None},
         "cpu_baseline": None,
     }
     print(json.dumps(line), flush=True)

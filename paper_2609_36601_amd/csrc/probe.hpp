@@ -3,11 +3,12 @@
 //   C_1 = S(v*_T), C_k = sum of S over the teacher's Top-k set (ties to the
 //   lower index), KL(T || S) = E_T[t - s] - (lse_t - lse_s), H(S).
 // One workgroup per row.  A sweep gives the normalisers and moments; the
-// teacher's k-th largest logit is found by bisection over the logits'
-// order-preserving integer images (16 bits for bf16, 32 for f32; one counting
-// sweep per bit), ties at the threshold go to the lowest indices (bisection
-// over the index), and a last sweep gathers the Top-k set.  Probe sets are
-// small (thousands of positions), so the sweeps re-read rows freely.
+// teacher's k-th largest logit is found by a search over the logits'
+// order-preserving integer images (16 bits for bf16, 32 for f32) that counts
+// twelve pivots per sweep (a 13-way split: 5 sweeps for bf16, 9 for f32); ties
+// at the threshold go to the lowest indices (the same search over the index,
+// only when the threshold value has more entries than are taken), and a last
+// sweep gathers the Top-k set.
 #pragma once
 
 #include "row_engine.hpp"
@@ -53,18 +54,60 @@ struct ProbeShared {
   float red_f[NT / WAVE][4];
   int red_i[NT / WAVE][4];
   int n_sel;
+  float thread_max[NT];  // each thread's largest teacher logit of the row
   int sel_idx[SAKI_MAX_PROBE_K];
   float sel_t[SAKI_MAX_PROBE_K];
 };
 
-// Number of entries v of the row with pred(key(t_v), v), summed over the block.
-template <typename T, typename Pred>
-__device__ double probe_count(Block<NT, ProbeShared>& B, const T* trow, int V, Pred pred) {
-  double n = 0;
-  for (int v = B.tid; v < V; v += NT) n += pred(OrderKey<T>::of(Loader<T>::load1(trow + v)), v) ? 1.0 : 0.0;
-  double r[1] = {n};
-  B.sum(r);
-  return r[0];
+// Pivots counted per sweep in the Top-k searches (one block sum of RED_MAX doubles).
+constexpr int PROBE_PIVOTS = 12;
+
+struct Pivots {
+  uint32_t m[PROBE_PIVOTS];
+};
+struct PivotCounts {
+  double n[PROBE_PIVOTS];
+};
+
+// One sweep over the teacher row, for every pivot i: #{v : key(t_v) >= m_i}
+// (BY_INDEX false) or #{v : key(t_v) == K, v <= m_i} (BY_INDEX true), summed
+// over the block (every thread gets the same counts).  Pivots and counts are
+// passed by value so that they stay in registers.
+template <bool BY_INDEX, typename T>
+__device__ __forceinline__ PivotCounts probe_counts(Block<NT, ProbeShared>& B, const T* trow, int V, const Pivots pv,
+                                                    uint32_t K) {
+  constexpr int NW = NT / WAVE;
+  uint32_t cnt[PROBE_PIVOTS];
+#pragma unroll
+  for (int i = 0; i < PROBE_PIVOTS; ++i) cnt[i] = 0u;
+  for_chunks1<T, NW>(trow, V, B.wave, B.lane, [&](auto tail, const float* x, uint32_t vm, int c) {
+    constexpr bool TAIL = decltype(tail)::value;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+      const bool ok = !TAIL || ((vm >> e) & 1u);
+      const uint32_t key = OrderKey<T>::of(x[e]);
+      if (BY_INDEX) {
+        // entries outside the row or off the threshold value get an index no pivot reaches
+        const uint32_t v = (ok && key == K) ? static_cast<uint32_t>(c * CHUNK + elem_offset(B.lane, e)) : 0xffffffffu;
+#pragma unroll
+        for (int i = 0; i < PROBE_PIVOTS; ++i) cnt[i] += (v <= pv.m[i]) ? 1u : 0u;
+      } else {
+        // every pivot is >= 1 (key 0 is the image of a NaN, and rows with a
+        // non-finite logit are not searched): key 0 is never counted
+        const uint32_t kk = ok ? key : 0u;
+#pragma unroll
+        for (int i = 0; i < PROBE_PIVOTS; ++i) cnt[i] += (kk >= pv.m[i]) ? 1u : 0u;
+      }
+    }
+  });
+  double n[PROBE_PIVOTS];
+#pragma unroll
+  for (int i = 0; i < PROBE_PIVOTS; ++i) n[i] = static_cast<double>(cnt[i]);
+  B.sum(n);
+  PivotCounts out;
+#pragma unroll
+  for (int i = 0; i < PROBE_PIVOTS; ++i) out.n[i] = n[i];
+  return out;
 }
 
 template <typename T>
@@ -80,6 +123,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void probe_kernel(ProbeParams P) {
     // St = sum e^{t-Mt}, Td = sum e^{t-Mt} (t-s)
     float Ms = -finf(), Mt = -finf();
     double Ss = 0, Sa = 0, St = 0, Td = 0;
+    float Lt = -finf();  // this thread's largest teacher logit
     bool finite = true;
     for_chunks<T, NW>(srow, trow, V, B.wave, B.lane,
                       [&](auto tail, const float* s, const float* t, uint32_t vm, int c) {
@@ -95,6 +139,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void probe_kernel(ProbeParams P) {
                           }
                         }
                         finite = finite && !wave_any(!fin);
+                        Lt = fmaxf(Lt, lt);
                         if (wave_any(ls > Ms)) {
                           const float m = wave_max(ls);
                           const double f = static_cast<double>(fexp2((Ms - m) * LOG2E));
@@ -151,37 +196,90 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void probe_kernel(ProbeParams P) {
         for (int j = B.tid; j < k; j += NT) P.topk[r * k + j] = -1;
       continue;
     }
-    // the k-th largest key: the largest x with #{key >= x} >= k
-    uint32_t lo = 0, hi = (OrderKey<T>::BITS == 32) ? 0xffffffffu : 0xffffu;
+    // The k-th largest key K: the largest x with #{key >= x} >= k, searched with
+    // PROBE_PIVOTS pivots per sweep.  Invariants: #{key >= lo} = c_lo >= k and
+    // #{key >= hi + 1} = c_up < k.
+    // The search starts from [key(L), key(max t)]: L, the k-th largest of the
+    // threads' own maxima (k distinct entries of the row), is at most the k-th
+    // largest logit; #{key >= key(L)} is counted by the first sweep.
+    sh.thread_max[B.tid] = Lt;
+    __syncthreads();
+    int n_ge = 0;
+    for (int u = 0; u < NT; ++u) n_ge += (sh.thread_max[u] >= Lt) ? 1 : 0;
+    const float L = B.max(n_ge >= k ? Lt : -finf());
+    uint64_t lo = OrderKey<T>::of(L), hi = OrderKey<T>::of(mt);
+    double c_lo = __builtin_huge_val(), c_up = 0.0;
     while (lo < hi) {
-      const uint32_t mid = lo + static_cast<uint32_t>((static_cast<uint64_t>(hi) - lo + 1) / 2);
-      const double n = probe_count<T>(B, trow, V, [&](uint32_t key, int) { return key >= mid; });
-      if (n >= k) lo = mid; else hi = mid - 1;
+      Pivots pv;  // in (lo, hi], non-decreasing
+#pragma unroll
+      for (int i = 0; i < PROBE_PIVOTS; ++i)
+        pv.m[i] = static_cast<uint32_t>(lo + 1 + (hi - lo) * static_cast<uint64_t>(i + 1) / (PROBE_PIVOTS + 1));
+      // while #{key >= lo} is unknown, the first pivot counts it (lo stays valid)
+      if (c_lo == __builtin_huge_val()) pv.m[0] = static_cast<uint32_t>(lo);
+      const PivotCounts pc = probe_counts<false>(B, trow, V, pv, 0u);
+      const double* n = pc.n;
+      const uint32_t* piv = pv.m;
+      // counts fall as pivots rise: lo moves to the last pivot with count >= k,
+      // hi below the first with count < k (static indices: no scratch arrays)
+      uint64_t lo2 = lo, hi2 = hi;
+      double c_lo2 = c_lo, c_up2 = c_up;
+#pragma unroll
+      for (int i = 0; i < PROBE_PIVOTS; ++i)
+        if (n[i] >= k) { lo2 = piv[i]; c_lo2 = n[i]; }
+#pragma unroll
+      for (int i = PROBE_PIVOTS - 1; i >= 0; --i)
+        if (n[i] < k) { hi2 = static_cast<uint64_t>(piv[i]) - 1; c_up2 = n[i]; }
+      lo = lo2; hi = hi2; c_lo = c_lo2; c_up = c_up2;
     }
-    const uint32_t K = lo;
-    const double n_gt = probe_count<T>(B, trow, V, [&](uint32_t key, int) { return key > K; });
-    const double need = k - n_gt;  // entries with key K to take, lowest indices first
-    // the smallest J with #{key == K, v <= J} >= need
-    int jlo = 0, jhi = V - 1;
-    while (jlo < jhi) {
-      const int mid = jlo + (jhi - jlo) / 2;
-      const double n = probe_count<T>(B, trow, V, [&](uint32_t key, int v) { return key == K && v <= mid; });
-      if (n >= need) jhi = mid; else jlo = mid + 1;
+    const uint32_t K = static_cast<uint32_t>(lo);
+    const double need = k - c_up;  // entries with key K to take, lowest indices first
+    // the smallest J with #{key == K, v <= J} >= need; every entry with key K
+    // is taken when there are exactly need of them
+    int J = V - 1;
+    if (c_lo - c_up > need) {
+      // invariants: #{key == K, v <= jhi} >= need > #{key == K, v < jlo}
+      int jlo = 0, jhi = V - 1;
+      while (jlo < jhi) {
+        Pivots pv;  // in [jlo, jhi), non-decreasing
+#pragma unroll
+        for (int i = 0; i < PROBE_PIVOTS; ++i)
+          pv.m[i] = static_cast<uint32_t>(jlo + static_cast<int>(static_cast<int64_t>(jhi - jlo) * (i + 1) / (PROBE_PIVOTS + 1)));
+        const PivotCounts pc = probe_counts<true>(B, trow, V, pv, K);
+        const double* n = pc.n;
+        const uint32_t* piv = pv.m;
+        // counts grow with the pivot: jlo moves past the last pivot with count
+        // < need, jhi to the first with count >= need
+        int jlo2 = jlo, jhi2 = jhi;
+#pragma unroll
+        for (int i = 0; i < PROBE_PIVOTS; ++i)
+          if (n[i] < need) jlo2 = static_cast<int>(piv[i]) + 1;
+#pragma unroll
+        for (int i = PROBE_PIVOTS - 1; i >= 0; --i)
+          if (n[i] >= need) jhi2 = static_cast<int>(piv[i]);
+        jlo = jlo2;
+        jhi = jhi2;
+      }
+      J = jlo;
     }
-    const int J = jlo;
     if (B.tid == 0) sh.n_sel = 0;
     __syncthreads();
-    for (int v = B.tid; v < V; v += NT) {
-      const float tv = Loader<T>::load1(trow + v);
-      const uint32_t key = OrderKey<T>::of(tv);
-      if (key > K || (key == K && v <= J)) {
-        const int slot = atomicAdd(&sh.n_sel, 1);
-        if (slot < SAKI_MAX_PROBE_K) {
-          sh.sel_idx[slot] = v;
-          sh.sel_t[slot] = tv;
+    for_chunks1<T, NW>(trow, V, B.wave, B.lane, [&](auto tail, const float* x, uint32_t vm, int c) {
+      constexpr bool TAIL = decltype(tail)::value;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) {
+        if (!TAIL || ((vm >> e) & 1u)) {
+          const uint32_t key = OrderKey<T>::of(x[e]);
+          const int v = c * CHUNK + elem_offset(B.lane, e);
+          if (key > K || (key == K && v <= J)) {
+            const int slot = atomicAdd(&sh.n_sel, 1);
+            if (slot < SAKI_MAX_PROBE_K) {
+              sh.sel_idx[slot] = v;
+              sh.sel_t[slot] = x[e];
+            }
+          }
         }
       }
-    }
+    });
     __syncthreads();
     if (B.tid == 0) {
       const int n = min(sh.n_sel, k);
