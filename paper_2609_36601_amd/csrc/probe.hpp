@@ -49,14 +49,20 @@ struct OrderKey<float> {
   }
 };
 
+// Entries the gathering sweep can hold: those above the threshold value and,
+// when they fit, every entry at it (ties then need no index search).
+constexpr int PROBE_SEL_CAP = NT;
+static_assert(PROBE_SEL_CAP >= SAKI_MAX_PROBE_K, "the gathered set holds the Top-k");
+
 struct ProbeShared {
   double red_d[NT / WAVE][RED_MAX];
   float red_f[NT / WAVE][4];
   int red_i[NT / WAVE][4];
   int n_sel;
   float thread_max[NT];  // each thread's largest teacher logit of the row
-  int sel_idx[SAKI_MAX_PROBE_K];
-  float sel_t[SAKI_MAX_PROBE_K];
+  int sel_idx[PROBE_SEL_CAP];   // gathered entries, in arrival order
+  float sel_t[PROBE_SEL_CAP];
+  int ord_idx[PROBE_SEL_CAP];   // the same entries by (t descending, index ascending)
 };
 
 // Pivots counted per sweep in the Top-k searches (one block sum of RED_MAX doubles).
@@ -214,8 +220,14 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void probe_kernel(ProbeParams P) {
 #pragma unroll
       for (int i = 0; i < PROBE_PIVOTS; ++i)
         pv.m[i] = static_cast<uint32_t>(lo + 1 + (hi - lo) * static_cast<uint64_t>(i + 1) / (PROBE_PIVOTS + 1));
-      // while #{key >= lo} is unknown, the first pivot counts it (lo stays valid)
-      if (c_lo == __builtin_huge_val()) pv.m[0] = static_cast<uint32_t>(lo);
+      if (c_lo == __builtin_huge_val()) {
+        // first sweep: lo itself (its count), then lo + 1, lo + 2, lo + 4, ...:
+        // L is usually the k-th largest logit itself (the Top-k entries lie in
+        // different threads), and then this sweep ends the search
+#pragma unroll
+        for (int i = 0; i < PROBE_PIVOTS; ++i)
+          pv.m[i] = static_cast<uint32_t>(i == 0 ? lo : (lo + (1ull << (i - 1)) < hi ? lo + (1ull << (i - 1)) : hi));
+      }
       const PivotCounts pc = probe_counts<false>(B, trow, V, pv, 0u);
       const double* n = pc.n;
       const uint32_t* piv = pv.m;
@@ -233,10 +245,13 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void probe_kernel(ProbeParams P) {
     }
     const uint32_t K = static_cast<uint32_t>(lo);
     const double need = k - c_up;  // entries with key K to take, lowest indices first
-    // the smallest J with #{key == K, v <= J} >= need; every entry with key K
-    // is taken when there are exactly need of them
+    // the smallest J with #{key == K, v <= J} >= need.  Every entry with key K
+    // is gathered when there are exactly need of them, or when all entries at
+    // and above K fit the gathered set (the ordering then picks the lowest
+    // indices); otherwise the index search finds J.
+    const bool gather_all = c_lo - c_up == need || c_lo <= static_cast<double>(PROBE_SEL_CAP);
     int J = V - 1;
-    if (c_lo - c_up > need) {
+    if (!gather_all) {
       // invariants: #{key == K, v <= jhi} >= need > #{key == K, v < jlo}
       int jlo = 0, jhi = V - 1;
       while (jlo < jhi) {
@@ -272,7 +287,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void probe_kernel(ProbeParams P) {
           const int v = c * CHUNK + elem_offset(B.lane, e);
           if (key > K || (key == K && v <= J)) {
             const int slot = atomicAdd(&sh.n_sel, 1);
-            if (slot < SAKI_MAX_PROBE_K) {
+            if (slot < PROBE_SEL_CAP) {
               sh.sel_idx[slot] = v;
               sh.sel_t[slot] = x[e];
             }
@@ -281,27 +296,30 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void probe_kernel(ProbeParams P) {
       }
     });
     __syncthreads();
+    // rank sort of the gathered entries by (t descending, index ascending)
+    const int n_all = min(sh.n_sel, PROBE_SEL_CAP);
+    if (B.tid < n_all) {
+      const int vi = sh.sel_idx[B.tid];
+      const float ti = sh.sel_t[B.tid];
+      int rank = 0;
+      for (int j = 0; j < n_all; ++j) {
+        const float tj = sh.sel_t[j];
+        rank += (tj > ti || (tj == ti && sh.sel_idx[j] < vi)) ? 1 : 0;
+      }
+      sh.ord_idx[rank] = vi;
+    }
+    __syncthreads();
+    const int n = min(n_all, k);
+    // S over the Top-k set and at the teacher mode, summed over the block
+    double pv2[2] = {0.0, 0.0};
+    if (B.tid < n) {
+      const double p = exp(static_cast<double>(Loader<T>::load1(srow + sh.ord_idx[B.tid])) - lse_s);
+      pv2[0] = p;
+      if (B.tid == 0) pv2[1] = p;
+    }
+    B.sum(pv2);
     if (B.tid == 0) {
-      const int n = min(sh.n_sel, k);
-      // order by (t descending, index ascending)
-      for (int i = 1; i < n; ++i) {
-        const int vi = sh.sel_idx[i];
-        const float ti = sh.sel_t[i];
-        int j = i - 1;
-        while (j >= 0 && (sh.sel_t[j] < ti || (sh.sel_t[j] == ti && sh.sel_idx[j] > vi))) {
-          sh.sel_idx[j + 1] = sh.sel_idx[j];
-          sh.sel_t[j + 1] = sh.sel_t[j];
-          --j;
-        }
-        sh.sel_idx[j + 1] = vi;
-        sh.sel_t[j + 1] = ti;
-      }
-      double ck = 0.0, c1 = 0.0;
-      for (int i = 0; i < n; ++i) {
-        const double p = exp(static_cast<double>(Loader<T>::load1(srow + sh.sel_idx[i])) - lse_s);
-        ck += p;
-        if (i == 0) c1 = p;
-      }
+      const double ck = pv2[0], c1 = pv2[1];
       const double kl = Td / St - (lse_t - lse_s);
       const double h = log(Ss) - Sa / Ss;  // lse_s - E_S[s]
       if (P.c1) P.c1[r] = static_cast<float>(c1);
@@ -310,7 +328,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void probe_kernel(ProbeParams P) {
       if (P.entropy) P.entropy[r] = static_cast<float>(fmax(h, 0.0));
       if (P.row_status) P.row_status[r] = SAKI_ROW_OK;
       if (P.topk)
-        for (int i = 0; i < k; ++i) P.topk[r * k + i] = i < n ? sh.sel_idx[i] : -1;
+        for (int i = 0; i < k; ++i) P.topk[r * k + i] = i < n ? sh.ord_idx[i] : -1;
     }
     __syncthreads();
   }
