@@ -213,91 +213,104 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void probe_kernel(ProbeParams P) {
     int n_ge = 0;
     for (int u = 0; u < NT; ++u) n_ge += (sh.thread_max[u] >= Lt) ? 1 : 0;
     const float L = B.max(n_ge >= k ? Lt : -finf());
-    uint64_t lo = OrderKey<T>::of(L), hi = OrderKey<T>::of(mt);
-    double c_lo = __builtin_huge_val(), c_up = 0.0;
-    while (lo < hi) {
-      Pivots pv;  // in (lo, hi], non-decreasing
+    // Gathers into LDS the entries with KEEP(key, logit, index); every thread
+    // gets the number that matched (the set holds the first PROBE_SEL_CAP).
+    auto gather = [&](auto keep) {
+      if (B.tid == 0) sh.n_sel = 0;
+      __syncthreads();
+      for_chunks1<T, NW>(trow, V, B.wave, B.lane, [&](auto tail, const float* x, uint32_t vm, int c) {
+        constexpr bool TAIL = decltype(tail)::value;
 #pragma unroll
-      for (int i = 0; i < PROBE_PIVOTS; ++i)
-        pv.m[i] = static_cast<uint32_t>(lo + 1 + (hi - lo) * static_cast<uint64_t>(i + 1) / (PROBE_PIVOTS + 1));
-      if (c_lo == __builtin_huge_val()) {
-        // first sweep: lo itself (its count), then lo + 1, lo + 2, lo + 4, ...:
-        // L is usually the k-th largest logit itself (the Top-k entries lie in
-        // different threads), and then this sweep ends the search
-#pragma unroll
-        for (int i = 0; i < PROBE_PIVOTS; ++i)
-          pv.m[i] = static_cast<uint32_t>(i == 0 ? lo : (lo + (1ull << (i - 1)) < hi ? lo + (1ull << (i - 1)) : hi));
-      }
-      const PivotCounts pc = probe_counts<false>(B, trow, V, pv, 0u);
-      const double* n = pc.n;
-      const uint32_t* piv = pv.m;
-      // counts fall as pivots rise: lo moves to the last pivot with count >= k,
-      // hi below the first with count < k (static indices: no scratch arrays)
-      uint64_t lo2 = lo, hi2 = hi;
-      double c_lo2 = c_lo, c_up2 = c_up;
-#pragma unroll
-      for (int i = 0; i < PROBE_PIVOTS; ++i)
-        if (n[i] >= k) { lo2 = piv[i]; c_lo2 = n[i]; }
-#pragma unroll
-      for (int i = PROBE_PIVOTS - 1; i >= 0; --i)
-        if (n[i] < k) { hi2 = static_cast<uint64_t>(piv[i]) - 1; c_up2 = n[i]; }
-      lo = lo2; hi = hi2; c_lo = c_lo2; c_up = c_up2;
-    }
-    const uint32_t K = static_cast<uint32_t>(lo);
-    const double need = k - c_up;  // entries with key K to take, lowest indices first
-    // the smallest J with #{key == K, v <= J} >= need.  Every entry with key K
-    // is gathered when there are exactly need of them, or when all entries at
-    // and above K fit the gathered set (the ordering then picks the lowest
-    // indices); otherwise the index search finds J.
-    const bool gather_all = c_lo - c_up == need || c_lo <= static_cast<double>(PROBE_SEL_CAP);
-    int J = V - 1;
-    if (!gather_all) {
-      // invariants: #{key == K, v <= jhi} >= need > #{key == K, v < jlo}
-      int jlo = 0, jhi = V - 1;
-      while (jlo < jhi) {
-        Pivots pv;  // in [jlo, jhi), non-decreasing
-#pragma unroll
-        for (int i = 0; i < PROBE_PIVOTS; ++i)
-          pv.m[i] = static_cast<uint32_t>(jlo + static_cast<int>(static_cast<int64_t>(jhi - jlo) * (i + 1) / (PROBE_PIVOTS + 1)));
-        const PivotCounts pc = probe_counts<true>(B, trow, V, pv, K);
-        const double* n = pc.n;
-        const uint32_t* piv = pv.m;
-        // counts grow with the pivot: jlo moves past the last pivot with count
-        // < need, jhi to the first with count >= need
-        int jlo2 = jlo, jhi2 = jhi;
-#pragma unroll
-        for (int i = 0; i < PROBE_PIVOTS; ++i)
-          if (n[i] < need) jlo2 = static_cast<int>(piv[i]) + 1;
-#pragma unroll
-        for (int i = PROBE_PIVOTS - 1; i >= 0; --i)
-          if (n[i] >= need) jhi2 = static_cast<int>(piv[i]);
-        jlo = jlo2;
-        jhi = jhi2;
-      }
-      J = jlo;
-    }
-    if (B.tid == 0) sh.n_sel = 0;
-    __syncthreads();
-    for_chunks1<T, NW>(trow, V, B.wave, B.lane, [&](auto tail, const float* x, uint32_t vm, int c) {
-      constexpr bool TAIL = decltype(tail)::value;
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) {
-        if (!TAIL || ((vm >> e) & 1u)) {
-          const uint32_t key = OrderKey<T>::of(x[e]);
-          const int v = c * CHUNK + elem_offset(B.lane, e);
-          if (key > K || (key == K && v <= J)) {
-            const int slot = atomicAdd(&sh.n_sel, 1);
-            if (slot < PROBE_SEL_CAP) {
-              sh.sel_idx[slot] = v;
-              sh.sel_t[slot] = x[e];
+        for (int e = 0; e < EPL; ++e) {
+          if (!TAIL || ((vm >> e) & 1u)) {
+            const int v = c * CHUNK + elem_offset(B.lane, e);
+            if (keep(OrderKey<T>::of(x[e]), x[e], v)) {
+              const int slot = atomicAdd(&sh.n_sel, 1);
+              if (slot < PROBE_SEL_CAP) {
+                sh.sel_idx[slot] = v;
+                sh.sel_t[slot] = x[e];
+              }
             }
           }
         }
+      });
+      __syncthreads();
+      const int n = sh.n_sel;
+      __syncthreads();  // read by every thread before the next gather clears it
+      return n;
+    };
+    // First sweep: every entry >= L (in the float order of the ranking below,
+    // so that -0 and +0 tie).  There are at least k of them, and when they fit
+    // the set holds the Top-k with all its ties: no counting sweep is needed.
+    int n_got = gather([&](uint32_t, float x, int) { return x >= L; });
+    if (n_got > PROBE_SEL_CAP) {
+      uint64_t lo = OrderKey<T>::of(L), hi = OrderKey<T>::of(mt);
+      double c_lo = __builtin_huge_val(), c_up = 0.0;
+      while (lo < hi) {
+        Pivots pv;  // in (lo, hi], non-decreasing
+#pragma unroll
+        for (int i = 0; i < PROBE_PIVOTS; ++i)
+          pv.m[i] = static_cast<uint32_t>(lo + 1 + (hi - lo) * static_cast<uint64_t>(i + 1) / (PROBE_PIVOTS + 1));
+        if (c_lo == __builtin_huge_val()) {
+          // first sweep: lo itself (its count), then lo + 1, lo + 2, lo + 4, ...:
+          // L is usually the k-th largest logit itself (the Top-k entries lie in
+          // different threads), and then this sweep ends the search
+#pragma unroll
+          for (int i = 0; i < PROBE_PIVOTS; ++i)
+            pv.m[i] = static_cast<uint32_t>(i == 0 ? lo : (lo + (1ull << (i - 1)) < hi ? lo + (1ull << (i - 1)) : hi));
+        }
+        const PivotCounts pc = probe_counts<false>(B, trow, V, pv, 0u);
+        const double* n = pc.n;
+        const uint32_t* piv = pv.m;
+        // counts fall as pivots rise: lo moves to the last pivot with count >= k,
+        // hi below the first with count < k (static indices: no scratch arrays)
+        uint64_t lo2 = lo, hi2 = hi;
+        double c_lo2 = c_lo, c_up2 = c_up;
+#pragma unroll
+        for (int i = 0; i < PROBE_PIVOTS; ++i)
+          if (n[i] >= k) { lo2 = piv[i]; c_lo2 = n[i]; }
+#pragma unroll
+        for (int i = PROBE_PIVOTS - 1; i >= 0; --i)
+          if (n[i] < k) { hi2 = static_cast<uint64_t>(piv[i]) - 1; c_up2 = n[i]; }
+        lo = lo2; hi = hi2; c_lo = c_lo2; c_up = c_up2;
       }
-    });
-    __syncthreads();
+      const uint32_t K = static_cast<uint32_t>(lo);
+      const double need = k - c_up;  // entries with key K to take, lowest indices first
+      // the smallest J with #{key == K, v <= J} >= need.  Every entry with key K
+      // is gathered when there are exactly need of them, or when all entries at
+      // and above K fit the gathered set (the ordering then picks the lowest
+      // indices); otherwise the index search finds J.
+      const bool gather_all = c_lo - c_up == need || c_lo <= static_cast<double>(PROBE_SEL_CAP);
+      int J = V - 1;
+      if (!gather_all) {
+        // invariants: #{key == K, v <= jhi} >= need > #{key == K, v < jlo}
+        int jlo = 0, jhi = V - 1;
+        while (jlo < jhi) {
+          Pivots pv;  // in [jlo, jhi), non-decreasing
+#pragma unroll
+          for (int i = 0; i < PROBE_PIVOTS; ++i)
+            pv.m[i] = static_cast<uint32_t>(jlo + static_cast<int>(static_cast<int64_t>(jhi - jlo) * (i + 1) / (PROBE_PIVOTS + 1)));
+          const PivotCounts pc = probe_counts<true>(B, trow, V, pv, K);
+          const double* n = pc.n;
+          const uint32_t* piv = pv.m;
+          // counts grow with the pivot: jlo moves past the last pivot with count
+          // < need, jhi to the first with count >= need
+          int jlo2 = jlo, jhi2 = jhi;
+#pragma unroll
+          for (int i = 0; i < PROBE_PIVOTS; ++i)
+            if (n[i] < need) jlo2 = static_cast<int>(piv[i]) + 1;
+#pragma unroll
+          for (int i = PROBE_PIVOTS - 1; i >= 0; --i)
+            if (n[i] >= need) jhi2 = static_cast<int>(piv[i]);
+          jlo = jlo2;
+          jhi = jhi2;
+        }
+        J = jlo;
+      }
+      n_got = gather([&](uint32_t key, float, int v) { return key > K || (key == K && v <= J); });
+    }
     // rank sort of the gathered entries by (t descending, index ascending)
-    const int n_all = min(sh.n_sel, PROBE_SEL_CAP);
+    const int n_all = min(n_got, PROBE_SEL_CAP);
     if (B.tid < n_all) {
       const int vi = sh.sel_idx[B.tid];
       const float ti = sh.sel_t[B.tid];
