@@ -2,13 +2,16 @@
 // teacher T = softmax(t) at each row (the paper's probe analysis):
 //   C_1 = S(v*_T), C_k = sum of S over the teacher's Top-k set (ties to the
 //   lower index), KL(T || S) = E_T[t - s] - (lse_t - lse_s), H(S).
-// One workgroup per row.  A sweep gives the normalisers and moments; the
-// teacher's k-th largest logit is found by a search over the logits'
-// order-preserving integer images (16 bits for bf16, 32 for f32) that counts
-// twelve pivots per sweep (a 13-way split: 5 sweeps for bf16, 9 for f32); ties
-// at the threshold go to the lowest indices (the same search over the index,
-// only when the threshold value has more entries than are taken), and a last
-// sweep gathers the Top-k set.
+// One workgroup per row.  A sweep gives the normalisers and moments, each
+// thread's largest teacher logit and each chunk's.  L, the k-th largest of the
+// threads' maxima, bounds the k-th largest logit from below, and the entries
+// at or above L are gathered from the chunks whose maximum reaches L (a few
+// chunks of the row).  When more entries than LDS holds reach L, the k-th
+// largest logit is found by a search over the logits' order-preserving integer
+// images (16 bits for bf16, 32 for f32) that counts twelve pivots per sweep;
+// ties at the threshold go to the lowest indices (the same search over the
+// index, only when the threshold value has more entries than are taken), and
+// a last sweep gathers the Top-k set.
 #pragma once
 
 #include "row_engine.hpp"
@@ -53,6 +56,11 @@ struct OrderKey<float> {
 // when they fit, every entry at it (ties then need no index search).
 constexpr int PROBE_SEL_CAP = NT;
 static_assert(PROBE_SEL_CAP >= SAKI_MAX_PROBE_K, "the gathered set holds the Top-k");
+// Rows of up to PROBE_MAXC chunks keep each chunk's largest teacher logit.
+constexpr int PROBE_MAXC = 512;
+// Workgroups per CU: four, so that while some are in a row's serial steps
+// (reductions, the threshold, the gathering) the others stream.
+constexpr int PROBE_WG_PER_CU = 4;
 
 struct ProbeShared {
   double red_d[NT / WAVE][RED_MAX];
@@ -60,6 +68,7 @@ struct ProbeShared {
   int red_i[NT / WAVE][4];
   int n_sel;
   float thread_max[NT];  // each thread's largest teacher logit of the row
+  float chunk_tmax[PROBE_MAXC];  // each chunk's largest teacher logit
   int sel_idx[PROBE_SEL_CAP];   // gathered entries, in arrival order
   float sel_t[PROBE_SEL_CAP];
   int ord_idx[PROBE_SEL_CAP];   // the same entries by (t descending, index ascending)
@@ -117,11 +126,12 @@ __device__ __forceinline__ PivotCounts probe_counts(Block<NT, ProbeShared>& B, c
 }
 
 template <typename T>
-__global__ __launch_bounds__(NT, WG_PER_CU) void probe_kernel(ProbeParams P) {
+__global__ __launch_bounds__(NT, PROBE_WG_PER_CU) void probe_kernel(ProbeParams P) {
   __shared__ ProbeShared sh;
   Block<NT, ProbeShared> B(sh);
   constexpr int NW = NT / WAVE;
   const int V = P.V, k = P.k;
+  const int nch = (V + CHUNK - 1) / CHUNK;
   for (int64_t r = blockIdx.x; r < P.n_rows; r += gridDim.x) {
     const T* srow = static_cast<const T*>(P.s) + r * P.stride;
     const T* trow = static_cast<const T*>(P.t) + r * P.stride;
@@ -146,6 +156,8 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void probe_kernel(ProbeParams P) {
                         }
                         finite = finite && !wave_any(!fin);
                         Lt = fmaxf(Lt, lt);
+                        const float cmt = wave_max(lt);
+                        if (c < PROBE_MAXC && B.lane == 0) sh.chunk_tmax[c] = cmt;
                         if (wave_any(ls > Ms)) {
                           const float m = wave_max(ls);
                           const double f = static_cast<double>(fexp2((Ms - m) * LOG2E));
@@ -154,8 +166,8 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void probe_kernel(ProbeParams P) {
                           Ss *= f;
                           Ms = m;
                         }
-                        if (wave_any(lt > Mt)) {
-                          const float m = wave_max(lt);
+                        if (cmt > Mt) {
+                          const float m = cmt;
                           const double f = static_cast<double>(fexp2((Mt - m) * LOG2E));
                           St *= f;
                           Td *= f;
@@ -242,7 +254,37 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void probe_kernel(ProbeParams P) {
     // First sweep: every entry >= L (in the float order of the ranking below,
     // so that -0 and +0 tie).  There are at least k of them, and when they fit
     // the set holds the Top-k with all its ties: no counting sweep is needed.
-    int n_got = gather([&](uint32_t, float x, int) { return x >= L; });
+    int n_got;
+    if (nch <= PROBE_MAXC) {
+      // only the chunks whose maximum reaches L hold such entries; the test is
+      // uniform in the wave that owns the chunk (and stored its maximum)
+      if (B.tid == 0) sh.n_sel = 0;
+      __syncthreads();
+      for (int c = B.wave; c < nch; c += NW) {
+        if (!(sh.chunk_tmax[c] >= L)) continue;
+        float x[EPL];
+        uint32_t vm;
+        if (c < V / CHUNK)
+          load_lane<T, false>(trow, c, B.lane, V, x, &vm);
+        else
+          load_lane<T, true>(trow, c, B.lane, V, x, &vm);
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) {
+          if (((vm >> e) & 1u) && x[e] >= L) {
+            const int slot = atomicAdd(&sh.n_sel, 1);
+            if (slot < PROBE_SEL_CAP) {
+              sh.sel_idx[slot] = c * CHUNK + elem_offset(B.lane, e);
+              sh.sel_t[slot] = x[e];
+            }
+          }
+        }
+      }
+      __syncthreads();
+      n_got = sh.n_sel;
+      __syncthreads();  // read by every thread before a later gather clears it
+    } else {
+      n_got = gather([&](uint32_t, float x, int) { return x >= L; });
+    }
     if (n_got > PROBE_SEL_CAP) {
       uint64_t lo = OrderKey<T>::of(L), hi = OrderKey<T>::of(mt);
       double c_lo = __builtin_huge_val(), c_up = 0.0;

@@ -1064,7 +1064,7 @@ saki_status saki_probe_metrics(const saki_rows* in, int32_t k, float* c1, float*
   P.entropy = entropy;
   P.topk = topk;
   P.row_status = row_status;
-  const int grid = static_cast<int>(std::min<int64_t>(in->n_rows, static_cast<int64_t>(cus) * saki::WG_PER_CU));
+  const int grid = static_cast<int>(std::min<int64_t>(in->n_rows, static_cast<int64_t>(cus) * saki::PROBE_WG_PER_CU));
   hipStream_t hs = static_cast<hipStream_t>(stream);
   if (in->dtype == SAKI_BF16)
     hipLaunchKernelGGL(saki::probe_kernel<uint16_t>, dim3(grid), dim3(saki::NT), 0, hs, P);

@@ -60,3 +60,19 @@ def test_probe_ties_ragged_vocab_and_bad_rows(saki_lib):
     assert int(out["row_status"][7]) == 1 and torch.isnan(out["c1"][7])
     assert torch.all(out["topk"][7] == -1)
     assert int(out["row_status"][6]) == 0
+
+
+def test_probe_vocab_beyond_chunk_table(saki_lib):
+    # more than 512 chunks of 1024 entries (the per-chunk maxima are then not
+    # kept and every gather is a full sweep), with a ragged last chunk
+    V = 512 * 1024 + 1001
+    g = torch.Generator(device="cpu").manual_seed(5)
+    s = (torch.randn(6, V, generator=g) * 3).to(torch.bfloat16)
+    t = (torch.randn(6, V, generator=g) * 3).to(torch.bfloat16)
+    t[2] = torch.round(t[2].float())  # heavy ties at the threshold
+    t[4] = -2.0                       # all equal
+    S, T = saki_lib.alloc_rows(6, V, torch.bfloat16, DEV), saki_lib.alloc_rows(6, V, torch.bfloat16, DEV)
+    S.copy_(s)
+    T.copy_(t)
+    _check(saki_lib, S, T, 16)
+    assert list(_check(saki_lib, S, T, 16, rows=[4])[0]["topk"][0]) == list(range(16))
