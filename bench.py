@@ -18,38 +18,43 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
 
-# The sources the couple and route kernels are built from (the probe and
-# rollout kernels live in headers of their own, which these kernels do not use).
-KERNEL_SOURCES = ["include/saki.h", "paper_2609_36601_amd/csrc/saki.hip", "paper_2609_36601_amd/csrc/row_engine.hpp",
-                  "paper_2609_36601_amd/csrc/device_util.hpp"]
+# The sources each measured kernel is built from (the rollout kernels live in a
+# header of their own, which these kernels do not use).
+_CORE_SOURCES = ["include/saki.h", "paper_2609_36601_amd/csrc/saki.hip", "paper_2609_36601_amd/csrc/row_engine.hpp",
+                 "paper_2609_36601_amd/csrc/device_util.hpp"]
+KERNEL_SOURCES = {"couple": _CORE_SOURCES, "route": _CORE_SOURCES,
+                  "probe": _CORE_SOURCES + ["paper_2609_36601_amd/csrc/probe.hpp"]}
 
 # HBM traffic of one launch of the dominant kernel, from two rocprofv3 --pmc
 # runs (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch): the couple kernel on the
-# large workload at eps 0.2 (profiles/couple_kernel_large.md) and the route
-# kernel on the same rows (profiles/route_kernel_large.md).  A plain 1 GiB
-# device copy reads FETCH_SIZE = 524,309 KiB and WRITE_SIZE = 1,048,576 KiB on
-# the same box, so FETCH_SIZE is scaled by 2.0 and WRITE_SIZE by 1.0.  Keyed by
-# the SHA-256 of the kernel sources: a changed kernel reports traffic = null
+# large workload at eps 0.2 (profiles/couple_kernel_large.md), the route kernel
+# on the same rows (profiles/route_kernel_large.md) and the probe kernel on
+# 4,096 of them (profiles/probe_kernel_large.md).  A plain 1 GiB device copy
+# reads FETCH_SIZE = 524,309 KiB and WRITE_SIZE = 1,048,576 KiB on the same
+# box, so FETCH_SIZE is scaled by 2.0 and WRITE_SIZE by 1.0.  Keyed by the
+# SHA-256 of the kernel's sources: a changed kernel reports traffic = null
 # until re-measured.
 MEASURED_TRAFFIC = {
-    "1c269644ad79dd54edbadb0d61355811e4644612b4910cfc5a0d8c484da30623": {
-        "couple": dict(fetch_kib=55343079.9, write_kib=41529901.6, fetch_scale=2.0, write_scale=1.0),
-        "route": dict(fetch_kib=17096676.1, write_kib=42635141.7, fetch_scale=2.0, write_scale=1.0),
-    },
+    "couple": {"f51fe5a2645edb0209150c5d1820d9a08d08d26f74d9e62b40091e678abdcaa2":
+               dict(fetch_kib=55341600.8, write_kib=41626396.8, fetch_scale=2.0, write_scale=1.0)},
+    "route": {"f51fe5a2645edb0209150c5d1820d9a08d08d26f74d9e62b40091e678abdcaa2":
+              dict(fetch_kib=17096839.0, write_kib=42813865.5, fetch_scale=2.0, write_scale=1.0)},
+    "probe": {"8dbe62cff38f719884516372a45eb76de659e622bd83f5274dc23a4fc10d7b3e":
+              dict(fetch_kib=1307172.1, write_kib=33216.9, fetch_scale=2.0, write_scale=1.0)},
 }
 
 
-def kernel_source_hash():
+def kernel_source_hash(workload="couple"):
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in KERNEL_SOURCES[workload]:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
 
 
 def measured_traffic_bytes(workload="couple"):
-    m = MEASURED_TRAFFIC.get(kernel_source_hash(), {}).get(workload)
+    m = MEASURED_TRAFFIC.get(workload, {}).get(kernel_source_hash(workload))
     if m is None:
         return None
     return (m["fetch_kib"] * m["fetch_scale"] + m["write_kib"] * m["write_scale"]) * 1024.0
@@ -493,7 +498,8 @@ def bench_probe(args, saki, workloads, dev):
                    "workload": "probe: 4,096 rows of the large workload, V=151,936 bf16, k=16",
                    "rows": n, "vocab": V, "k": k, "mean_c16": float(out["ck"].mean())},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None},
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": measured_traffic_bytes("probe") if n == 4096 else None},
         "cpu_baseline": None,
     }
     print(json.dumps(line), flush=True)

@@ -58,9 +58,9 @@ constexpr int PROBE_SEL_CAP = NT;
 static_assert(PROBE_SEL_CAP >= SAKI_MAX_PROBE_K, "the gathered set holds the Top-k");
 // Rows of up to PROBE_MAXC chunks keep each chunk's largest teacher logit.
 constexpr int PROBE_MAXC = 512;
-// Workgroups per CU: four, so that while some are in a row's serial steps
+// Workgroups per CU: three, so that while some are in a row's serial steps
 // (reductions, the threshold, the gathering) the others stream.
-constexpr int PROBE_WG_PER_CU = 4;
+constexpr int PROBE_WG_PER_CU = 3;
 
 struct ProbeShared {
   double red_d[NT / WAVE][RED_MAX];

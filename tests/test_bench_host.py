@@ -30,10 +30,13 @@ def test_help_lists_the_workloads():
 def test_traffic_table_is_keyed_by_source_hash():
     sys.path.insert(0, ROOT)
     import bench
-    h = bench.kernel_source_hash()
-    assert len(h) == 64
-    t = bench.measured_traffic_bytes()
-    # either the counters were taken for exactly these sources, or traffic is unknown
-    assert (t is None) == (h not in bench.MEASURED_TRAFFIC)
-    if t is not None:
-        assert 79e9 < t < 400e9  # at least the algorithmic 79.7 GB
+    # algorithmic bytes per launch: couple 79.7 GB, route 59.7 GB, probe 2.49 GB
+    floor = {"couple": 79e9, "route": 59e9, "probe": 2.4e9}
+    for w in ("couple", "route", "probe"):
+        h = bench.kernel_source_hash(w)
+        assert len(h) == 64
+        t = bench.measured_traffic_bytes(w)
+        # either the counters were taken for exactly these sources, or traffic is unknown
+        assert (t is None) == (h not in bench.MEASURED_TRAFFIC[w])
+        if t is not None:
+            assert floor[w] < t < 5 * floor[w]
