@@ -8,7 +8,7 @@
 // at or above L are gathered from the chunks whose maximum reaches L (a few
 // chunks of the row).  When more entries than LDS holds reach L, the k-th
 // largest logit is found by a search over the logits' order-preserving integer
-// images (16 bits for bf16, 32 for f32) that counts twelve pivots per sweep;
+// images (16 bits for bf16, 32 for f32) that counts four pivots per sweep;
 // ties at the threshold go to the lowest indices (the same search over the
 // index, only when the threshold value has more entries than are taken), and
 // a last sweep gathers the Top-k set.
@@ -74,8 +74,10 @@ struct ProbeShared {
   int ord_idx[PROBE_SEL_CAP];   // the same entries by (t descending, index ascending)
 };
 
-// Pivots counted per sweep in the Top-k searches (one block sum of RED_MAX doubles).
-constexpr int PROBE_PIVOTS = 12;
+// Pivots counted per sweep in the Top-k searches (one block sum of that many
+// doubles).  Four keep the kernel free of register spills at three workgroups
+// per CU; the searches run only when more than PROBE_SEL_CAP entries reach L.
+constexpr int PROBE_PIVOTS = 4;
 
 struct Pivots {
   uint32_t m[PROBE_PIVOTS];
