@@ -39,8 +39,8 @@ MEASURED_TRAFFIC = {
                dict(fetch_kib=55341600.8, write_kib=41626396.8, fetch_scale=2.0, write_scale=1.0)},
     "route": {"f51fe5a2645edb0209150c5d1820d9a08d08d26f74d9e62b40091e678abdcaa2":
               dict(fetch_kib=17096839.0, write_kib=42813865.5, fetch_scale=2.0, write_scale=1.0)},
-    "probe": {"bc12749280eb95864f5470918f52348c80d2f3e640278f96216e1d2770744968":
-              dict(fetch_kib=1284975.0, write_kib=952.75, fetch_scale=2.0, write_scale=1.0)},
+    "probe": {"14f43ec556f3a13ee2fade7ce9ee22e5b1e61ed67aa7c256860eb9b7c7201bc2":
+              dict(fetch_kib=1284865.6, write_kib=939.2, fetch_scale=2.0, write_scale=1.0)},
 }
 
 

@@ -39,7 +39,7 @@ template <>
 struct OrderKey<uint16_t> {
   static constexpr int BITS = 16;
   static __device__ __forceinline__ uint32_t of(float x) {
-    const uint32_t u = __float_as_uint(x);
+    const uint32_t u = x == 0.0f ? 0u : __float_as_uint(x);  // -0 and +0 tie
     return ((u >> 31) ? ~u : (u | 0x80000000u)) >> 16;
   }
 };
@@ -47,7 +47,7 @@ template <>
 struct OrderKey<float> {
   static constexpr int BITS = 32;
   static __device__ __forceinline__ uint32_t of(float x) {
-    const uint32_t u = __float_as_uint(x);
+    const uint32_t u = x == 0.0f ? 0u : __float_as_uint(x);  // -0 and +0 tie
     return (u >> 31) ? ~u : (u | 0x80000000u);
   }
 };

@@ -76,3 +76,22 @@ def test_probe_vocab_beyond_chunk_table(saki_lib):
     T.copy_(t)
     _check(saki_lib, S, T, 16)
     assert list(_check(saki_lib, S, T, 16, rows=[4])[0]["topk"][0]) == list(range(16))
+
+
+def test_probe_signed_zero_ties_past_the_gather_capacity(saki_lib):
+    # ten positive teacher logits, then 3,000 zeros of both signs: the 16th
+    # largest value is 0, more than 256 entries reach it (the counting search
+    # runs), and -0 and +0 tie, so the six lowest-index zeros complete the set
+    V, k = 3010, 16
+    g = torch.Generator(device="cpu").manual_seed(11)
+    s = (torch.randn(4, V, generator=g) * 2).to(torch.bfloat16)
+    sign = torch.where(torch.rand(4, V, generator=g) < 0.5, -1.0, 1.0)
+    t = sign * 0.0
+    pos = torch.stack([torch.randperm(V, generator=g)[:10] for _ in range(4)])
+    t.scatter_(1, pos, torch.rand(4, 10, generator=g) + 1.0)
+    t[1, :8] = -0.0  # the lowest indices are -0 in this row
+    S, T = saki_lib.alloc_rows(4, V, torch.bfloat16, DEV), saki_lib.alloc_rows(4, V, torch.bfloat16, DEV)
+    S.copy_(s)
+    T.copy_(t.to(torch.bfloat16))
+    assert torch.signbit(T.float()).any() and (T.float() == 0).sum() > 4 * 256
+    _check(saki_lib, S, T, k)
