@@ -35,11 +35,11 @@ KERNEL_SOURCES = {"couple": _CORE_SOURCES, "route": _CORE_SOURCES,
 # SHA-256 of the kernel's sources: a changed kernel reports traffic = null
 # until re-measured.
 MEASURED_TRAFFIC = {
-    "couple": {"f51fe5a2645edb0209150c5d1820d9a08d08d26f74d9e62b40091e678abdcaa2":
+    "couple": {"a734d2e29a9c6b0c8263f3415efcfe7a5a2f371b6b7dea7f896a98ceeef8676c":
                dict(fetch_kib=55341600.8, write_kib=41626396.8, fetch_scale=2.0, write_scale=1.0)},
-    "route": {"f51fe5a2645edb0209150c5d1820d9a08d08d26f74d9e62b40091e678abdcaa2":
+    "route": {"a734d2e29a9c6b0c8263f3415efcfe7a5a2f371b6b7dea7f896a98ceeef8676c":
               dict(fetch_kib=17096839.0, write_kib=42813865.5, fetch_scale=2.0, write_scale=1.0)},
-    "probe": {"14f43ec556f3a13ee2fade7ce9ee22e5b1e61ed67aa7c256860eb9b7c7201bc2":
+    "probe": {"12ef1ba31790647def0782c558292ca4ac9c1c1157150bd79a38e1349be3ebc8":
               dict(fetch_kib=1284865.6, write_kib=939.2, fetch_scale=2.0, write_scale=1.0)},
 }
 

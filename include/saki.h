@@ -307,8 +307,10 @@ saki_status saki_select_positions(int32_t mode, int64_t n_traj, int64_t n_rows,
  *   topk       = [n_rows, k] the Top-k indices, best first.
  * Every output may be NULL.  1 <= k <= min(SAKI_MAX_PROBE_K, vocab).  Rows with a
  * non-finite logit get NaN metrics, topk -1 and row_status SAKI_ROW_NONFINITE.
- * One workgroup per row, with ~40 sweeps over the teacher row for the exact
- * Top-k threshold: meant for probe sets, not for every training position. */
+ * One workgroup per row: one sweep over both rows, then only the teacher
+ * chunks whose maximum reaches a lower bound of the k-th largest logit (a few
+ * per row); a row where more than 256 teacher entries reach that bound (heavy
+ * ties) takes a counting search of several more sweeps of the teacher row. */
 saki_status saki_probe_metrics(const saki_rows *in, int32_t k, float *c1, float *ck, float *kl_ts,
                                float *entropy, int32_t *topk, uint8_t *row_status,
                                saki_stream_t stream);
