@@ -31,7 +31,10 @@ from .coupling import residual_draw, CHUNK
 
 def verify_blocks(s, t, k, draft, eps, seed, row_offset=0, eos_id=-1, chunk=CHUNK):
     """Returns dict: accepted_len [B], correction [B], and per-position arrays
-    lam, kl, tv, accept_prob, u, margin, accepted (0/1), evaluated (0/1)."""
+    lam, kl, tv, accept_prob, u, margin, accepted (0/1), evaluated (0/1).
+    Positions are examined in order and the bridge is formed only at the
+    positions a block reaches (up to its first rejection): the per-position
+    values of positions after that are NaN."""
     s = np.atleast_2d(np.asarray(s, np.float64))
     t = np.atleast_2d(np.asarray(t, np.float64))
     n_rows, V = s.shape
@@ -41,13 +44,13 @@ def verify_blocks(s, t, k, draft, eps, seed, row_offset=0, eos_id=-1, chunk=CHUN
     finite = np.isfinite(s).all(axis=1) & np.isfinite(t).all(axis=1)
     ok_draft = (draft >= 0) & (draft < V)
     good = finite & ok_draft
-    b = bridge_rows(np.where(good[:, None], s, 0.0), np.where(good[:, None], t, 0.0), eps)
+    lam = np.full(n_rows, np.nan)
+    kl = np.full(n_rows, np.nan)
+    tv = np.full(n_rows, np.nan)
     alpha = np.full(n_rows, np.nan)
     u = np.full(n_rows, np.nan)
-    for r in np.nonzero(good)[0]:
-        z = draft[r]
-        alpha[r] = np.exp(min(0.0, b["logq"][r, z] - b["logp"][r, z]))
-        u[r] = philox.uniform(seed, philox.STREAM_ACCEPT, row_offset + r, 0)
+    logp = np.full((n_rows, V), np.nan)
+    logq = np.full((n_rows, V), np.nan)
     accepted = np.zeros(n_rows, np.int64)
     evaluated = np.zeros(n_rows, np.int64)
     acc_len = np.empty(B, np.int64)
@@ -62,6 +65,12 @@ def verify_blocks(s, t, k, draft, eps, seed, row_offset=0, eos_id=-1, chunk=CHUN
                 n = j
                 break
             evaluated[r] = 1
+            b = bridge_rows(s[r:r + 1], t[r:r + 1], eps)
+            lam[r], kl[r], tv[r] = b["lam"][0], b["kl"][0], b["tv"][0]
+            logp[r], logq[r] = b["logp"][0], b["logq"][0]
+            z = draft[r]
+            alpha[r] = np.exp(min(0.0, logq[r, z] - logp[r, z]))
+            u[r] = philox.uniform(seed, philox.STREAM_ACCEPT, row_offset + r, 0)
             if u[r] < alpha[r]:
                 accepted[r] = 1
                 if eos_id >= 0 and draft[r] == eos_id:
@@ -74,9 +83,9 @@ def verify_blocks(s, t, k, draft, eps, seed, row_offset=0, eos_id=-1, chunk=CHUN
         acc_len[blk] = n
         if draw:
             r = blk * k + n
-            c, gp = residual_draw(b["logp"][r], b["logq"][r], seed, row_offset + r, chunk)
+            c, gp = residual_draw(logp[r], logq[r], seed, row_offset + r, chunk)
             corr[blk] = c
             gaps[blk] = gp
-    return dict(accepted_len=acc_len, correction=corr, lam=b["lam"], kl=b["kl"], tv=b["tv"],
+    return dict(accepted_len=acc_len, correction=corr, lam=lam, kl=kl, tv=tv,
                 accept_prob=alpha, u=u, margin=np.abs(u - alpha), accepted=accepted,
-                evaluated=evaluated, good=good, gaps=gaps, logp=b["logp"], logq=b["logq"])
+                evaluated=evaluated, good=good, gaps=gaps, logp=logp, logq=logq)

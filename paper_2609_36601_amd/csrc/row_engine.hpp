@@ -22,24 +22,6 @@ namespace saki {
 
 constexpr int RED_MAX = 12;  // widest block reduction (doubles per thread)
 
-// MAXC: chunk capacity (rows of up to MAXC * CHUNK entries).  KC > 0 adds a
-// row cache of KC chunks per wave (bf16 rows): the stats sweep stores the
-// wave's last KC full chunks there and the later sweeps of the row read them
-// from LDS instead of memory (4 KiB per chunk: 1 KiB each of s and t per half).
-template <int NT, int MAXC = MAX_CHUNKS, int KC = 0>
-struct RowShared {
-  static constexpr int NW = NT / WAVE;
-  static constexpr int CACHE_CHUNKS = KC;
-  float chunk_a[MAXC];  // proposal: reference (log2 units) | residual: chunk mass
-  float chunk_b[MAXC];  // proposal: chunk sum of 2^(s log2 e - reference)
-  float chunk_c[MAXC];  // teacher draw: reference (log2 units)
-  float chunk_d[MAXC];  // teacher draw: chunk sum of 2^(t log2 e - reference)
-  double red_d[NW][RED_MAX];
-  float red_f[NW][4];
-  int red_i[NW][4];
-  uint4 cache[KC > 0 ? NW * KC * 4 * WAVE : 1];  // [wave][slot][s0, s1, t0, t1][lane]
-};
-
 // Row-uniform results of the stats sweep.
 struct RowStats {
   float ms, mt;        // max s, max t
@@ -56,8 +38,36 @@ struct RowStats {
   float dmin, dmax;    // range of d = t - s
   float tmax;          // max t
   int vstar;           // argmax t, lowest index on ties
+  int sidx;            // argmax s (the dominant entry of p), lowest index on ties
+  float t_sidx;        // t at sidx
+  double pmax;         // max_v p_v = exp(ms - lse_s)
   bool finite;
 };
+
+// The row statistics as kept in LDS.
+struct RowStatsLDS {
+  RowStats r;
+};
+
+// MAXC: chunk capacity (rows of up to MAXC * CHUNK entries).  KC > 0 adds a
+// row cache of KC chunks per wave (bf16 rows): the stats sweep stores the
+// wave's last KC full chunks there and the later sweeps of the row read them
+// from LDS instead of memory (4 KiB per chunk: 1 KiB each of s and t per half).
+template <int NT, int MAXC = MAX_CHUNKS, int KC = 0>
+struct RowShared {
+  static constexpr int NW = NT / WAVE;
+  static constexpr int CACHE_CHUNKS = KC;
+  float chunk_a[MAXC];  // proposal: reference (log2 units) | residual: chunk mass
+  float chunk_b[MAXC];  // proposal: chunk sum of 2^(s log2 e - reference)
+  float chunk_c[MAXC];  // teacher draw: reference (log2 units)
+  float chunk_d[MAXC];  // teacher draw: chunk sum of 2^(t log2 e - reference)
+  double red_d[NW][RED_MAX];
+  float red_f[NW][4];
+  int red_i[NW][4];
+  uint4 cache[KC > 0 ? NW * KC * 4 * WAVE : 1];  // [wave][slot][s0, s1, t0, t1][lane]
+  RowStatsLDS rs;  // the current row's statistics (stats_sweep)
+};
+
 
 template <int NT, typename SH = RowShared<NT>>
 struct Block {
@@ -365,6 +375,8 @@ struct StatsAcc {
   float S1, S2, S3, S4;         // per-lane p-weighted powers of d (relative to Ms)
   float T1, T2;                 // per-lane pi-weighted sums of d, d^2 (relative to Mt)
   int tidx;                     // wave-uniform lowest index of the running max of t
+  int sidx;                     // wave-uniform lowest index of the running max of s
+  float t_sidx;                 // t at sidx
   float dmin, dmax;             // per-lane range of d
   __device__ void init() {
     Ms = -finf(); Mt = -finf();
@@ -372,6 +384,8 @@ struct StatsAcc {
     Ss = St = 0.0;
     S1 = S2 = S3 = S4 = T1 = T2 = 0.f;
     tidx = 0x7fffffff;
+    sidx = 0x7fffffff;
+    t_sidx = 0.f;
     dmin = finf(); dmax = -finf();
   }
 };
@@ -404,6 +418,15 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
   a.dmax = fmaxf(a.dmax, lmax);
   if (wave_any(ls > a.Ms)) {
     const float cms = wave_max(ls);
+    // a new running maximum of s: its lowest index in this chunk, and its t
+    int li = 0x7fffffff;
+    float lt = 0.f;
+#pragma unroll
+    for (int e = EPL - 1; e >= 0; --e)
+      if (SAKI_VALID(e) && s[e] == cms) { li = c * CHUNK + elem_offset(lane, e); lt = t[e]; }
+    wave_min_index_with(li, lt);
+    a.sidx = li;
+    a.t_sidx = lt;
     // rounded product and difference, never contracted into one fma: the sums
     // so far are relative to exactly the MsL the later terms use
     const float cmsL = __fmul_rn(cms, LOG2E);
@@ -429,10 +452,11 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
     a.Mt = cmt;
     a.MtL = cmtL;
   }
-  // normalisers: float sums of four entries (within three roundings each),
-  // then double
+  // normalisers: each term added in double (a float sum of terms next to a
+  // dominant one of ~1 would lose ~6e-8 of it: the log-probability of the
+  // dominant entry of a peaked row needs it)
   double ps = 0.0, pt = 0.0;
-  float gs = 0.f, gt = 0.f, p1 = 0.f, p2 = 0.f, p3 = 0.f, p4 = 0.f, t1 = 0.f, t2 = 0.f;
+  float p1 = 0.f, p2 = 0.f, p3 = 0.f, p4 = 0.f, t1 = 0.f, t2 = 0.f;
 #pragma unroll
   for (int e = 0; e < EPL; ++e) {
     float es = fexp2(fmaf(s[e], LOG2E, -a.MsL));
@@ -449,14 +473,8 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
     const float etd = et * d;
     t1 += etd;
     t2 = fmaf(etd, d, t2);
-    gs += es;
-    gt += et;
-    if ((e & 3) == 3) {
-      ps += static_cast<double>(gs);
-      pt += static_cast<double>(gt);
-      gs = 0.f;
-      gt = 0.f;
-    }
+    ps += static_cast<double>(es);
+    pt += static_cast<double>(et);
   }
   if (keep_chunks) {
     const float csum = static_cast<float>(wave_sum(ps));
@@ -488,6 +506,8 @@ struct StatsBlock {
   double Ss, S1, S2, S3, S4, St, T1, T2;
   float tbest;
   int tidx;
+  int sidx;
+  float t_sidx;
   float dmin, dmax;
 };
 
@@ -513,6 +533,8 @@ __device__ StatsBlock stats_combine_block(Block<NT, SH>& B, StatsAcc& a) {
     B.sh.red_f[B.wave][2] = wdmin;
     B.sh.red_f[B.wave][3] = wdmax;
     B.sh.red_i[B.wave][0] = a.tidx;
+    B.sh.red_i[B.wave][1] = a.sidx;
+    B.sh.red_d[B.wave][10] = static_cast<double>(a.t_sidx);
   }
   __syncthreads();
   StatsBlock O;
@@ -528,7 +550,8 @@ __device__ StatsBlock stats_combine_block(Block<NT, SH>& B, StatsAcc& a) {
   }
   double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   float tb = -finf();
-  int ti = 0x7fffffff;
+  int ti = 0x7fffffff, si = 0x7fffffff;
+  float st = 0.f;
   // each wave's sums are relative to 2^(its MsL): rescale to the block's
   // msL = ms log2(e) rounded (the MsL of a wave holding the maximum), then
   // remove that rounding (shift_correction)
@@ -544,13 +567,23 @@ __device__ StatsBlock stats_combine_block(Block<NT, SH>& B, StatsAcc& a) {
     for (int i = 5; i < 8; ++i) acc[i] += B.sh.red_d[w][i] * gt;
     const int wi = B.sh.red_i[w][0];
     if (wMt > tb || (wMt == tb && wi < ti)) { tb = wMt; ti = wi; }
+    const int ws = B.sh.red_i[w][1];
+    if (wMs == O.ms && ws < si) { si = ws; st = static_cast<float>(B.sh.red_d[w][10]); }
   }
   __syncthreads();
   const double cs = shift_correction(O.ms, msL), ct = shift_correction(O.mt, mtL);
-  O.Ss = acc[0] * cs; O.S1 = acc[1] * cs; O.S2 = acc[2] * cs; O.S3 = acc[3] * cs; O.S4 = acc[4] * cs;
-  O.St = acc[5] * ct; O.T1 = acc[6] * ct; O.T2 = acc[7] * ct;
+  // The maximum's own term went into the sums as 2^d0 rounded to float (d0 =
+  // the rounding of the shift, ~1e-6: a rounding of ~6e-8 next to 1); after
+  // the shift correction it is exactly 1.  The log-probability of a dominant
+  // entry (near 0 on a peaked row) needs that term exact.
+  const double dom_s = 1.0 - static_cast<double>(fexp2(fmaf(O.ms, LOG2E, -msL))) * cs;
+  const double dom_t = 1.0 - static_cast<double>(fexp2(fmaf(O.mt, LOG2E, -mtL))) * ct;
+  O.Ss = acc[0] * cs + dom_s; O.S1 = acc[1] * cs; O.S2 = acc[2] * cs; O.S3 = acc[3] * cs; O.S4 = acc[4] * cs;
+  O.St = acc[5] * ct + dom_t; O.T1 = acc[6] * ct; O.T2 = acc[7] * ct;
   O.tbest = tb;
   O.tidx = ti;
+  O.sidx = si;
+  O.t_sidx = st;
   return O;
 }
 
@@ -563,6 +596,8 @@ __device__ inline RowStats row_stats_from(const StatsBlock& O) {
   R.dmax = O.dmax;
   R.tmax = O.tbest;
   R.vstar = O.tidx;
+  R.sidx = O.sidx;
+  R.t_sidx = O.t_sidx;
   R.sum_s = O.Ss;
   R.lse_s = static_cast<double>(R.ms) + log(O.Ss);
   R.lse_t = static_cast<double>(R.mt) + log(O.St);
@@ -574,6 +609,7 @@ __device__ inline RowStats row_stats_from(const StatsBlock& O) {
   R.mean_pi = O.T1 / O.St;
   R.var_pi = fmax(O.T2 / O.St - R.mean_pi * R.mean_pi, 0.0);
   R.kl1_est = R.mean_pi - (R.lse_t - R.lse_s);
+  R.pmax = exp(static_cast<double>(R.ms) - R.lse_s);
   R.c = static_cast<float>(Ed);
   if (!isfinite(R.c)) R.c = 0.0f;
   R.cL = R.c * LOG2E;
@@ -583,9 +619,12 @@ __device__ inline RowStats row_stats_from(const StatsBlock& O) {
 }
 
 // keep_chunks: store the proposal chunk masses (of p); keep_teacher: those of pi.
+// The statistics are kept in the workgroup's LDS (thread 0 writes them): the
+// caller reads its fields there where it needs them rather than holding the
+// whole record in registers across the later sweeps.
 template <typename T, int NT, typename SH>
-__device__ RowStats stats_sweep(Block<NT, SH>& B, const T* srow, const T* trow, int V, bool keep_chunks,
-                                bool keep_teacher = false) {
+__device__ const RowStats& stats_sweep(Block<NT, SH>& B, const T* srow, const T* trow, int V, bool keep_chunks,
+                                       bool keep_teacher = false) {
   constexpr int NW = NT / WAVE;
   StatsAcc a;
   a.init();
@@ -594,7 +633,20 @@ __device__ RowStats stats_sweep(Block<NT, SH>& B, const T* srow, const T* trow, 
                       constexpr bool TAIL = decltype(tail)::value;
                       stats_math<TAIL>(s, t, vm, c, B.lane, keep_chunks, keep_teacher, B.sh, a);
                     }, row_cache<T>(B.sh));
-  return row_stats_from(stats_combine_block(B, a));
+  const StatsBlock O = stats_combine_block(B, a);
+  if (B.tid == 0) B.sh.rs.r = row_stats_from(O);
+  __syncthreads();
+  return B.sh.rs.r;
+}
+
+// Thread of a workgroup of NT threads that holds entry v in the chunk sweeps
+// (wave c % NW of chunk c = v / CHUNK, lane and slot by elem_offset).
+template <int NT>
+__device__ __forceinline__ int entry_owner(int v) {
+  constexpr int NW = NT / WAVE;
+  const int o = v % CHUNK;
+  const int lane = (o < 512) ? (o >> 3) : ((o - 512) >> 3);
+  return ((v / CHUNK) % NW) * WAVE + lane;
 }
 
 // ---------------------------------------------------------------------------
@@ -603,13 +655,17 @@ __device__ RowStats stats_sweep(Block<NT, SH>& B, const T* srow, const T* trow, 
 // sums kept are W = sum (w - p~) (so that A = log1p(W / sum p~) keeps its
 // relative precision when A is small) and S_k = sum w X^k, k = 1..4, which
 // give A(lam) and its first four derivatives, the cumulants of x under q_lam.
-//   FAST: w = 2^{a + lam X}.
-//   GEN : w = 2^{a + lam X - sigl}, with a shift sigl (log2 units) where
-//         lam (dmax - c) could overflow float.
-//   ACC : w - p~ = p~ expm1(lam x), with expm1 accurate for small arguments
-//         (rows whose KL is small).
+//   FAST : w = 2^{a + lam X}.
+//   ACC  : w - p~ = p~ expm1(lam x), with expm1 accurate for small arguments
+//          (rows whose KL is small).
+//   SHIFT: where lam (dmax - c) could overflow float, w' = 2^{a + lam X - sigl}
+//          with a shift sigl (log2 units); W = sum w' (plain form), or in the
+//          expm1 form sum (w' - p~') with w' - p~' = p~' expm1(lam x) where
+//          |lam x| < 1/16 (p~' = 2^{a - sigl}), so the sums keep their
+//          relative precision and do not overflow.  Rows need it rarely, so
+//          one loop serves both forms.
 // ---------------------------------------------------------------------------
-enum LamMode { LAM_FAST = 0, LAM_GEN = 1, LAM_ACC = 2 };
+enum LamMode { LAM_FAST = 0, LAM_ACC = 1, LAM_SHIFT = 2 };
 
 // exp(y) - 1 for |y| < 1/16 to ~1e-7 relative: the Taylor polynomial through
 // y^4 / 24 (the next term is below y^5 / 120).
@@ -637,7 +693,7 @@ struct LamEval {
 // row sums are multiplied by 2^-d0 once (shift_correction).
 template <int MODE, bool TAIL>
 __device__ __forceinline__ void lam_math(const float* s, const float* t, uint32_t vm, float msL,
-                                         float cL, float lam, float sigl, double (&acc)[5]) {
+                                         float cL, float lam, float sigl, bool accf, double (&acc)[5]) {
   float W = 0.f, S1 = 0.f, S2 = 0.f, S3 = 0.f, S4 = 0.f;
 #pragma unroll
   for (int e = 0; e < EPL; ++e) {
@@ -648,14 +704,16 @@ __device__ __forceinline__ void lam_math(const float* s, const float* t, uint32_
     if (MODE == LAM_FAST) {
       w = fexp2(fmaf(lam, X, a));
       u = w - pt;
-    } else if (MODE == LAM_GEN) {
-      w = fexp2(fmaf(lam, X, a) - sigl);
-      u = (sigl == 0.f) ? (w - pt) : w;
-    } else {
+    } else if (MODE == LAM_ACC) {
       const float yl = lam * X;
       const float ee = fexp2(yl);
       w = pt * ee;
       u = pt * expm1_sel(yl * LN2, ee);
+    } else {  // LAM_SHIFT: exponents shifted by sigl; accf selects the expm1 form
+      w = fexp2(fmaf(lam, X, a) - sigl);
+      const float y = lam * X * LN2;
+      const float ps = fexp2(a - sigl);
+      u = !accf ? w : (fabsf(y) < 0.0625f) ? ps * expm1_small(y) : w - ps;
     }
     if (TAIL && !SAKI_VALID(e)) { w = 0.f; u = 0.f; }
     const float wx = w * X;
@@ -675,21 +733,27 @@ __device__ __forceinline__ void lam_math(const float* s, const float* t, uint32_
 }
 
 // A and its derivatives at lam from the row sums v = {W, S1..S4} (log2
-// units) and b0 = sum p~.
-__device__ inline LamEval lam_finish(const double (&v)[5], double b0, float lam, float sigl) {
+// units) and b0 = sum p~.  acc: W = sum (w - p~), scaled by 2^-sigl when
+// sigl != 0; otherwise W = sum w when sigl != 0.
+__device__ inline LamEval lam_finish(const double (&v)[5], double b0, float lam, float sigl, bool acc) {
   LamEval E;
   E.lam = lam;
-  double S0;
+  double S0, r = 1.0;
   if (sigl == 0.f) {
     S0 = b0 + v[0];
     E.A = log1p(v[0] / b0);
+  } else if (acc) {
+    // the sums carry the factor 2^-sigl: undo it in double
+    r = exp2(static_cast<double>(sigl));
+    S0 = b0 + v[0] * r;
+    E.A = log1p(v[0] * r / b0);
   } else {
     // sigl is in log2 units: the shift in natural units is sigl ln 2
     S0 = v[0];
     E.A = static_cast<double>(sigl) * LN2_D + log(v[0] / b0);
   }
   // raw moments of X under q, then its cumulants; x = X ln 2
-  const double m1 = v[1] / S0, m2 = v[2] / S0, m3 = v[3] / S0, m4 = v[4] / S0;
+  const double m1 = v[1] * r / S0, m2 = v[2] * r / S0, m3 = v[3] * r / S0, m4 = v[4] * r / S0;
   const double c2 = fmax(m2 - m1 * m1, 0.0);
   const double c3 = m3 - 3.0 * m1 * m2 + 2.0 * m1 * m1 * m1;
   const double c4 = m4 - 4.0 * m1 * m3 + 6.0 * m1 * m1 * m2 - 3.0 * m1 * m1 * m1 * m1 - 3.0 * c2 * c2;
@@ -704,33 +768,58 @@ __device__ inline LamEval lam_finish(const double (&v)[5], double b0, float lam,
 
 template <typename T, int NT, int MODE, typename SH>
 __device__ LamEval lam_sweep_mode(Block<NT, SH>& B, const T* srow, const T* trow, int V, const RowStats& R,
-                                  float lam, float sigl) {
+                                  float lam, float sigl, bool accf) {
   constexpr int NW = NT / WAVE;
   double v[5] = {0, 0, 0, 0, 0};
   const float msL = R.ms * LOG2E;
   for_chunks<T, NW, false, use_mode<T, SH>()>(srow, trow, V, B.wave, B.lane,
                     [&](auto tail, const float* s, const float* t, uint32_t vm, int c) {
                       constexpr bool TAIL = decltype(tail)::value;
-                      lam_math<MODE, TAIL>(s, t, vm, msL, R.cL, lam, sigl, v);
+                      lam_math<MODE, TAIL>(s, t, vm, msL, R.cL, lam, sigl, accf, v);
                     }, row_cache<T>(B.sh));
+  if constexpr (MODE == LAM_FAST) {
+    // The dominant entry of p (sidx) carries the largest rounding of the
+    // plain w - p~ (~6e-8 of its p~, a p~ near 1 on a peaked row): its owner
+    // replaces that term with the exact value, p~ expm1(lam x) in double, for
+    // the same float a and X.
+    // Its own a is the shift's rounding (|a| ~ 1e-6), so 2^a is the
+    // quadratic below to rounding; only where |lam x| < 1/16 is the plain
+    // term's rounding large next to the term itself (expm1 by its series).
+    const int sidx = R.sidx;
+    if (sidx < V && B.tid == entry_owner<NT>(sidx)) {
+      const float s = R.ms, t = R.t_sidx;
+      const float a = fmaf(s, LOG2E, -msL);
+      const float X = fmaf(t - s, LOG2E, -R.cL);
+      const double y = static_cast<double>(lam) * static_cast<double>(X) * LN2_D;
+      if (fabs(y) < 0.0625) {
+        const float uf = fexp2(fmaf(lam, X, a)) - fexp2(a);
+        const double al = static_cast<double>(a) * LN2_D;
+        const double pt = 1.0 + al * (1.0 + 0.5 * al);
+        const double em = y * (1.0 + y * (0.5 + y * (1.0 / 6 + y * (1.0 / 24 + y * (1.0 / 120 + y * (1.0 / 720 +
+                          y * (1.0 / 5040)))))));
+        v[0] += pt * em - static_cast<double>(uf);
+      }
+    }
+  }
   B.sum(v);
   const double corr = shift_correction(R.ms, msL);
 #pragma unroll
   for (int j = 0; j < 5; ++j) v[j] *= corr;
-  return lam_finish(v, R.sum_s, lam, sigl);
+  return lam_finish(v, R.sum_s, lam, sigl, accf);
 }
 
 // Evaluates A and its derivatives at lam over the whole row; acc selects the
-// expm1 form.  Every thread gets the same result.
+// expm1 form.  Where lam x can exceed 60 (natural units) for some entry, the
+// exponents are shifted by sigl so that lam x - sig <= 60 for every entry.
+// Every thread gets the same result.
 template <typename T, int NT, typename SH>
 __device__ LamEval lam_sweep(Block<NT, SH>& B, const T* srow, const T* trow, int V, const RowStats& R,
                              float lam, bool acc) {
   const double top = static_cast<double>(lam) * (static_cast<double>(R.dmax) - R.c);  // largest lam x
-  if (acc) return lam_sweep_mode<T, NT, LAM_ACC>(B, srow, trow, V, R, lam, 0.0f);
-  if (top <= 60.0) return lam_sweep_mode<T, NT, LAM_FAST>(B, srow, trow, V, R, lam, 0.0f);
-  // keep lam x - sig <= 60 (natural units) for every entry
-  const float sigl = static_cast<float>((top - 60.0) * static_cast<double>(LOG2E));
-  return lam_sweep_mode<T, NT, LAM_GEN>(B, srow, trow, V, R, lam, sigl);
+  const float sigl = top <= 60.0 ? 0.0f : static_cast<float>((top - 60.0) * static_cast<double>(LOG2E));
+  if (sigl != 0.0f) return lam_sweep_mode<T, NT, LAM_SHIFT>(B, srow, trow, V, R, lam, sigl, acc);
+  if (acc) return lam_sweep_mode<T, NT, LAM_ACC>(B, srow, trow, V, R, lam, 0.0f, true);
+  return lam_sweep_mode<T, NT, LAM_FAST>(B, srow, trow, V, R, lam, 0.0f, false);
 }
 
 // Rows whose KL (the radius, or KL(pi||p) at the teacher endpoint) is below
@@ -740,6 +829,17 @@ constexpr double KL_ACCURATE = 0.01;
 // ~6e-8 absolute error per entry, which summed over the positive residual is
 // ~1e-5 of a TV near 0.01 (TV <= sqrt(KL / 2)).
 constexpr double TV_ACCURATE = 0.1;
+// In the plain forms each w - p~ (and q/p - 1) carries ~4e-8 of its p as
+// rounding, so A carries ~4e-8 |p'|_2 (random over the entries) and TV as
+// much.  The lambda sweep takes the dominant entry's term exactly, so p' is p
+// without it (|p'|_2 <= sqrt(min(max p, 1 - max p) (1 - max p))); peaked rows
+// (max p above P_PEAKED) take the final sweep in the expm1 form, where the
+// dominant entry's q/p - 1 is exact to rounding.
+constexpr double P_PEAKED = 0.25;
+// A row resolved in a plain form whose TV is below TV_PLAIN_MIN times that
+// bound of |p'|_2 (A's error then above ~2e-6 of TV) is resolved again in the
+// expm1 forms.
+constexpr double TV_PLAIN_MIN = 0.02;
 
 // Result of the lambda search.
 struct LamResult {
@@ -749,6 +849,7 @@ struct LamResult {
   float c;     // centring constant used by A (may differ from RowStats::c)
   float cL;    // c log2(e) as used in X = fma(d, log2 e, -cL)
   bool qp;     // q = p exactly (eps = 0, or t - s constant): the sweeps use lambda 0
+  bool acc;    // A and KL come from a sweep in the expm1 form
   // x of one entry exactly as the sweeps see it: X ln 2, X = fma(d, log2 e, -cL)
   __device__ double x_of(float s, float t) const {
     return (static_cast<double>(LOG2E) * (static_cast<double>(t) - static_cast<double>(s)) -
@@ -840,9 +941,13 @@ __device__ inline double two_ended_start(const RowStats& R, double eps) {
 // (the next term is smaller by about |l - node| times the cumulant growth);
 // otherwise the next node is that root (or the edge of the trust interval).
 // sweep1(lam, acc) evaluates one node over the whole row.
+// force_acc: every sweep in the expm1 form; lam_hint > 0: the first node (a
+// lambda* found before, resolved again in the accurate form).
 template <typename Sweep1>
-__device__ LamResult lambda_search_with(const RowStats& R, double eps, Sweep1&& sweep1) {
+__device__ LamResult lambda_search_with(const RowStats& R, double eps, Sweep1&& sweep1, bool force_acc = false,
+                                        float lam_hint = 0.0f) {
   LamResult out;
+  out.acc = true;
   if (R.dmin == R.dmax) {
     // t - s constant: p = pi, KL = 0 for every lambda, lambda* = 1, q = p
     out.lam = 1.0f; out.A = 0.0; out.KL = 0.0; out.c = R.dmin; out.cL = R.dmin * LOG2E; out.qp = true;
@@ -857,9 +962,9 @@ __device__ LamResult lambda_search_with(const RowStats& R, double eps, Sweep1&& 
   }
   // A KL below KL_ACCURATE is resolved with the expm1 form of the sweep: the
   // plain form carries ~2^-24 absolute error per weight, too much next to a
-  // KL of that size.  Its overflow guard needs lam (dmax - c) <= 60.
-  const bool acc_ok = (static_cast<double>(R.dmax) - R.c) <= 60.0;
-  bool acc = eps < KL_ACCURATE && acc_ok;
+  // KL of that size.
+  bool acc = force_acc || eps < KL_ACCURATE;
+  out.acc = acc;
   constexpr double TAYLOR_TOL = 1e-7;
   constexpr double TRUST = 0.3;
   constexpr double LMAX = 1.0 - 1e-6;
@@ -871,12 +976,25 @@ __device__ LamResult lambda_search_with(const RowStats& R, double eps, Sweep1&& 
   double lg = (l_two > 0.0 && fabs(l_two - l_cum) <= 0.3 * l_cum) ? l_two : l_cum;
   lg = fmin(fmax(lg, 1e-7), LMAX);
   bool try_one = R.kl1_est <= 1.05 * eps + 1e-5;
-  for (int sweep = 0; sweep < 12; ++sweep) {
+  if (lam_hint > 0.0f) {
+    lg = lam_hint;
+    try_one = lam_hint == 1.0f;
+  }
+  // The first TRUST_SWEEPS sweeps step within TRUST of the node.  A row still
+  // unresolved after them (a KL that rises steeply, e.g. a few entries with
+  // tiny p and a large d) continues with safeguarded steps: the model's root
+  // inside the bracket when it at least halves the step of two sweeps
+  // before, the bracket's midpoint otherwise.
+  constexpr int TRUST_SWEEPS = 4;
+  constexpr int MAX_SWEEPS = 64;
+  double step1 = 2.0, step2 = 2.0;  // the last two node steps (safeguard)
+  for (int sweep = 0; sweep < MAX_SWEEPS; ++sweep) {
     const float lf = try_one ? 1.0f : static_cast<float>(lg);
     const LamEval E = sweep1(lf, acc);
     if (lf == 1.0f && E.KL <= eps) {
-      if (!acc && acc_ok && E.KL < KL_ACCURATE) {
+      if (!acc && E.KL < KL_ACCURATE) {
         acc = true;  // resolve a small endpoint KL with the accurate form
+        out.acc = true;
         continue;
       }
       out.lam = 1.0f; out.A = E.A; out.KL = E.KL;
@@ -888,13 +1006,20 @@ __device__ LamResult lambda_search_with(const RowStats& R, double eps, Sweep1&& 
     } else {
       hi = fmin(hi, E.lam);
     }
+    const bool trust = sweep < TRUST_SWEEPS;
+    if (!trust) {
+      // a feasible node at the radius, or a bracket at float resolution
+      if (E.KL <= eps && eps - E.KL <= TAYLOR_TOL * eps) break;
+      if (hi - lo <= 1e-7 * hi) break;
+    }
     TaylorA M;
     M.n = E;
     if (!M.usable()) {
       lg = 0.5 * (lo + hi);
       continue;
     }
-    const double a = fmax(lo, E.lam * (1.0 - TRUST)), b = fmin(hi, E.lam * (1.0 + TRUST));
+    const double a = trust ? fmax(lo, E.lam * (1.0 - TRUST)) : lo;
+    const double b = trust ? fmin(hi, E.lam * (1.0 + TRUST)) : hi;
     const double fa = M.kl(a) - eps, fb = M.kl(b) - eps;
     if (fa <= 0.0 && fb > 0.0) {
       // safeguarded Newton on the model inside [a, b]
@@ -924,23 +1049,31 @@ __device__ LamResult lambda_search_with(const RowStats& R, double eps, Sweep1&& 
         out.KL = fmax(static_cast<double>(lr) * Ap - A, 0.0);
         return out;
       }
-      lg = fmin(fmax(l, 1e-7), LMAX);
-      continue;
-    }
-    // the model's root is outside the trust interval: go to its edge
-    if (fb <= 0.0) {
-      if (b >= 1.0 || E.lam * (1.0 + TRUST) >= 1.0) {
-        try_one = hi >= 1.0;  // the teacher endpoint may be feasible
-        lg = fmin(0.5 * (E.lam + hi), LMAX);
+      lg = l;
+    } else if (trust) {
+      // the model's root is outside the trust interval: go to its edge
+      if (fb <= 0.0) {
+        if (b >= 1.0 || E.lam * (1.0 + TRUST) >= 1.0) {
+          try_one = hi >= 1.0;  // the teacher endpoint may be feasible
+          lg = fmin(0.5 * (E.lam + hi), LMAX);
+        } else {
+          lg = b;
+        }
       } else {
-        lg = b;
+        lg = a;
       }
     } else {
-      lg = a;
+      lg = 0.5 * (lo + hi);
+    }
+    if (!trust) {
+      const double st = fabs(lg - E.lam);
+      if (!(lg > lo && lg < hi) || st > 0.5 * step2) lg = 0.5 * (lo + hi);
+      step2 = step1;
+      step1 = fabs(lg - E.lam);
     }
     lg = fmin(fmax(lg, 1e-7), LMAX);
   }
-  // not reached in practice (the bracket shrinks every sweep): keep the
+  // the bracket has closed on the root (or the sweeps ran out): keep the
   // largest feasible evaluated lambda
   out.lam = static_cast<float>(feas.lam); out.A = feas.A; out.KL = feas.KL;
   return out;
@@ -948,10 +1081,20 @@ __device__ LamResult lambda_search_with(const RowStats& R, double eps, Sweep1&& 
 
 template <typename T, int NT, typename SH>
 __device__ LamResult lambda_search(Block<NT, SH>& B, const T* srow, const T* trow, int V,
-                                   const RowStats& R, double eps) {
+                                   const RowStats& R, double eps, bool force_acc = false, float lam_hint = 0.0f) {
   return lambda_search_with(R, eps, [&](float lam, bool acc) {
     return lam_sweep<T, NT>(B, srow, trow, V, R, lam, acc);
-  });
+  }, force_acc, lam_hint);
+}
+
+// A row resolved in a plain form whose TV is too small for that form's
+// rounding (TV_PLAIN_MIN) is resolved again in the expm1 forms.
+__device__ inline bool redo_accurate(const RowStats& R, const LamResult& L, bool final_acc, double TV) {
+  if (L.qp || (L.acc && final_acc)) return false;
+  const double rest = 1.0 - R.pmax;
+  const double lam_err = L.acc ? 0.0 : sqrt(fmax(fmin(R.pmax, rest) * rest, 0.0));
+  const double fin_err = final_acc ? 0.0 : sqrt(R.pmax);
+  return TV < TV_PLAIN_MIN * fmax(lam_err, fin_err);
 }
 
 // ---------------------------------------------------------------------------
@@ -962,9 +1105,16 @@ __device__ LamResult lambda_search(Block<NT, SH>& B, const T* srow, const T* tro
 struct FinalConst {
   float msL, invS, cL, lam, AL;  // msL = ms log2(e); AL = A* log2(e)
   bool acc;                      // expm1 form (rows whose KL is small)
+  bool wide;                     // q/p can exceed 2^60 for some entry
 };
 
-__device__ inline FinalConst final_const(const RowStats& R, const LamResult& L) {
+// Forms of the final sweep's weights: FIN_FAST 2^y - 1, FIN_ACC its expm1
+// form; FIN_WIDE (rows where q/p can overflow float) takes [q - p]_+ with
+// q = 2^(a + y) / sum p~ for the entries with q/p > 2^64 (q <= 1 there while
+// q/p would overflow), the FIN_FAST / FIN_ACC form (by F.acc) elsewhere.
+enum FinMode { FIN_FAST = 0, FIN_ACC = 1, FIN_WIDE = 2 };
+
+__device__ inline FinalConst final_const(const RowStats& R, const LamResult& L, bool force_acc = false) {
   FinalConst F;
   F.msL = R.ms * LOG2E;
   // p = 2^{fma(s, log2 e, -msL)} * invS: the shift's rounding is folded into invS
@@ -972,32 +1122,41 @@ __device__ inline FinalConst final_const(const RowStats& R, const LamResult& L) 
   F.cL = L.cL;
   F.lam = L.qp ? 0.0f : L.lam;
   F.AL = L.qp ? 0.0f : static_cast<float>(L.A * static_cast<double>(LOG2E));
-  F.acc = L.KL < TV_ACCURATE;
+  F.acc = force_acc || L.KL < TV_ACCURATE || R.pmax > P_PEAKED;
+  // largest log q/p over the row: lam* (dmax - c) - A*
+  const double top = static_cast<double>(F.lam) * (static_cast<double>(R.dmax) - L.c) - (L.qp ? 0.0 : L.A);
+  F.wide = top * static_cast<double>(LOG2E) > 60.0;
   return F;
 }
 
 // Residual weight [q_v - p_v]_+ and p_v of one entry; the residual race uses
 // the same function, so its weights are bit-identical to the chunk masses'.
-template <bool ACC>
+template <int MODE>
 __device__ __forceinline__ float res_weight(float s, float t, const FinalConst& F, float* p_out) {
-  const float p = fexp2(fmaf(s, LOG2E, -F.msL)) * F.invS;
+  const float a = fmaf(s, LOG2E, -F.msL);
+  const float p = fexp2(a) * F.invS;
   const float X = fmaf(t - s, LOG2E, -F.cL);
   const float y2 = fmaf(F.lam, X, -F.AL);  // log2 of q/p
-  const float ee = fexp2(y2);
   *p_out = p;
-  const float em1 = ACC ? expm1_sel(y2 * LN2, ee) : (ee - 1.0f);
-  return p * fmaxf(em1, 0.0f);
+  if constexpr (MODE == FIN_WIDE) {
+    const float ee = fexp2(fminf(y2, 64.0f));
+    const float em1 = F.acc ? expm1_sel(y2 * LN2, ee) : (ee - 1.0f);
+    const float q = fexp2(a + y2) * F.invS;
+    const float w = (y2 > 64.0f) ? q - p : p * em1;
+    return fmaxf(w, 0.0f);
+  } else {
+    const float ee = fexp2(y2);
+    const float em1 = (MODE == FIN_ACC) ? expm1_sel(y2 * LN2, ee) : (ee - 1.0f);
+    return p * fmaxf(em1, 0.0f);
+  }
 }
 
-// Thread of a workgroup of NT threads that holds entry v in the chunk sweeps
-// (wave c % NW of chunk c = v / CHUNK, lane and slot by elem_offset).
-template <int NT>
-__device__ __forceinline__ int entry_owner(int v) {
-  constexpr int NW = NT / WAVE;
-  const int o = v % CHUNK;
-  const int lane = (o < 512) ? (o >> 3) : ((o - 512) >> 3);
-  return ((v / CHUNK) % NW) * WAVE + lane;
+// res_weight in the form F selects.
+__device__ __forceinline__ float res_weight_any(float s, float t, const FinalConst& F, float* p_out) {
+  if (F.wide) return res_weight<FIN_WIDE>(s, t, F, p_out);
+  return F.acc ? res_weight<FIN_ACC>(s, t, F, p_out) : res_weight<FIN_FAST>(s, t, F, p_out);
 }
+
 
 // F is taken by value: the loop then holds its fields in registers, with no
 // reloads through a pointer that the gradient stores might alias.  The
@@ -1006,7 +1165,7 @@ __device__ __forceinline__ int entry_owner(int v) {
 // stored coef * p_hot overwrites it with coef * (p_hot - 1), p_hot computed by
 // the same expression (same thread, same address, so the later store is the
 // one that stays).
-template <typename T, typename G, int NT, bool GRAD, bool ACC, typename SH>
+template <typename T, typename G, int NT, bool GRAD, int MODE, typename SH>
 __device__ __forceinline__ double final_sweep(Block<NT, SH>& B, const T* srow, const T* trow, G* grow, int V,
                               const FinalConst F, bool keep_res, float coef, int hot, float s_hot) {
   constexpr int NW = NT / WAVE;
@@ -1018,7 +1177,7 @@ __device__ __forceinline__ double final_sweep(Block<NT, SH>& B, const T* srow, c
 #pragma unroll
                       for (int e = 0; e < EPL; ++e) {
                         float p;
-                        const float w = res_weight<ACC>(s[e], t[e], F, &p);
+                        const float w = res_weight<MODE>(s[e], t[e], F, &p);
                         if (SAKI_VALID(e)) tv += w;
                         if (GRAD) g[e] = coef * p;
                       }
@@ -1036,6 +1195,34 @@ __device__ __forceinline__ double final_sweep(Block<NT, SH>& B, const T* srow, c
   double v[1] = {TV};
   B.sum(v);
   return v[0];
+}
+
+// A gradient row of one value (rows without a usable coupling: NaN at a valid
+// row with non-finite logits, exact zeros at a masked row whatever its
+// logits); the logits are not read.
+template <typename G, int NT>
+__device__ void fill_row(int wave, int lane, G* grow, int V, float value) {
+  constexpr int NW = NT / WAVE;
+  const int nchunks = (V + CHUNK - 1) / CHUNK;
+  const bool ragged = (V % CHUNK) != 0;
+  float g[EPL];
+#pragma unroll
+  for (int e = 0; e < EPL; ++e) g[e] = value;
+  for (int c = wave; c < nchunks; c += NW) {
+    if (ragged && c == nchunks - 1)
+      store_lane<G, true>(grow, c, lane, V, g);
+    else
+      store_lane<G, false>(grow, c, lane, V, g);
+  }
+}
+
+// The final sweep in the form F selects.
+template <typename T, typename G, int NT, bool GRAD, typename SH>
+__device__ double final_sweep_any(Block<NT, SH>& B, const T* srow, const T* trow, G* grow, int V,
+                                  const FinalConst& F, bool keep_res, float coef, int hot, float s_hot) {
+  if (F.wide) return final_sweep<T, G, NT, GRAD, FIN_WIDE>(B, srow, trow, grow, V, F, keep_res, coef, hot, s_hot);
+  if (F.acc) return final_sweep<T, G, NT, GRAD, FIN_ACC>(B, srow, trow, grow, V, F, keep_res, coef, hot, s_hot);
+  return final_sweep<T, G, NT, GRAD, FIN_FAST>(B, srow, trow, grow, V, F, keep_res, coef, hot, s_hot);
 }
 
 // Standalone routed loss, first sweep: the log-sum-exp of one array, with the
@@ -1064,16 +1251,11 @@ __device__ double lse_sweep(Block<NT, SH>& B, const T* srow, int V, float* msL_o
       MsL = cmsL;
     }
     double ps = 0.0;
-    float gs = 0.f;
 #pragma unroll
     for (int e = 0; e < EPL; ++e) {
       float es = fexp2(fmaf(s[e], LOG2E, -MsL));
       if (TAIL && !SAKI_VALID(e)) es = 0.f;
-      gs += es;
-      if ((e & 3) == 3) {
-        ps += static_cast<double>(gs);
-        gs = 0.f;
-      }
+      ps += static_cast<double>(es);
     }
     Ss += ps;
   }, row_cache<T>(B.sh));
@@ -1082,16 +1264,28 @@ __device__ double lse_sweep(Block<NT, SH>& B, const T* srow, int V, float* msL_o
   double v[1] = {(Ms == -finf()) ? 0.0 : (Ms == ms) ? Ss : Ss * static_cast<double>(fexp2(__fsub_rn(MsL, msL)))};
   B.sum(v);
   *msL_out = msL;
+  // the maximum's own term exactly: 2^d0 (d0 = ms log2 e - msL, exact in
+  // double) instead of its float rounding (see stats_combine_block)
+  if (isfinite(ms)) {
+    const double d0 = static_cast<double>(LOG2E) * static_cast<double>(ms) - static_cast<double>(msL);
+    v[0] += exp2(d0) - static_cast<double>(fexp2(fmaf(ms, LOG2E, -msL)));
+  }
   return v[0];
 }
 
 // Standalone routed loss, second sweep: grad_v = coef * p_v with the
 // indicator entry (hot, logit s_hot) rewritten after the loop by the thread
-// that stored it, as in the final sweep; a row flagged nan_row is all NaN.
+// that stored it, as in the final sweep; a row flagged nan_row is all NaN and
+// a row with coef = 0 all zeros.
 template <typename T, typename G, int NT, typename SH>
 __device__ void route_grad_sweep(Block<NT, SH>& B, const T* srow, G* grow, int V, float msL, float invS,
                                  float coef, int hot, float s_hot, bool nan_row) {
   constexpr int NW = NT / WAVE;
+  if (!nan_row && coef == 0.0f) {
+    // a masked row (or a zero weight): exact zeros whatever the logits
+    fill_row<G, NT>(B.wave, B.lane, grow, V, 0.0f);
+    return;
+  }
   const float cf = nan_row ? __builtin_nanf("") : coef;
   for_chunks1<T, NW, use_mode<T, SH>()>(srow, V, B.wave, B.lane, [&](auto tail, const float* s, uint32_t vm, int c) {
     constexpr bool TAIL = decltype(tail)::value;
@@ -1107,39 +1301,6 @@ __device__ void route_grad_sweep(Block<NT, SH>& B, const T* srow, G* grow, int V
 }
 
 #undef SAKI_VALID
-
-// Gradient-only sweep for rows that carry no coupling (non-finite rows, or
-// the standalone routed loss): grad_v = coef * (p_v - 1[v = hot]).
-template <typename T, typename G, int NT, bool TAIL>
-__device__ __forceinline__ void grad_chunk(const T* srow, G* grow, int V, int c, int lane, float ms,
-                                           float invS, float coef, int hot, bool nan_row) {
-  float s[EPL];
-  uint32_t vm;
-  load_lane<T, TAIL>(srow, c, lane, V, s, &vm);
-  float g[EPL];
-  const int base = c * CHUNK;
-#pragma unroll
-  for (int e = 0; e < EPL; ++e) {
-    const float p = fexp2((s[e] - ms) * LOG2E) * invS;
-    g[e] = nan_row ? __builtin_nanf("") : coef * (p - ((base + elem_offset(lane, e) == hot) ? 1.0f : 0.0f));
-  }
-  store_lane<G, TAIL>(grow, c, lane, V, g);
-}
-
-template <typename T, typename G, int NT, typename SH>
-__device__ void grad_sweep(Block<NT, SH>& B, const T* srow, G* grow, int V, float ms, double sum_s,
-                           float coef, int hot, bool nan_row) {
-  constexpr int NW = NT / WAVE;
-  const int nchunks = (V + CHUNK - 1) / CHUNK;
-  const bool ragged = (V % CHUNK) != 0;
-  const float invS = static_cast<float>(1.0 / sum_s);
-  for (int c = B.wave; c < nchunks; c += NW) {
-    if (ragged && c == nchunks - 1)
-      grad_chunk<T, G, NT, true>(srow, grow, V, c, B.lane, ms, invS, coef, hot, nan_row);
-    else
-      grad_chunk<T, G, NT, false>(srow, grow, V, c, B.lane, ms, invS, coef, hot, nan_row);
-  }
-}
 
 // ---------------------------------------------------------------------------
 // Two-level exponential races (the sampler this library fixes for z ~ p and
@@ -1203,44 +1364,74 @@ __device__ int elem_race(Block<NT, SH>& B, int c, int V, uint64_t seed, uint32_t
 // elem_pick then runs the race of elem_race on them (same uniforms, keys and
 // ties) and returns the winner with its s and t, so no later load is needed.
 // logw(s, t, v) returns ln w_v up to a row constant, or -inf.
-struct ElemFetch {
-  float s[4], t[4];
+// The entries are held as loaded (packed bf16 words, or floats) and unpacked
+// when raced, so that a fetch kept across the lambda search holds few registers.
+template <typename T>
+struct ElemFetch;
+template <>
+struct ElemFetch<uint16_t> {
+  uint2 qs, qt;
   int v0;  // first of this thread's entries
+  __device__ float s(int k) const {
+    const uint32_t w = (k < 2) ? qs.x : qs.y;
+    return __uint_as_float((k & 1) ? (w & 0xffff0000u) : (w << 16));
+  }
+  __device__ float t(int k) const {
+    const uint32_t w = (k < 2) ? qt.x : qt.y;
+    return __uint_as_float((k & 1) ? (w & 0xffff0000u) : (w << 16));
+  }
+};
+template <>
+struct ElemFetch<float> {
+  float4 qs, qt;
+  int v0;
+  __device__ float s(int k) const { return k == 0 ? qs.x : k == 1 ? qs.y : k == 2 ? qs.z : qs.w; }
+  __device__ float t(int k) const { return k == 0 ? qt.x : k == 1 ? qt.y : k == 2 ? qt.z : qt.w; }
 };
 
 template <typename T, int NT>
-__device__ __forceinline__ ElemFetch elem_fetch(const T* srow, const T* trow, int c, int V, int tid) {
+__device__ __forceinline__ ElemFetch<T> elem_fetch(const T* srow, const T* trow, int c, int V, int tid) {
   static_assert(4 * NT >= CHUNK, "four entries per thread cover a chunk");
-  ElemFetch f;
+  ElemFetch<T> f;
   const int hi = min(V, c * CHUNK + CHUNK);
   f.v0 = c * CHUNK + 4 * tid;
   if (f.v0 + 4 <= hi) {
     if constexpr (sizeof(T) == 2) {
-      const uint2 qs = *reinterpret_cast<const uint2*>(srow + f.v0);
-      const uint2 qt = *reinterpret_cast<const uint2*>(trow + f.v0);
-      f.s[0] = __uint_as_float(qs.x << 16); f.s[1] = __uint_as_float(qs.x & 0xffff0000u);
-      f.s[2] = __uint_as_float(qs.y << 16); f.s[3] = __uint_as_float(qs.y & 0xffff0000u);
-      f.t[0] = __uint_as_float(qt.x << 16); f.t[1] = __uint_as_float(qt.x & 0xffff0000u);
-      f.t[2] = __uint_as_float(qt.y << 16); f.t[3] = __uint_as_float(qt.y & 0xffff0000u);
+      f.qs = *reinterpret_cast<const uint2*>(srow + f.v0);
+      f.qt = *reinterpret_cast<const uint2*>(trow + f.v0);
     } else {
-      const float4 qs = *reinterpret_cast<const float4*>(srow + f.v0);
-      const float4 qt = *reinterpret_cast<const float4*>(trow + f.v0);
-      f.s[0] = qs.x; f.s[1] = qs.y; f.s[2] = qs.z; f.s[3] = qs.w;
-      f.t[0] = qt.x; f.t[1] = qt.y; f.t[2] = qt.z; f.t[3] = qt.w;
+      f.qs = *reinterpret_cast<const float4*>(srow + f.v0);
+      f.qt = *reinterpret_cast<const float4*>(trow + f.v0);
     }
   } else {
+    // the ragged end of the row: entries past it read as 0 (and are not raced)
+    if constexpr (sizeof(T) == 2) {
+      uint32_t ws[4], wt[4];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const bool in = f.v0 + k < hi;
-      f.s[k] = in ? Loader<T>::load1(srow + f.v0 + k) : 0.0f;
-      f.t[k] = in ? Loader<T>::load1(trow + f.v0 + k) : 0.0f;
+      for (int k = 0; k < 4; ++k) {
+        const bool in = f.v0 + k < hi;
+        ws[k] = in ? static_cast<uint32_t>(srow[f.v0 + k]) : 0u;
+        wt[k] = in ? static_cast<uint32_t>(trow[f.v0 + k]) : 0u;
+      }
+      f.qs = make_uint2(ws[0] | (ws[1] << 16), ws[2] | (ws[3] << 16));
+      f.qt = make_uint2(wt[0] | (wt[1] << 16), wt[2] | (wt[3] << 16));
+    } else {
+      float xs[4], xt[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const bool in = f.v0 + k < hi;
+        xs[k] = in ? srow[f.v0 + k] : 0.0f;
+        xt[k] = in ? trow[f.v0 + k] : 0.0f;
+      }
+      f.qs = make_float4(xs[0], xs[1], xs[2], xs[3]);
+      f.qt = make_float4(xt[0], xt[1], xt[2], xt[3]);
     }
   }
   return f;
 }
 
-template <int NT, typename SH, typename F>
-__device__ int elem_pick(Block<NT, SH>& B, const ElemFetch& f, int c, int V, uint64_t seed, uint32_t stream,
+template <int NT, typename SH, typename T, typename F>
+__device__ int elem_pick(Block<NT, SH>& B, const ElemFetch<T>& f, int c, int V, uint64_t seed, uint32_t stream,
                          uint64_t g, F logw, float* s_win, float* t_win) {
   float best = finf(), bs = 0.0f, bt = 0.0f;
   int bi = 0x7fffffff;
@@ -1252,12 +1443,13 @@ __device__ int elem_pick(Block<NT, SH>& B, const ElemFetch& f, int c, int V, uin
     for (int k = 0; k < 4; ++k) {
       const int v = f.v0 + k;
       if (v < hi) {
-        const float lw = logw(f.s[k], f.t[k], v);
+        const float sk = f.s(k), tk = f.t(k);
+        const float lw = logw(sk, tk, v);
         if (lw > -finf()) {
           const float u = word_to_uniform(words[k]);
           const float E = -flog2(u) * LN2;
           const float key = flog2(E) * LN2 - lw;
-          if (key < best) { best = key; bi = v; bs = f.s[k]; bt = f.t[k]; }
+          if (key < best) { best = key; bi = v; bs = sk; bt = tk; }
         }
       }
     }

@@ -93,9 +93,14 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
     const float M = (ROUTE && P.valid) ? (P.valid[r] ? 1.0f : 0.0f) : 1.0f;
 
     const bool sample_target = ROUTE && P.target_mode == SAKI_TARGET_SAMPLE;
-    const RowStats R = stats_sweep<T, NT>(B, srow, trow, V, true, sample_target);
+    // A row resolved in a plain form whose TV turns out too small for that
+    // form's rounding is processed again from the start with every sweep in
+    // the expm1 form (rare); nothing but the pass number crosses the restart.
+    for (int pass = 0; pass < 2; ++pass) {
+    const bool force_acc = pass > 0;
+    const RowStats& R = stats_sweep<T, NT>(B, srow, trow, V, true, sample_target);
     if (!R.finite) {
-      if (GRAD) grad_sweep<T, G, NT>(B, srow, grow, V, 0.0f, 1.0, 0.0f, -1, M != 0.0f);
+      if (GRAD) fill_row<G, NT>(B.wave, B.lane, grow, V, M != 0.0f ? nanf_() : 0.0f);
       if (B.tid == 0) {
         const saki_couple_out& o = P.out;
         if (o.lambda) o.lambda[r] = nanf_();
@@ -118,7 +123,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
           if (P.scaled_loss) P.scaled_loss[r] = static_cast<double>(l);
         }
       }
-      continue;
+      break;
     }
 
     // z ~ p by the two-level race (chunk masses from the stats sweep): the
@@ -129,10 +134,10 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
       return static_cast<double>(sh.chunk_a[c]) * LN2_D + log(static_cast<double>(sh.chunk_b[c]));
     });
     const int cz = c0 < nch ? c0 : 0;
-    const ElemFetch fz = elem_fetch<T, NT>(srow, trow, cz, V, B.tid);
+    const ElemFetch<T> fz = elem_fetch<T, NT>(srow, trow, cz, V, B.tid);
     const float s_vstar = Loader<T>::load1(srow + R.vstar);
 
-    const LamResult L = lambda_search<T, NT>(B, srow, trow, V, R, P.eps);
+    const LamResult L = lambda_search<T, NT>(B, srow, trow, V, R, P.eps, force_acc);
 
     float sz, tz;
     int z = elem_pick<NT>(B, fz, cz, V, P.seed, PROP_ELEM, g,
@@ -162,7 +167,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
         return static_cast<double>(sh.chunk_c[c]) * LN2_D + log(static_cast<double>(sh.chunk_d[c]));
       });
       const int cc = ct < nch ? ct : 0;
-      const ElemFetch ft = elem_fetch<T, NT>(srow, trow, cc, V, B.tid);
+      const ElemFetch<T> ft = elem_fetch<T, NT>(srow, trow, cc, V, B.tid);
       float sv, tv;
       const int vt = elem_pick<NT>(B, ft, cc, V, P.seed, TS_ELEM, g,
                                    [&](float, float tl, int) { return tl; }, &sv, &tv);
@@ -172,9 +177,9 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
       }
     }
 
-    const FinalConst F = final_const(R, L);
-    const double TV = F.acc ? final_sweep<T, G, NT, GRAD, true>(B, srow, trow, grow, V, F, C, coef, hot, s_hot)
-                            : final_sweep<T, G, NT, GRAD, false>(B, srow, trow, grow, V, F, C, coef, hot, s_hot);
+    const FinalConst F = final_const(R, L, force_acc);
+    const double TV = final_sweep_any<T, G, NT, GRAD>(B, srow, trow, grow, V, F, C, coef, hot, s_hot);
+    if (!force_acc && redo_accurate(R, L, F.acc, TV)) continue;
 
     int y = z;
     float sy = sz, ty = tz;
@@ -186,11 +191,11 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
       // a residual that rounds to zero everywhere in float (lambda* x within
       // rounding of A*) leaves no chunk with mass; the proposal is kept then
       if (c1 < nch) {
-        const ElemFetch fr = elem_fetch<T, NT>(srow, trow, c1, V, B.tid);
+        const ElemFetch<T> fr = elem_fetch<T, NT>(srow, trow, c1, V, B.tid);
         float sw, tw;
         const int yc = elem_pick<NT>(B, fr, c1, V, P.seed, RES_ELEM, g, [&](float sv, float tv, int) {
           float p;
-          const float w = F.acc ? res_weight<true>(sv, tv, F, &p) : res_weight<false>(sv, tv, F, &p);
+          const float w = res_weight_any(sv, tv, F, &p);
           return w > 0.0f ? flog2(w) * LN2 : -finf();
         }, &sw, &tw);
         if (yc < V) {
@@ -234,6 +239,8 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
         if (P.scaled_loss) P.scaled_loss[r] = static_cast<double>(P.grad_scale) * l;
       }
     }
+    break;
+    }  // pass
   }
 }
 
@@ -308,6 +315,10 @@ __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyP
     int n = P.k;
     int corr = -1;
     int next_unwritten = P.k;  // first position whose per-position outputs are not yet written
+    // a position resolved in a plain form whose TV turns out too small for
+    // that form's rounding is processed again with every sweep in the expm1
+    // form (rare): force_acc is all that crosses the restart
+    bool force_acc = false;
     for (int j = 0; j < P.k; ++j) {
       const int64_t r = b * P.k + j;
       const T* srow = static_cast<const T*>(P.s) + r * P.stride;
@@ -320,7 +331,7 @@ __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyP
         next_unwritten = j + 1;
         break;
       }
-      const RowStats R = stats_sweep<T, VNT>(B, srow, trow, V, false);
+      const RowStats& R = stats_sweep<T, VNT>(B, srow, trow, V, false);
       if (!R.finite) {
         if (P.has_pp && B.tid == 0) write_skipped(o, r, z, SAKI_ROW_NONFINITE);
         n = j;
@@ -354,14 +365,20 @@ __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyP
           continue;
         }
       }
-      const LamResult L = lambda_search<T, VNT>(B, srow, trow, V, R, P.eps);
+      const LamResult L = lambda_search<T, VNT>(B, srow, trow, V, R, P.eps, force_acc);
       const double alpha = exp(fmin(0.0, L.log_ratio(sz, tz)));
       const bool accept = u < alpha;
       double TV = __builtin_nan("");
-      const FinalConst F = final_const(R, L);
-      if (need_tv || !accept)
-        TV = F.acc ? final_sweep<T, float, VNT, false, true>(B, srow, trow, nullptr, V, F, !accept, 0.0f, -1, 0.0f)
-                   : final_sweep<T, float, VNT, false, false>(B, srow, trow, nullptr, V, F, !accept, 0.0f, -1, 0.0f);
+      const FinalConst F = final_const(R, L, force_acc);
+      if (need_tv || !accept) {
+        TV = final_sweep_any<T, float, VNT, false>(B, srow, trow, nullptr, V, F, !accept, 0.0f, -1, 0.0f);
+        if (!force_acc && redo_accurate(R, L, F.acc, TV)) {
+          force_acc = true;
+          --j;
+          continue;
+        }
+      }
+      force_acc = false;
       int y = z;
       float sy = sz, ty = tz;
       if (!accept) {
@@ -370,11 +387,11 @@ __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyP
           return m > 0.0f ? log(static_cast<double>(m)) : -__builtin_huge_val();
         });
         if (c1 < nch) {
-          const ElemFetch fr = elem_fetch<T, VNT>(srow, trow, c1, V, B.tid);
+          const ElemFetch<T> fr = elem_fetch<T, VNT>(srow, trow, c1, V, B.tid);
           float sw, tw;
           const int yc = elem_pick<VNT>(B, fr, c1, V, P.seed, RES_ELEM, g, [&](float sv, float tv, int) {
             float p;
-            const float w = F.acc ? res_weight<true>(sv, tv, F, &p) : res_weight<false>(sv, tv, F, &p);
+            const float w = res_weight_any(sv, tv, F, &p);
             return w > 0.0f ? flog2(w) * LN2 : -finf();
           }, &sw, &tw);
           if (yc < V) {
@@ -788,7 +805,27 @@ size_t saki_workspace_bytes(int op, int64_t n_rows, int64_t vocab) {
   }
 }
 
+}  // extern "C"
+
+namespace {
+
+saki_status couple_impl(const saki_rows* in, double eps, uint64_t seed, const saki_couple_out* out,
+                        const saki_route_args* route, void* ws, size_t ws_bytes, saki_stream_t stream);
+
+}  // namespace
+
+extern "C" {
+
 saki_status saki_couple(const saki_rows* in, double eps, uint64_t seed, const saki_couple_out* out,
+                        const saki_route_args* route, void* ws, size_t ws_bytes, saki_stream_t stream) {
+  return couple_impl(in, eps, seed, out, route, ws, ws_bytes, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+saki_status couple_impl(const saki_rows* in, double eps, uint64_t seed, const saki_couple_out* out,
                         const saki_route_args* route, void* ws, size_t ws_bytes, saki_stream_t stream) {
   saki_status st = check_rows(in);
   if (st != SAKI_OK) return st;
@@ -845,6 +882,10 @@ saki_status saki_couple(const saki_rows* in, double eps, uint64_t seed, const sa
   }
   return ok();
 }
+
+}  // namespace
+
+extern "C" {
 
 saki_status saki_route_loss(const void* student, int32_t dtype, int64_t n_rows, int64_t vocab,
                             int64_t row_stride, const int32_t* token, const uint8_t* corrected,

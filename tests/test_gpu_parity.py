@@ -24,7 +24,9 @@ def say(msg):
 
 
 def np_out(out):
-    return {k: v.cpu().numpy() for k, v in out.items() if isinstance(v, torch.Tensor)}
+    """Per-row outputs as numpy arrays (bf16 tensors widened to float32)."""
+    return {k: (v.float() if v.dtype == torch.bfloat16 else v).cpu().numpy()
+            for k, v in out.items() if isinstance(v, torch.Tensor)}
 
 
 def f64(x):
@@ -57,22 +59,20 @@ def test_tiny_all_rows(saki_lib):
 
 
 @pytest.mark.parametrize("eps", [0.05, 0.2])
-def test_mid_sampled_rows(saki_lib, eps):
+def test_mid_all_rows(saki_lib, eps):
+    """The mid configuration (4,096 rows, V = 32,000 bf16, with the gradient)
+    against the oracle on every row, the oracle spread over worker processes."""
     s, t = workloads.rows("mid", 0, 4096, device=DEV)
-    rng = np.random.default_rng(int(eps * 100))
-    rows = np.unique(np.concatenate([[0, 1, 4095], rng.choice(4096, 45, replace=False)]))
-    out, o, R = run_and_compare(saki_lib, s, t, eps, workloads.coupling_seed("mid"), rows=rows)
-    # properties on every row; rows that break one are compared with the oracle
-    bad = np.nonzero((o["row_status"] != 0) | (o["kl"] > eps * (1 + 1e-5) + 1e-9) |
-                     (o["tv"] > np.sqrt(o["kl"] / 2) * (1 + 1e-5) + 1e-7))[0]
-    if bad.size:
-        say(f"rows breaking a property: {bad[:10].tolist()} (of {bad.size})")
-        ii = torch.as_tensor(bad[:4], device=DEV)
-        R2 = parity.compare_couple(o, f64(s[ii]), f64(t[ii]), eps, workloads.coupling_seed("mid"), 0,
-                                   bad[:4])
-        say(R2.summary())
-        R2.check()
-    assert bad.size == 0
+    seed = workloads.coupling_seed("mid")
+    say(f"mid all rows eps={eps}")
+    out = saki_lib.couple(s, t, eps, seed, 0, route=True, grad_dtype=torch.float32, grad_scale=1.0)
+    torch.cuda.synchronize()
+    o = np_out(out)
+    _row_properties(o, eps)
+    rows = np.arange(4096)
+    R = parity.compare_couple_pool(o, f64(s), f64(t), eps, seed, 0, rows, grad=f64(out["grad"]))
+    say(f"mid eps={eps}: {R.summary()}")
+    R.check()
 
 
 def _row_properties(o, eps, grad=None):
@@ -92,23 +92,51 @@ def _row_properties(o, eps, grad=None):
     assert np.array_equal(o["token"][acc], o["proposal"][acc])
 
 
-def test_large_full_size_sampled(saki_lib):
+def _spread_rows(rng, n_seq, seq_len, per_seq):
+    """Rows spread over the sequences: each sequence's first and last position
+    and per_seq - 2 others at random."""
+    out = []
+    for q in range(n_seq):
+        lo = q * seq_len
+        mid = rng.choice(np.arange(lo + 1, lo + seq_len - 1), per_seq - 2, replace=False)
+        out.extend([lo, lo + seq_len - 1, *mid.tolist()])
+    return np.unique(np.asarray(out))
+
+
+def test_large_full_size(saki_lib):
+    """The large workload at full size (65,536 rows, V = 151,936 bf16, coupling +
+    routed loss + f32 gradient) in the benchmark's launch configuration, at each
+    radius of the sweep: 512 seeded rows spread over the 64 sequences (first and
+    last position of each, six others) plus every row whose decision margin is
+    below 1e-6 compared with the oracle element by element (events, tokens,
+    lambda, KL, TV, losses, gradient rows); the properties that hold at any
+    size checked on every row."""
     cfg = workloads.CONFIGS["large"]
     n, V = cfg["rows"], cfg["V"]
     say(f"generate large {n}x{V}")
     s = torch.empty(n, V, dtype=torch.bfloat16, device=DEV)
     t = torch.empty_like(s)
     workloads.fill("large", s, t)
-    eps = 0.2
-    rng = np.random.default_rng(3)
-    rows = np.unique(np.concatenate([[0, 1023, 1024, n - 1], rng.choice(n, 6, replace=False)]))
-    out, o, R = run_and_compare(saki_lib, s, t, eps, workloads.coupling_seed("large"), rows=rows)
-    _row_properties(o, eps)
-    g = out["grad"]
-    # every gradient row sums to zero (sum_j (p_j - 1[j = hot]) = 0)
-    sums = g[:4096].double().sum(dim=1).abs().max().item()
-    assert sums < 1e-3
-    del s, t, out, g
+    seed = workloads.coupling_seed("large")
+    rows0 = _spread_rows(np.random.default_rng(3), 64, 1024, 8)
+    assert rows0.size == 512
+    for eps in cfg["eps"]:
+        out = saki_lib.couple(s, t, eps, seed, 0, route=True, grad_dtype=torch.float32, grad_scale=1.0)
+        torch.cuda.synchronize()
+        o = np_out(out)
+        _row_properties(o, eps)
+        # every gradient row sums to zero (sum_j (p_j - 1[j = hot]) = 0)
+        assert out["grad"][:4096].double().sum(dim=1).abs().max().item() < 1e-3
+        near = np.nonzero(o["margin"] < parity.MARGIN)[0]
+        rows = np.unique(np.concatenate([rows0, near]))
+        ii = torch.as_tensor(rows, device=DEV)
+        say(f"large eps={eps}: oracle on {rows.size} rows ({near.size} with GPU margin < 1e-6)")
+        R = parity.compare_couple_pool(o, f64(s[ii]), f64(t[ii]), eps, seed, 0, rows, grad=f64(out["grad"][ii]))
+        say(f"large eps={eps}: {R.summary()}")
+        R.check()
+        del out
+        torch.cuda.empty_cache()
+    del s, t
     torch.cuda.empty_cache()
 
 
@@ -193,11 +221,13 @@ def test_verify_without_per_position_outputs(saki_lib):
     assert out["accepted_len"].cpu().tolist() == [2, 4] and out["correction"].cpu().tolist() == [-1, -1]
 
 
-def test_verify_full_size_sampled(saki_lib):
+def test_verify_full_size(saki_lib):
     """The verify workload at full size (8,192 blocks of k = 8, V = 151,936
     bf16) in the configuration the benchmark times (accepted lengths and
-    corrections only): sampled blocks against the oracle, and the first-
-    rejection structure on every block."""
+    corrections only): 512 seeded blocks spread over the 256 sequences (the
+    first or last block of each, and one other) plus every block with a GPU
+    decision margin below 1e-6 at an evaluated position against the oracle,
+    and the first-rejection structure on every block."""
     cfg = workloads.CONFIGS["verify"]
     k, n, V = cfg["k"], cfg["rows"], cfg["V"]
     nb = n // k
@@ -208,21 +238,33 @@ def test_verify_full_size_sampled(saki_lib):
     draft = workloads.drafts(s)
     eps, seed = 0.2, workloads.coupling_seed("verify")
     out = saki_lib.spec_verify(s, t, k, draft, eps, seed, per_pos=False)
+    full = saki_lib.spec_verify(s, t, k, draft, eps, seed)
     torch.cuda.synchronize()
     gpu = dict(accepted_len=out["accepted_len"].cpu().numpy(), correction=out["correction"].cpu().numpy())
     al, co = gpu["accepted_len"], gpu["correction"]
     assert al.shape == (nb,) and al.min() >= 0 and al.max() <= k
     assert np.all((co >= 0) == (al < k)) and co.max() < V
+    # blocks with a near-tie accept decision at an evaluated position (the
+    # margins come from the call with per-position outputs)
+    margin = full["per_pos"]["margin"].cpu().numpy().reshape(nb, k)
+    near = np.nonzero(np.nanmin(np.where(np.isnan(margin), np.inf, margin), axis=1) < parity.MARGIN)[0]
     rng = np.random.default_rng(11)
-    blocks = np.unique(np.concatenate([[0, 1, nb // 2, nb - 1], rng.choice(nb, 4, replace=False)]))
+    per_seq = 32
+    blocks0 = []
+    for q in range(nb // per_seq):
+        lo = q * per_seq
+        edge = lo if q % 2 == 0 else lo + per_seq - 1
+        other = rng.integers(lo + 1, lo + per_seq - 1)
+        blocks0.extend([edge, other])
+    blocks = np.unique(np.concatenate([np.asarray(blocks0), near]))
     idx = np.concatenate([np.arange(b * k, (b + 1) * k) for b in blocks])
     ii = torch.as_tensor(idx, device=DEV)
-    say(f"oracle on blocks {blocks.tolist()}")
-    R = parity.compare_verify(gpu, f64(s[ii]), f64(t[ii]), k, draft[ii].cpu().numpy(), eps, seed, 0,
-                              blocks)
-    say(R.summary())
+    say(f"verify: oracle on {blocks.size} blocks ({near.size} with a GPU margin < 1e-6)")
+    R = parity.compare_verify_pool(gpu, f64(s[ii]), f64(t[ii]), k, draft[ii].cpu().numpy(), eps, seed, 0,
+                                   blocks)
+    say(f"verify: {R.summary()}; mean accepted length {al.mean():.3f}")
     R.check()
-    del s, t, draft, out
+    del s, t, draft, out, full
     torch.cuda.empty_cache()
 
 
@@ -300,32 +342,46 @@ def test_row_cache_boundaries(saki_lib, V):
 
 
 def test_bf16_gradient_and_masks(saki_lib):
+    """bf16 gradient rows against the oracle's gradient (2e-3 absolute plus the
+    bf16 rounding, 2^-8 relative), with masked rows (exact zeros)."""
     s, t = workloads.rows("mid", 0, 64, device=DEV)
     valid = (np.arange(64) % 3 != 0).astype(np.uint8)
     out = saki_lib.couple(s, t, 0.2, 3, 0, route=True, grad_dtype=torch.bfloat16,
                           valid_mask=torch.as_tensor(valid, device=DEV), grad_scale=1.0)
-    ref = saki_lib.couple(s, t, 0.2, 3, 0, route=True, grad_dtype=torch.float32,
-                          valid_mask=torch.as_tensor(valid, device=DEV), grad_scale=1.0)
     torch.cuda.synchronize()
-    gb, gf = out["grad"].float(), ref["grad"]
-    assert torch.all((gb - gf).abs() <= 2 ** -8 * gf.abs() + 1e-30)
-    assert torch.all(gf[torch.as_tensor(valid == 0, device=DEV)] == 0)
+    o = np_out(out)
+    rows = np.arange(64)
+    R = parity.compare_couple(o, f64(s), f64(t), 0.2, 3, 0, rows, grad=f64(out["grad"]), valid=valid,
+                              grad_rtol=2.0 ** -8)
+    say(R.summary())
+    R.check()
+    assert torch.all(out["grad"][torch.as_tensor(valid == 0, device=DEV)] == 0)
 
 
 def test_loss_sum_and_scale(saki_lib):
+    """Events exact except counted near-margin rows; the scaled loss sum
+    against the routed objective (Eq. general_objective) evaluated by the
+    oracle on the GPU's own events."""
     s, t = workloads.rows("tiny", 0, 256, device=DEV)
     valid = (np.arange(256) % 4 != 1).astype(np.uint8)
-    scale = 1.0 / valid.sum()
+    scale = np.float32(1.0 / valid.sum())
     out = saki_lib.couple(s, t, 0.1, 11, 0, route=True, grad_dtype=torch.float32,
-                          valid_mask=torch.as_tensor(valid, device=DEV), grad_scale=scale)
+                          valid_mask=torch.as_tensor(valid, device=DEV), grad_scale=float(scale))
     torch.cuda.synchronize()
     o = np_out(out)
-    ev = coupling.couple_rows(f64(s), f64(t), 0.1, 11, 0)
-    rl, ls, _ = routing.couple_and_route(ev, f64(s), valid, np.float32(scale), want_grad=False)
-    same = (ev["corrected"] == o["corrected"]) & (ev["token"] == o["token"])
-    assert same.mean() > 0.99
-    if same.all():
-        assert abs(o["loss_sum"][0] - ls) <= 1e-5 * np.abs(rl * scale).sum()
+    S, T = f64(s), f64(t)
+    R = parity.compare_couple(o, S, T, 0.1, 11, 0, np.arange(256), valid=valid, grad_scale=float(scale))
+    say(R.summary())
+    R.check()
+    logp, logpi = bridge.log_softmax(S), bridge.log_softmax(T)
+    idx = np.arange(256)
+    y = o["token"].astype(np.int64)
+    adv = logpi[idx, y] - logp[idx, y]
+    rl, ls, _ = routing.route_rows(S, y, o["corrected"], o["target"], adv, valid, float(scale), want_grad=False)
+    assert abs(o["loss_sum"][0] - ls) <= 1e-5 * np.abs(rl * float(scale)).sum()
+    for i in range(256):
+        tol = parity.loss_atol(o["corrected"][i], adv[i], logp[i, y[i]]) if valid[i] else 0.0
+        assert parity.close(o["row_loss"][i], rl[i], atol=tol), i
 
 
 def test_route_loss_standalone(saki_lib):
@@ -423,3 +479,147 @@ def test_zero_rows_is_a_no_op(saki_lib):
     out = saki_lib.couple(s, s, 0.1, 1, 0, route=True, grad_dtype=torch.float32)
     torch.cuda.synchronize()
     assert out["lambda"].numel() == 0
+
+
+def _collect(o, rows, store, idx):
+    for key, v in o.items():
+        if key in ("grad", "loss_sum"):
+            continue
+        if key not in store:
+            store[key] = np.zeros(idx, dtype=v.dtype)
+        store[key][rows] = v
+
+
+@pytest.mark.parametrize("variant", ["", "shared"])
+def test_stream_full_size(saki_lib, variant):
+    """The long-rollout stress workload (262,144 rows of V = 151,936 bf16,
+    eps 0.02) in its 64 chunks of 4,096 rows, each call with its row_offset:
+    8 seeded rows of every chunk (its first and last row, six others) plus every
+    row with a GPU margin below 1e-6 against the oracle (512 rows); the
+    'shared' variant (teacher = the student base, spike moved) on 4 chunks,
+    32 rows each.  The properties that hold at any size on every row."""
+    cfg = workloads.CONFIGS["stream"]
+    V, chunk = cfg["V"], cfg["chunk"]
+    n_total = cfg["rows"]
+    eps, seed = 0.02, workloads.coupling_seed("stream")
+    chunks = range(n_total // chunk) if variant == "" else (0, 21, 42, 63)
+    per_chunk = 8 if variant == "" else 32
+    s = torch.empty(chunk, V, dtype=torch.bfloat16, device=DEV)
+    t = torch.empty_like(s)
+    rng = np.random.default_rng(17)
+    store, S, T, G, rows_all = {}, [], [], [], []
+    n_near = 0
+    for c in chunks:
+        lo = c * chunk
+        workloads.fill("stream", s, t, lo=lo, variant=variant)
+        out = saki_lib.couple(s, t, eps, seed, lo, route=True, grad_dtype=torch.float32, grad_scale=1.0)
+        torch.cuda.synchronize()
+        o = np_out(out)
+        _row_properties(o, eps)
+        near = np.nonzero(o["margin"] < parity.MARGIN)[0]
+        n_near += near.size
+        loc = np.unique(np.concatenate([[0, chunk - 1], rng.choice(np.arange(1, chunk - 1), per_chunk - 2,
+                                                                    replace=False), near]))
+        ii = torch.as_tensor(loc, device=DEV)
+        _collect({k: v[loc] for k, v in o.items() if k not in ("grad", "loss_sum")}, lo + loc, store, n_total)
+        S.append(f64(s[ii]))
+        T.append(f64(t[ii]))
+        G.append(f64(out["grad"][ii]))
+        rows_all.append(lo + loc)
+        del out
+    rows = np.concatenate(rows_all)
+    say(f"stream{'/' + variant if variant else ''}: oracle on {rows.size} rows of {len(chunks)} chunks "
+        f"({n_near} with GPU margin < 1e-6)")
+    R = parity.compare_couple_pool(store, np.concatenate(S), np.concatenate(T), eps, seed, 0, rows,
+                                   grad=np.concatenate(G))
+    say(f"stream{'/' + variant if variant else ''}: {R.summary()}")
+    R.check()
+    del s, t
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("eps", [1e-4, 1e-3, 5e-3])
+def test_annealing_radii(saki_lib, eps):
+    """Radii of the annealing schedule (eps from 0.02 down to 0 over the first
+    50 steps, Sec. 4.1; App. "Limiting Cases"), where the lambda sweeps and
+    the final sweep take their expm1 forms: every tiny row, 64 rows of the
+    large workload, both with the gradient, against the oracle."""
+    s, t = workloads.rows("tiny", 0, 256, device=DEV)
+    out, o, R = run_and_compare(saki_lib, s, t, eps, workloads.coupling_seed("tiny"))
+    _row_properties(o, eps)
+    s, t = workloads.rows("large", 0, 64, device=DEV)
+    out, o, R = run_and_compare(saki_lib, s, t, eps, workloads.coupling_seed("large"))
+    _row_properties(o, eps)
+
+
+def test_annealing_stream_chunk(saki_lib):
+    """A chunk of the long-rollout workload at eps = 4e-4 (step 49 of the
+    linear schedule from 0.02 to 0 over 50 steps): its rows have
+    lambda (d_max - c) above 60 at some search nodes, so the expm1 sweeps take
+    their shifted form.  64 rows plus every near-margin row against the oracle."""
+    lo = 4096 * 5
+    eps, seed = 4e-4, workloads.coupling_seed("stream")
+    s, t = workloads.rows("stream", lo, lo + 4096, device=DEV)
+    out = saki_lib.couple(s, t, eps, seed, lo, route=True, grad_dtype=torch.float32, grad_scale=1.0)
+    torch.cuda.synchronize()
+    o = np_out(out)
+    _row_properties(o, eps)
+    rng = np.random.default_rng(5)
+    near = np.nonzero(o["margin"] < parity.MARGIN)[0]
+    loc = np.unique(np.concatenate([[0, 4095], rng.choice(4096, 62, replace=False), near]))
+    ii = torch.as_tensor(loc, device=DEV)
+    say(f"stream chunk eps={eps}: oracle on {loc.size} rows ({near.size} near-margin)")
+    R = parity.compare_couple_pool(o, f64(s[ii]), f64(t[ii]), eps, seed, lo, loc, grad=f64(out["grad"][ii]))
+    say(R.summary())
+    R.check()
+
+
+def _wide_rows(V, n, s_special, t_special, noise, seed):
+    """Rows of N(0, 1) student logits whose teacher equals the student plus
+    N(0, noise^2), except at one entry per row where the student logit is
+    s_special and the teacher logit t_special: d = t - s spans more than 100
+    there, so lambda* (d_max - c) exceeds 60 at the radii below and q/p can
+    exceed float's range."""
+    g = torch.Generator(device=DEV).manual_seed(seed)
+    s = torch.randn(n, V, generator=g, device=DEV)
+    t = s + noise * torch.randn(n, V, generator=g, device=DEV)
+    j = torch.randint(0, V, (n,), generator=g, device=DEV)
+    r = torch.arange(n, device=DEV)
+    s[r, j] = s_special
+    t[r, j] = t_special
+    return padded(s.to(torch.bfloat16)), padded(t.to(torch.bfloat16))
+
+
+@pytest.mark.parametrize("V,s_sp,t_sp,noise,eps", [
+    (151936, -80.0, 40.0, 0.3, 1.0),    # lambda* ~ 0.7: shifted node sums
+    (151936, -80.0, 40.0, 0.3, 20.0),   # q concentrated on the special entry: q/p ~ e^92
+    (151936, -100.0, 30.0, 0.0, 5e-3),  # small radius with lambda* (d_max - c) > 60: shifted expm1 sums
+    (4096, -100.0, 30.0, 0.0, 2e-3),
+])
+def test_wide_range_rows(saki_lib, V, s_sp, t_sp, noise, eps):
+    """Rows whose d = t - s spans more than 100: the lambda sweeps take their
+    shifted exponents (lambda (d_max - c) > 60), in the plain or the expm1
+    form, and the final sweep the form for q/p beyond float's range.  Every
+    row against the oracle, with the gradient."""
+    s, t = _wide_rows(V, 8, s_sp, t_sp, noise, 1000 + V)
+    out, o, R = run_and_compare(saki_lib, s, t, eps, 31337, row_offset=40)
+    assert np.all(np.isfinite(o["tv"])) and np.all(o["row_status"] == 0)
+    lam = o["lambda"]
+    say(f"lambda* {np.round(lam, 4).tolist()}")
+    assert np.all(lam < 1)
+
+
+@pytest.mark.parametrize("sigma", [0.05, 0.01])
+def test_endpoint_small_kl(saki_lib, sigma):
+    """t = s + N(0, sigma^2): KL(pi || p) ~ sigma^2 / 2 lies below both the
+    radius 0.02 and 0.01, so lambda* = 1 and the endpoint is resolved with the
+    expm1 form of the sweep (and the final sweep's).  Every row against the
+    oracle."""
+    g = torch.Generator(device=DEV).manual_seed(int(sigma * 1000))
+    n, V = 32, 3000
+    s = 2.0 * torch.randn(n, V, generator=g, device=DEV)
+    t = s + sigma * torch.randn(n, V, generator=g, device=DEV)
+    s, t = padded(s), padded(t)
+    out, o, R = run_and_compare(saki_lib, s, t, 0.02, 404)
+    assert np.all(o["lambda"] == 1.0)
+    assert np.all(o["kl"] < 0.01)
