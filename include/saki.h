@@ -169,6 +169,29 @@ saki_status saki_couple(const saki_rows *in, double eps, uint64_t seed, const sa
                         const saki_route_args *route, void *ws, size_t ws_bytes,
                         saki_stream_t stream);
 
+/* Largest n_rows of one saki_couple_static call. */
+#define SAKI_STATIC_MAX_ROWS 262144
+
+/* saki_couple for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation.  Same
+ * arguments, kernels and results as saki_couple, without the workspace: the
+ * row work counter and the scaled row losses live in a static device array of
+ * the library (256 + 8 * SAKI_STATIC_MAX_ROWS bytes = 2 MiB + 256 B), which
+ * each GPU the library runs on holds until the process ends.  Its device
+ * address is looked up once per device, on the first call made with that
+ * device current.  The call allocates and frees nothing.
+ *   n_rows > SAKI_STATIC_MAX_ROWS  SAKI_E_SHAPE, nothing enqueued (split the
+ *                                  rows into calls with row_offset)
+ * The array keeps the last call's contents; each call clears the counter
+ * itself (a kernel on `stream`) and writes every scaled row loss before
+ * summing them.  All calls on one GPU share the array: calls whose work can
+ * overlap in time on one GPU (other streams, concurrent graph replays) race
+ * and give wrong results; serialise them, or use saki_couple with separate
+ * workspaces. */
+saki_status saki_couple_static(const saki_rows *in, double eps, uint64_t seed,
+                               const saki_couple_out *out, const saki_route_args *route,
+                               saki_stream_t stream);
+
 /* Routed loss and gradient from given events (Sec. 3.4), for callers that
  * already hold the coupling results.  student: [n_rows, row_stride] logits of
  * pi_theta (= p).  token y, corrected C, teacher_argmax v* and advantage A

@@ -18,6 +18,7 @@ SAKI_OP_COUPLE, SAKI_OP_ROUTE, SAKI_OP_VERIFY, SAKI_OP_SELECT = 0, 1, 2, 3
 SAKI_TARGET_MODE, SAKI_TARGET_SAMPLE = 0, 1
 SAKI_SELECT_RANDOM, SAKI_SELECT_TV_WEIGHTED = 0, 1
 SAKI_MAX_VOCAB = 1 << 21
+SAKI_STATIC_MAX_ROWS = 262144
 SAKI_CHUNK = 1024
 ROW_OK, ROW_NONFINITE, ROW_BAD_DRAFT, ROW_SKIPPED = 0, 1, 2, 3
 
@@ -25,7 +26,7 @@ STATUS = {0: "SAKI_OK", 1: "SAKI_E_NULLPTR", 2: "SAKI_E_SHAPE", 3: "SAKI_E_VALUE
           4: "SAKI_E_DTYPE", 5: "SAKI_E_ALIGN", 6: "SAKI_E_WORKSPACE", 7: "SAKI_E_DEVICE",
           8: "SAKI_E_LAUNCH"}
 
-EXPORTED = ["saki_workspace_bytes", "saki_couple", "saki_route_loss", "saki_spec_verify",
+EXPORTED = ["saki_workspace_bytes", "saki_couple", "saki_couple_static", "saki_route_loss", "saki_spec_verify",
             "saki_select_positions", "saki_probe_metrics", "saki_sample", "saki_commit",
             "saki_status_str", "saki_last_error"]
 SEQ_RUNNING, SEQ_FINISHED, SEQ_STOPPED = 0, 1, 2
@@ -93,6 +94,10 @@ def load(path=LIB_PATH):
     lib.saki_couple.argtypes = [ctypes.POINTER(SakiRows), ctypes.c_double, ctypes.c_uint64,
                                 ctypes.POINTER(SakiCoupleOut), ctypes.POINTER(SakiRouteArgs),
                                 ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    lib.saki_couple_static.restype = ctypes.c_int
+    lib.saki_couple_static.argtypes = [ctypes.POINTER(SakiRows), ctypes.c_double, ctypes.c_uint64,
+                                       ctypes.POINTER(SakiCoupleOut), ctypes.POINTER(SakiRouteArgs),
+                                       ctypes.c_void_p]
     lib.saki_route_loss.restype = ctypes.c_int
     lib.saki_route_loss.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64,
                                     ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
@@ -223,6 +228,23 @@ def saki_couple(student, teacher, eps, seed, row_offset=0, out=None, route=None,
     st = _lib.saki_couple(ctypes.byref(rows), float(eps), int(seed) & (2**64 - 1),
                           ctypes.byref(co), ctypes.byref(rt) if rt is not None else None,
                           _ptr(workspace), ws_b, _stream(stream))
+    _check(st)
+
+
+def saki_couple_static(student, teacher, eps, seed, row_offset=0, out=None, route=None, stream=None):
+    """Call saki_couple_static (no workspace: the library's static scratch) on
+    preallocated buffers; out and route as for saki_couple."""
+    load()
+    rows = _rows(student, teacher, row_offset)
+    co = _couple_struct(out or {})
+    rt = None
+    if route is not None:
+        rt = _route_struct(route.get("valid_mask"), route.get("grad_scale", 1.0),
+                           route.get("row_loss"), route.get("loss_sum"), route.get("grad"),
+                           route.get("correction_target", SAKI_TARGET_MODE))
+    st = _lib.saki_couple_static(ctypes.byref(rows), float(eps), int(seed) & (2**64 - 1),
+                                 ctypes.byref(co), ctypes.byref(rt) if rt is not None else None,
+                                 _stream(stream))
     _check(st)
 
 

@@ -807,10 +807,42 @@ size_t saki_workspace_bytes(int op, int64_t n_rows, int64_t vocab) {
 
 }  // extern "C"
 
+// The library's own scratch for saki_couple_static: the row work counter (256
+// bytes), then one double per row for the scaled row losses.  Each GPU the
+// library runs on holds its own copy until the process ends.  In host code
+// `scratch` names a host-side stand-in, not the device array: only the
+// address from hipGetSymbolAddress (static_scratch) is passed to kernels.
+static __device__ __align__(256) unsigned char scratch[256 + SAKI_STATIC_MAX_ROWS * sizeof(double)];
+
 namespace {
 
+constexpr size_t STATIC_SCRATCH_BYTES = 256 + static_cast<size_t>(SAKI_STATIC_MAX_ROWS) * sizeof(double);
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept.
+saki_status static_scratch(void** ptr) {
+  static std::mutex mu;
+  static void* cache[64] = {nullptr};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return fail(SAKI_E_DEVICE, "hipGetDevice failed");
+  if (dev >= 64) return fail(SAKI_E_DEVICE, "device index above 63");
+  std::lock_guard<std::mutex> lock(mu);
+  if (cache[dev] == nullptr) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return fail(SAKI_E_DEVICE, std::string("hipGetSymbolAddress(scratch) failed: ") + hipGetErrorString(e));
+    cache[dev] = p;
+  }
+  *ptr = cache[dev];
+  return SAKI_OK;
+}
+
+// use_static: the workspace is the static scratch (ws and ws_bytes unused),
+// looked up after every argument check.
 saki_status couple_impl(const saki_rows* in, double eps, uint64_t seed, const saki_couple_out* out,
-                        const saki_route_args* route, void* ws, size_t ws_bytes, saki_stream_t stream);
+                        const saki_route_args* route, void* ws, size_t ws_bytes, saki_stream_t stream,
+                        bool use_static);
 
 }  // namespace
 
@@ -818,7 +850,12 @@ extern "C" {
 
 saki_status saki_couple(const saki_rows* in, double eps, uint64_t seed, const saki_couple_out* out,
                         const saki_route_args* route, void* ws, size_t ws_bytes, saki_stream_t stream) {
-  return couple_impl(in, eps, seed, out, route, ws, ws_bytes, stream);
+  return couple_impl(in, eps, seed, out, route, ws, ws_bytes, stream, false);
+}
+
+saki_status saki_couple_static(const saki_rows* in, double eps, uint64_t seed, const saki_couple_out* out,
+                               const saki_route_args* route, saki_stream_t stream) {
+  return couple_impl(in, eps, seed, out, route, nullptr, 0, stream, true);
 }
 
 }  // extern "C"
@@ -826,7 +863,8 @@ saki_status saki_couple(const saki_rows* in, double eps, uint64_t seed, const sa
 namespace {
 
 saki_status couple_impl(const saki_rows* in, double eps, uint64_t seed, const saki_couple_out* out,
-                        const saki_route_args* route, void* ws, size_t ws_bytes, saki_stream_t stream) {
+                        const saki_route_args* route, void* ws, size_t ws_bytes, saki_stream_t stream,
+                        bool use_static) {
   saki_status st = check_rows(in);
   if (st != SAKI_OK) return st;
   if (!out) return fail(SAKI_E_NULLPTR, "out is NULL");
@@ -834,8 +872,15 @@ saki_status couple_impl(const saki_rows* in, double eps, uint64_t seed, const sa
   bool want_sum = false;
   st = check_route(route, in->vocab, &want_sum);
   if (st != SAKI_OK) return st;
+  if (use_static && in->n_rows > SAKI_STATIC_MAX_ROWS)
+    return fail(SAKI_E_SHAPE, "n_rows above SAKI_STATIC_MAX_ROWS (the static scratch holds one double per row)");
   if (in->n_rows == 0) return ok();
   if (in->n_rows >= (int64_t{1} << 31)) return fail(SAKI_E_SHAPE, "more than 2^31 - 1 rows in one call");
+  if (use_static) {
+    st = static_scratch(&ws);
+    if (st != SAKI_OK) return st;
+    ws_bytes = STATIC_SCRATCH_BYTES;
+  }
   if (!ws) return fail(SAKI_E_WORKSPACE, "workspace is NULL");
   if (ws_bytes < saki_workspace_bytes(SAKI_OP_COUPLE, in->n_rows, in->vocab))
     return fail(SAKI_E_WORKSPACE, "workspace smaller than saki_workspace_bytes(SAKI_OP_COUPLE)");

@@ -199,3 +199,21 @@ def test_commit_argument_errors(lib):
     assert f(ctypes.byref(_traj()), 4, -1, a, c, None, None, None) == 1
     assert f(ctypes.byref(_traj()), 4, -1, a, c, ctypes.byref(binding.SakiCoupleOut()), None, None) == 1
     assert f(ctypes.byref(_traj(n_seq=0)), 4, -1, None, None, None, None, None) == 0
+
+
+def test_static_scratch_entry_rejects_without_launch(lib):
+    """saki_couple_static: the same argument checks as saki_couple, and more
+    rows than its static scratch holds is SAKI_E_SHAPE before any device call."""
+    co = binding.SakiCoupleOut()
+
+    def call(rows, eps=0.1):
+        return lib.saki_couple_static(ctypes.byref(rows), eps, 1, ctypes.byref(co), None, None)
+
+    assert binding.SAKI_STATIC_MAX_ROWS == 262144
+    assert call(_rows(n_rows=binding.SAKI_STATIC_MAX_ROWS + 1)) == 2
+    assert b"SAKI_STATIC_MAX_ROWS" in lib.saki_last_error()
+    assert call(_rows(vocab=0)) == 2
+    assert call(_rows(), eps=-1.0) == 3
+    assert call(_rows(student=17)) == 5
+    assert call(_rows(n_rows=0)) == 0
+    assert lib.saki_couple_static(None, 0.1, 1, ctypes.byref(co), None, None) == 1
