@@ -159,10 +159,13 @@ size_t saki_workspace_bytes(int op, int64_t n_rows, int64_t vocab);
  *   out    per-row outputs (any field may be NULL); out itself may not be NULL
  *   route  NULL for coupling only
  *   ws     required when n_rows > 0: ws_bytes >= saki_workspace_bytes(SAKI_OP_COUPLE,
- *          n_rows, vocab), 8-byte aligned.  Its first 256 bytes hold the counter from
- *          which workgroups take rows (cleared by the call on `stream`); with
- *          route->loss_sum the scaled row losses follow.  Calls that may run at the
- *          same time need separate workspaces.
+ *          n_rows, vocab), 8-byte aligned.  Its first 256 bytes hold the counters
+ *          from which workgroups take rows (cleared by the call on `stream`); the
+ *          scaled row losses follow (with route->loss_sum), then the list of rows
+ *          a second launch of the call resolves again with every sweep in its
+ *          expm1 form (rows whose TV turns out too small for the plain forms'
+ *          rounding; rare).  Calls that may run at the same time need separate
+ *          workspaces.
  * More than 2^31 - 1 rows in one call is SAKI_E_SHAPE (split the rows into calls
  * with row_offset; results do not change). */
 saki_status saki_couple(const saki_rows *in, double eps, uint64_t seed, const saki_couple_out *out,
@@ -175,16 +178,17 @@ saki_status saki_couple(const saki_rows *in, double eps, uint64_t seed, const sa
 /* saki_couple for callers that cannot allocate device memory: code under HIP
  * graph capture, tight serving loops, harnesses that forbid allocation.  Same
  * arguments, kernels and results as saki_couple, without the workspace: the
- * row work counter and the scaled row losses live in a static device array of
- * the library (256 + 8 * SAKI_STATIC_MAX_ROWS bytes = 2 MiB + 256 B), which
- * each GPU the library runs on holds until the process ends.  Its device
+ * work counters, the scaled row losses and the list of rows for the second
+ * launch live in a static device array of the library (256 + 12 *
+ * SAKI_STATIC_MAX_ROWS bytes = 3 MiB + 256 B), which each GPU the library runs
+ * on holds until the process ends.  Its device
  * address is looked up once per device, on the first call made with that
  * device current.  The call allocates and frees nothing.
  *   n_rows > SAKI_STATIC_MAX_ROWS  SAKI_E_SHAPE, nothing enqueued (split the
  *                                  rows into calls with row_offset)
- * The array keeps the last call's contents; each call clears the counter
- * itself (a kernel on `stream`) and writes every scaled row loss before
- * summing them.  All calls on one GPU share the array: calls whose work can
+ * The array keeps the last call's contents; each call clears the counters
+ * itself (a kernel on `stream`), writes every scaled row loss before summing
+ * them and every list entry before the second launch reads it.  All calls on one GPU share the array: calls whose work can
  * overlap in time on one GPU (other streams, concurrent graph replays) race
  * and give wrong results; serialise them, or use saki_couple with separate
  * workspaces. */

@@ -298,15 +298,6 @@ __device__ __forceinline__ void wave_argmin(double& key, int& idx) {
     if (k2 < key || (k2 == key && i2 < idx)) { key = k2; idx = i2; }
   }
 }
-// Smallest index over the wave, carrying a float of its lane along.
-__device__ __forceinline__ void wave_min_index_with(int& idx, float& val) {
-#pragma unroll
-  for (int o = WAVE / 2; o > 0; o >>= 1) {
-    const int i2 = __shfl_xor(idx, o, WAVE);
-    const float v2 = __shfl_xor(val, o, WAVE);
-    if (i2 < idx) { idx = i2; val = v2; }
-  }
-}
 // (value, index) maximum; ties go to the lower index.
 __device__ __forceinline__ void wave_argmax(float& val, int& idx) {
 #pragma unroll

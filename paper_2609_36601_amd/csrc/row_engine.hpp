@@ -38,8 +38,7 @@ struct RowStats {
   float dmin, dmax;    // range of d = t - s
   float tmax;          // max t
   int vstar;           // argmax t, lowest index on ties
-  int sidx;            // argmax s (the dominant entry of p), lowest index on ties
-  float t_sidx;        // t at sidx
+  float t_smax;        // t at an entry holding max s (the dominant entry of p)
   double pmax;         // max_v p_v = exp(ms - lse_s)
   bool finite;
 };
@@ -375,8 +374,7 @@ struct StatsAcc {
   float S1, S2, S3, S4;         // per-lane p-weighted powers of d (relative to Ms)
   float T1, T2;                 // per-lane pi-weighted sums of d, d^2 (relative to Mt)
   int tidx;                     // wave-uniform lowest index of the running max of t
-  int sidx;                     // wave-uniform lowest index of the running max of s
-  float t_sidx;                 // t at sidx
+  float t_smax;                 // wave-uniform: t at an entry holding the running max of s
   float dmin, dmax;             // per-lane range of d
   __device__ void init() {
     Ms = -finf(); Mt = -finf();
@@ -384,8 +382,7 @@ struct StatsAcc {
     Ss = St = 0.0;
     S1 = S2 = S3 = S4 = T1 = T2 = 0.f;
     tidx = 0x7fffffff;
-    sidx = 0x7fffffff;
-    t_sidx = 0.f;
+    t_smax = 0.f;
     dmin = finf(); dmax = -finf();
   }
 };
@@ -418,15 +415,12 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
   a.dmax = fmaxf(a.dmax, lmax);
   if (wave_any(ls > a.Ms)) {
     const float cms = wave_max(ls);
-    // a new running maximum of s: its lowest index in this chunk, and its t
-    int li = 0x7fffffff;
-    float lt = 0.f;
+    // a new running maximum of s: the largest t among the entries holding it
+    float lt = -finf();
 #pragma unroll
-    for (int e = EPL - 1; e >= 0; --e)
-      if (SAKI_VALID(e) && s[e] == cms) { li = c * CHUNK + elem_offset(lane, e); lt = t[e]; }
-    wave_min_index_with(li, lt);
-    a.sidx = li;
-    a.t_sidx = lt;
+    for (int e = 0; e < EPL; ++e)
+      if (SAKI_VALID(e) && s[e] == cms) lt = fmaxf(lt, t[e]);
+    a.t_smax = wave_max(lt);
     // rounded product and difference, never contracted into one fma: the sums
     // so far are relative to exactly the MsL the later terms use
     const float cmsL = __fmul_rn(cms, LOG2E);
@@ -452,11 +446,10 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
     a.Mt = cmt;
     a.MtL = cmtL;
   }
-  // normalisers: each term added in double (a float sum of terms next to a
-  // dominant one of ~1 would lose ~6e-8 of it: the log-probability of the
-  // dominant entry of a peaked row needs it)
+  // normalisers: float sums of four entries (within three roundings each),
+  // then double
   double ps = 0.0, pt = 0.0;
-  float p1 = 0.f, p2 = 0.f, p3 = 0.f, p4 = 0.f, t1 = 0.f, t2 = 0.f;
+  float gs = 0.f, gt = 0.f, p1 = 0.f, p2 = 0.f, p3 = 0.f, p4 = 0.f, t1 = 0.f, t2 = 0.f;
 #pragma unroll
   for (int e = 0; e < EPL; ++e) {
     float es = fexp2(fmaf(s[e], LOG2E, -a.MsL));
@@ -473,8 +466,14 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
     const float etd = et * d;
     t1 += etd;
     t2 = fmaf(etd, d, t2);
-    ps += static_cast<double>(es);
-    pt += static_cast<double>(et);
+    gs += es;
+    gt += et;
+    if ((e & 3) == 3) {
+      ps += static_cast<double>(gs);
+      pt += static_cast<double>(gt);
+      gs = 0.f;
+      gt = 0.f;
+    }
   }
   if (keep_chunks) {
     const float csum = static_cast<float>(wave_sum(ps));
@@ -506,8 +505,7 @@ struct StatsBlock {
   double Ss, S1, S2, S3, S4, St, T1, T2;
   float tbest;
   int tidx;
-  int sidx;
-  float t_sidx;
+  float t_smax;
   float dmin, dmax;
 };
 
@@ -533,8 +531,7 @@ __device__ StatsBlock stats_combine_block(Block<NT, SH>& B, StatsAcc& a) {
     B.sh.red_f[B.wave][2] = wdmin;
     B.sh.red_f[B.wave][3] = wdmax;
     B.sh.red_i[B.wave][0] = a.tidx;
-    B.sh.red_i[B.wave][1] = a.sidx;
-    B.sh.red_d[B.wave][10] = static_cast<double>(a.t_sidx);
+    B.sh.red_d[B.wave][10] = static_cast<double>(a.t_smax);
   }
   __syncthreads();
   StatsBlock O;
@@ -550,8 +547,8 @@ __device__ StatsBlock stats_combine_block(Block<NT, SH>& B, StatsAcc& a) {
   }
   double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   float tb = -finf();
-  int ti = 0x7fffffff, si = 0x7fffffff;
-  float st = 0.f;
+  int ti = 0x7fffffff;
+  float st = -finf();
   // each wave's sums are relative to 2^(its MsL): rescale to the block's
   // msL = ms log2(e) rounded (the MsL of a wave holding the maximum), then
   // remove that rounding (shift_correction)
@@ -567,8 +564,7 @@ __device__ StatsBlock stats_combine_block(Block<NT, SH>& B, StatsAcc& a) {
     for (int i = 5; i < 8; ++i) acc[i] += B.sh.red_d[w][i] * gt;
     const int wi = B.sh.red_i[w][0];
     if (wMt > tb || (wMt == tb && wi < ti)) { tb = wMt; ti = wi; }
-    const int ws = B.sh.red_i[w][1];
-    if (wMs == O.ms && ws < si) { si = ws; st = static_cast<float>(B.sh.red_d[w][10]); }
+    if (wMs == O.ms) st = fmaxf(st, static_cast<float>(B.sh.red_d[w][10]));
   }
   __syncthreads();
   const double cs = shift_correction(O.ms, msL), ct = shift_correction(O.mt, mtL);
@@ -582,8 +578,7 @@ __device__ StatsBlock stats_combine_block(Block<NT, SH>& B, StatsAcc& a) {
   O.St = acc[5] * ct + dom_t; O.T1 = acc[6] * ct; O.T2 = acc[7] * ct;
   O.tbest = tb;
   O.tidx = ti;
-  O.sidx = si;
-  O.t_sidx = st;
+  O.t_smax = st;
   return O;
 }
 
@@ -596,8 +591,7 @@ __device__ inline RowStats row_stats_from(const StatsBlock& O) {
   R.dmax = O.dmax;
   R.tmax = O.tbest;
   R.vstar = O.tidx;
-  R.sidx = O.sidx;
-  R.t_sidx = O.t_sidx;
+  R.t_smax = O.t_smax;
   R.sum_s = O.Ss;
   R.lse_s = static_cast<double>(R.ms) + log(O.Ss);
   R.lse_t = static_cast<double>(R.mt) + log(O.St);
@@ -766,6 +760,27 @@ __device__ inline LamEval lam_finish(const double (&v)[5], double b0, float lam,
   return E;
 }
 
+// The dominant entry of p (an entry holding max s) carries the largest
+// rounding of the plain w - p~ (~6e-8 of its p~, a p~ near 1 on a peaked row).
+// Every thread computes that entry's plain term exactly as the sweep did (the
+// same float operations) and its exact value, p~ expm1(lam x) in double; the
+// difference replaces it in the row sum.  Its own a is the shift's rounding
+// (|a| ~ 1e-6), so 2^a is the quadratic below to rounding; only where
+// |lam x| < 1/16 is the plain term's rounding large next to the term itself
+// (expm1 by its series there).
+__device__ __forceinline__ double dominant_fix(float s, float t, float msL, float cL, float lam) {
+  const float a = fmaf(s, LOG2E, -msL);
+  const float X = fmaf(t - s, LOG2E, -cL);
+  const double y = static_cast<double>(lam) * static_cast<double>(X) * LN2_D;
+  if (!(fabs(y) < 0.0625)) return 0.0;
+  const float uf = fexp2(fmaf(lam, X, a)) - fexp2(a);
+  const double al = static_cast<double>(a) * LN2_D;
+  const double pt = 1.0 + al * (1.0 + 0.5 * al);
+  const double em = y * (1.0 + y * (0.5 + y * (1.0 / 6 + y * (1.0 / 24 + y * (1.0 / 120 + y * (1.0 / 720 +
+                    y * (1.0 / 5040)))))));
+  return pt * em - static_cast<double>(uf);
+}
+
 template <typename T, int NT, int MODE, typename SH>
 __device__ LamEval lam_sweep_mode(Block<NT, SH>& B, const T* srow, const T* trow, int V, const RowStats& R,
                                   float lam, float sigl, bool accf) {
@@ -777,31 +792,8 @@ __device__ LamEval lam_sweep_mode(Block<NT, SH>& B, const T* srow, const T* trow
                       constexpr bool TAIL = decltype(tail)::value;
                       lam_math<MODE, TAIL>(s, t, vm, msL, R.cL, lam, sigl, accf, v);
                     }, row_cache<T>(B.sh));
-  if constexpr (MODE == LAM_FAST) {
-    // The dominant entry of p (sidx) carries the largest rounding of the
-    // plain w - p~ (~6e-8 of its p~, a p~ near 1 on a peaked row): its owner
-    // replaces that term with the exact value, p~ expm1(lam x) in double, for
-    // the same float a and X.
-    // Its own a is the shift's rounding (|a| ~ 1e-6), so 2^a is the
-    // quadratic below to rounding; only where |lam x| < 1/16 is the plain
-    // term's rounding large next to the term itself (expm1 by its series).
-    const int sidx = R.sidx;
-    if (sidx < V && B.tid == entry_owner<NT>(sidx)) {
-      const float s = R.ms, t = R.t_sidx;
-      const float a = fmaf(s, LOG2E, -msL);
-      const float X = fmaf(t - s, LOG2E, -R.cL);
-      const double y = static_cast<double>(lam) * static_cast<double>(X) * LN2_D;
-      if (fabs(y) < 0.0625) {
-        const float uf = fexp2(fmaf(lam, X, a)) - fexp2(a);
-        const double al = static_cast<double>(a) * LN2_D;
-        const double pt = 1.0 + al * (1.0 + 0.5 * al);
-        const double em = y * (1.0 + y * (0.5 + y * (1.0 / 6 + y * (1.0 / 24 + y * (1.0 / 120 + y * (1.0 / 720 +
-                          y * (1.0 / 5040)))))));
-        v[0] += pt * em - static_cast<double>(uf);
-      }
-    }
-  }
   B.sum(v);
+  if constexpr (MODE == LAM_FAST) v[0] += dominant_fix(R.ms, R.t_smax, msL, R.cL, lam);
   const double corr = shift_correction(R.ms, msL);
 #pragma unroll
   for (int j = 0; j < 5; ++j) v[j] *= corr;

@@ -48,14 +48,20 @@ struct CoupleParams {
   int64_t grad_stride;
   int target_mode;      // SAKI_TARGET_MODE or SAKI_TARGET_SAMPLE
   unsigned int* next_row;  // work counter in the caller's workspace, zero at launch
+  // Rows resolved in the plain forms whose TV turns out too small for their
+  // rounding are listed (redo_list, redo_count, in the workspace) and processed
+  // again by a second launch with every sweep in the expm1 form (redo_pass).
+  unsigned int* redo_list;
+  unsigned int* redo_count;
+  int redo_pass;
 };
 
 __device__ __forceinline__ float nanf_() { return __builtin_nanf(""); }
 
-// Clears a work counter (a kernel rather than a memset node, so that a
-// captured graph replays it correctly).
+// Clears the work counters at the start of a workspace (a kernel rather than
+// a memset node, so that a captured graph replays it correctly).
 __global__ void clear_counter_kernel(unsigned int* c) {
-  if (threadIdx.x == 0) *c = 0u;
+  if (threadIdx.x < 4) c[threadIdx.x] = 0u;
 }
 
 // Takes the next work item (row or block) for the whole workgroup: thread 0
@@ -81,11 +87,16 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
   // a fixed stride left the slowest ones finishing ~15% after the median.
   // Each iteration takes a new row or ends the loop: at most n_rows + 1.
   __shared__ unsigned int next_r;
+  // the second launch takes its rows from the list the first one made
+  const unsigned int n_work = P.redo_pass
+      ? static_cast<unsigned int>(__builtin_amdgcn_readfirstlane(static_cast<int>(*P.redo_count)))
+      : static_cast<unsigned int>(P.n_rows);
+  const bool force_acc = P.redo_pass != 0;
   for (int64_t it = 0; it <= P.n_rows; ++it) {
     const unsigned int ru = take_next(P.next_row, &next_r);
     // unsigned: n_rows < 2^31 and the counter stays below n_rows + grid
-    if (ru >= static_cast<unsigned int>(P.n_rows)) break;
-    const int64_t r = static_cast<int64_t>(ru);
+    if (ru >= n_work) break;
+    const int64_t r = static_cast<int64_t>(P.redo_pass ? P.redo_list[ru] : ru);
     const T* srow = static_cast<const T*>(P.s) + r * P.stride;
     const T* trow = static_cast<const T*>(P.t) + r * P.stride;
     G* grow = GRAD ? static_cast<G*>(P.grad) + r * P.grad_stride : nullptr;
@@ -93,11 +104,6 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
     const float M = (ROUTE && P.valid) ? (P.valid[r] ? 1.0f : 0.0f) : 1.0f;
 
     const bool sample_target = ROUTE && P.target_mode == SAKI_TARGET_SAMPLE;
-    // A row resolved in a plain form whose TV turns out too small for that
-    // form's rounding is processed again from the start with every sweep in
-    // the expm1 form (rare); nothing but the pass number crosses the restart.
-    for (int pass = 0; pass < 2; ++pass) {
-    const bool force_acc = pass > 0;
     const RowStats& R = stats_sweep<T, NT>(B, srow, trow, V, true, sample_target);
     if (!R.finite) {
       if (GRAD) fill_row<G, NT>(B.wave, B.lane, grow, V, M != 0.0f ? nanf_() : 0.0f);
@@ -123,7 +129,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
           if (P.scaled_loss) P.scaled_loss[r] = static_cast<double>(l);
         }
       }
-      break;
+      continue;
     }
 
     // z ~ p by the two-level race (chunk masses from the stats sweep): the
@@ -179,7 +185,12 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
 
     const FinalConst F = final_const(R, L, force_acc);
     const double TV = final_sweep_any<T, G, NT, GRAD>(B, srow, trow, grow, V, F, C, coef, hot, s_hot);
-    if (!force_acc && redo_accurate(R, L, F.acc, TV)) continue;
+    if (!force_acc && redo_accurate(R, L, F.acc, TV)) {
+      // listed for the second launch, which rewrites the row's gradient and
+      // writes its outputs
+      if (B.tid == 0) P.redo_list[atomicAdd(P.redo_count, 1u)] = static_cast<unsigned int>(r);
+      continue;
+    }
 
     int y = z;
     float sy = sz, ty = tz;
@@ -239,8 +250,6 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
         if (P.scaled_loss) P.scaled_loss[r] = static_cast<double>(P.grad_scale) * l;
       }
     }
-    break;
-    }  // pass
   }
 }
 
@@ -751,6 +760,11 @@ size_t loss_ws_bytes(int64_t n_rows) {
   return (b + 255) & ~static_cast<size_t>(255);
 }
 
+size_t list_ws_bytes(int64_t n_rows) {
+  const size_t b = static_cast<size_t>(n_rows) * sizeof(unsigned int);
+  return (b + 255) & ~static_cast<size_t>(255);
+}
+
 saki_status launched(const char* what) {
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(SAKI_E_LAUNCH, std::string(what) + ": " + hipGetErrorString(e));
@@ -793,7 +807,9 @@ size_t saki_workspace_bytes(int op, int64_t n_rows, int64_t vocab) {
   if (n_rows <= 0) return 0;
   switch (op) {
     case SAKI_OP_COUPLE:
-      return 256 + loss_ws_bytes(n_rows);  // the row counter, then the scaled row losses
+      // the counters, the scaled row losses, the list of rows for the
+      // second (expm1-form) launch
+      return 256 + loss_ws_bytes(n_rows) + list_ws_bytes(n_rows);
     case SAKI_OP_ROUTE:
       return 256 + loss_ws_bytes(n_rows);  // the row counter, then the scaled row losses
     case SAKI_OP_VERIFY:
@@ -807,16 +823,18 @@ size_t saki_workspace_bytes(int op, int64_t n_rows, int64_t vocab) {
 
 }  // extern "C"
 
-// The library's own scratch for saki_couple_static: the row work counter (256
-// bytes), then one double per row for the scaled row losses.  Each GPU the
+// The library's own scratch for saki_couple_static: the work counters (256
+// bytes), one double per row for the scaled row losses, one index per row for
+// the list of rows the second launch processes in the expm1 forms.  Each GPU the
 // library runs on holds its own copy until the process ends.  In host code
 // `scratch` names a host-side stand-in, not the device array: only the
 // address from hipGetSymbolAddress (static_scratch) is passed to kernels.
-static __device__ __align__(256) unsigned char scratch[256 + SAKI_STATIC_MAX_ROWS * sizeof(double)];
+static __device__ __align__(256) unsigned char scratch[256 + SAKI_STATIC_MAX_ROWS * (sizeof(double) + sizeof(unsigned int))];
 
 namespace {
 
-constexpr size_t STATIC_SCRATCH_BYTES = 256 + static_cast<size_t>(SAKI_STATIC_MAX_ROWS) * sizeof(double);
+constexpr size_t STATIC_SCRATCH_BYTES =
+    256 + static_cast<size_t>(SAKI_STATIC_MAX_ROWS) * (sizeof(double) + sizeof(unsigned int));
 
 // Device address of `scratch` on the current device, looked up once per
 // device (with that device current) and kept.
@@ -908,17 +926,30 @@ saki_status couple_impl(const saki_rows* in, double eps, uint64_t seed, const sa
     P.grad_stride = route->grad_stride;
     P.target_mode = route->correction_target;
   }
-  P.next_row = static_cast<unsigned int*>(ws);
+  // workspace: [0] row counter, [1] second launch's row counter, [2] listed
+  // rows; then the scaled row losses; then the list
+  unsigned int* const counters = static_cast<unsigned int*>(ws);
+  P.next_row = counters;
+  P.redo_count = counters + 2;
+  P.redo_list = reinterpret_cast<unsigned int*>(static_cast<char*>(ws) + 256 + loss_ws_bytes(in->n_rows));
+  P.redo_pass = 0;
   const int grid = static_cast<int>(std::min<int64_t>(in->n_rows, static_cast<int64_t>(cus) * saki::WG_PER_CU));
   hipStream_t hs = static_cast<hipStream_t>(stream);
-  hipLaunchKernelGGL(saki::clear_counter_kernel, dim3(1), dim3(64), 0, hs, P.next_row);
+  hipLaunchKernelGGL(saki::clear_counter_kernel, dim3(1), dim3(64), 0, hs, counters);
   st = launched("clear_counter_kernel");
   if (st != SAKI_OK) return st;
   const bool grad = route && route->grad;
-  st = (in->dtype == SAKI_BF16)
-           ? dispatch_couple<uint16_t>(P, route != nullptr, grad, route ? route->grad_dtype : 0, grid, hs)
-           : dispatch_couple<float>(P, route != nullptr, grad, route ? route->grad_dtype : 0, grid, hs);
-  if (st != SAKI_OK) return st;
+  for (int pass = 0; pass < 2; ++pass) {
+    // the second launch: the listed rows, every sweep in the expm1 form
+    if (pass == 1) {
+      P.redo_pass = 1;
+      P.next_row = counters + 1;
+    }
+    st = (in->dtype == SAKI_BF16)
+             ? dispatch_couple<uint16_t>(P, route != nullptr, grad, route ? route->grad_dtype : 0, grid, hs)
+             : dispatch_couple<float>(P, route != nullptr, grad, route ? route->grad_dtype : 0, grid, hs);
+    if (st != SAKI_OK) return st;
+  }
   if (want_sum) {
     hipLaunchKernelGGL(saki::loss_sum_kernel, dim3(1), dim3(1024), 0, hs,
                        static_cast<const double*>(row_losses), in->n_rows, route->loss_sum);

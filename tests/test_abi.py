@@ -74,7 +74,7 @@ def test_argument_errors_without_launch(lib):
     # the row work counter needs a workspace on every call with rows
     assert _couple(lib, _rows()) == 6
     need = lib.saki_workspace_bytes(binding.SAKI_OP_COUPLE, 4, 64)
-    assert need == 256 + 256                                         # counter + 4 doubles, rounded
+    assert need == 256 + 256 + 256                                   # counters + 4 doubles + 4 indices, rounded
     assert _couple(lib, _rows(), ws=256, ws_bytes=need - 1) == 6
     assert _couple(lib, _rows(), ws=260, ws_bytes=need) == 5         # not 8-byte aligned
     assert _couple(lib, _rows(n_rows=1 << 31), ws=256, ws_bytes=1 << 40) == 2

@@ -623,3 +623,29 @@ def test_endpoint_small_kl(saki_lib, sigma):
     out, o, R = run_and_compare(saki_lib, s, t, 0.02, 404)
     assert np.all(o["lambda"] == 1.0)
     assert np.all(o["kl"] < 0.01)
+
+
+@pytest.mark.parametrize("D", [60.0, 70.0])
+def test_rows_resolved_again_in_the_expm1_forms(saki_lib, D):
+    """Rows whose TV is too small for the plain forms' rounding: five entries
+    share max p ~ 0.2, and one entry with p ~ 1e-23 carries the whole KL of
+    0.2 (t - s = D there), so TV ~ 0.0044 lies below 0.02 sqrt(max p): the
+    first launch lists these rows and the second resolves them with every
+    sweep in the expm1 form.  Every row against the oracle, with the gradient;
+    the oracle confirms that the rows meet that condition."""
+    rng = np.random.default_rng(int(D))
+    n, V = 16, 3000
+    s = np.full((n, V), -10.0) + rng.normal(0, 0.01, (n, V))
+    s[:, :5] = rng.normal(0, 0.01, (n, 5))
+    j = rng.integers(5, V, n)
+    s[np.arange(n), j] = -50.0
+    t = s.copy()
+    t[np.arange(n), j] += D
+    S = torch.as_tensor(s, dtype=torch.float32, device=DEV)
+    T = torch.as_tensor(t, dtype=torch.float32, device=DEV)
+    S, T = padded(S), padded(T)
+    b = bridge.bridge_rows(f64(S), f64(T), 0.2)
+    pmax = np.exp(b["logp"]).max(axis=1)
+    assert np.all(b["kl"] >= 0.1) and np.all(pmax < 0.25) and np.all(b["tv"] < 0.02 * np.sqrt(pmax))
+    out, o, R = run_and_compare(saki_lib, S, T, 0.2, 8080, row_offset=7)
+    _row_properties(o, 0.2)
