@@ -12,6 +12,8 @@ import os
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
@@ -22,7 +24,7 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
 # header of their own, which these kernels do not use).
 _CORE_SOURCES = ["include/saki.h", "paper_2609_36601_amd/csrc/saki.hip", "paper_2609_36601_amd/csrc/row_engine.hpp",
                  "paper_2609_36601_amd/csrc/device_util.hpp"]
-KERNEL_SOURCES = {"couple": _CORE_SOURCES, "route": _CORE_SOURCES,
+KERNEL_SOURCES = {"couple": _CORE_SOURCES, "route": _CORE_SOURCES, "verify": _CORE_SOURCES,
                   "probe": _CORE_SOURCES + ["paper_2609_36601_amd/csrc/probe.hpp"]}
 
 # HBM traffic of one launch of the dominant kernel, from two rocprofv3 --pmc
@@ -79,31 +81,89 @@ def _oracle_rows(args):
     return done, time.perf_counter() - t0
 
 
-def cpu_baseline(s, t, eps, seed, n_sample, workers, budget=20.0):
+def cpu_info():
+    """The host's CPU model (from /proc/cpuinfo), its logical CPUs and the
+    CPUs this process may run on."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except AttributeError:
+        affinity = os.cpu_count() or 1
+    return model, os.cpu_count() or 1, affinity
+
+
+def cpu_workers():
+    """Worker processes for the CPU baseline: every CPU this process may run
+    on, at most 16 (the CPU share of one GPU on the measuring machines)."""
+    return max(1, min(16, cpu_info()[2]))
+
+
+THREAD_VARS = ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS")
+
+
+def single_threaded_pool(n):
+    """A pool of n spawned worker processes whose numerical libraries start
+    single-threaded (the variables are set before the workers import numpy)."""
+    saved = {k: os.environ.get(k) for k in THREAD_VARS}
+    for k in THREAD_VARS:
+        os.environ[k] = "1"
+    try:
+        return mp.get_context("spawn").Pool(n)
+    finally:
+        for k, v in saved.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
+def _pool_rows(S, T, eps, seed, rows, workers, budget):
+    parts = [np.arange(w, len(rows), workers) for w in range(workers)]
+    jobs = [(S[p], T[p], eps, seed, rows[p], budget) for p in parts if len(p)]
+    with single_threaded_pool(len(jobs)) as pool:
+        pool.map(_noop, range(len(jobs)))  # start the workers before timing
+        t0 = time.perf_counter()
+        res = pool.map(_oracle_rows, jobs)
+        wall = time.perf_counter() - t0
+    return sum(r[0] for r in res), sum(r[1] for r in res), wall, len(jobs)
+
+
+def cpu_baseline(s, t, eps, seed, n_sample=512, budget=1.5, budget_single=6.0, n_full=None):
     """The float64 oracle (as it stands) on a bounded sample of the same rows:
-    each worker takes its share of n_sample evenly spaced rows in order and
-    stops after budget / workers seconds of work."""
-    import numpy as np
+    n_sample evenly spaced rows, split over one single-threaded worker process
+    per available CPU (at most 16), each stopping after `budget` seconds of
+    work; then one worker alone for `budget_single` seconds (the single-core
+    rate).  n_full: rows of the full configuration, for the extrapolated time
+    the oracle would take on all of them."""
     import torch
     n = s.shape[0]
     rows = np.linspace(0, n - 1, n_sample).astype(np.int64)
     idx = torch.as_tensor(rows, device=s.device)
     S = s[idx].float().cpu().numpy()
     T = t[idx].float().cpu().numpy()
-    parts = [np.arange(w, n_sample, workers) for w in range(workers)]
-    jobs = [(S[p], T[p], eps, seed, rows[p], budget / workers) for p in parts if len(p)]
-    ctx = mp.get_context("spawn")
-    with ctx.Pool(len(jobs)) as pool:
-        pool.map(_noop, range(len(jobs)))  # start the workers before timing
-        t0 = time.perf_counter()
-        res = pool.map(_oracle_rows, jobs)
-        wall = time.perf_counter() - t0
-    done = sum(r[0] for r in res)
-    busy = sum(r[1] for r in res)
-    return dict(value=done / wall, unit="positions/s", cores=len(jobs), kind="oracle",
+    workers = cpu_workers()
+    done, busy, wall, used = _pool_rows(S, T, eps, seed, rows, workers, budget)
+    done1, busy1, wall1, _ = _pool_rows(S, T, eps, seed, rows, 1, budget_single)
+    model, host_cpus, affinity = cpu_info()
+    value, single = done / wall, done1 / wall1
+    n_full = n_full or n
+    return dict(value=value, unit="positions/s", cores=used, kind="oracle",
                 sample=f"{done} rows of the same workload (from {n_sample} evenly spaced), coupling + "
-                       f"routed loss + gradient, {len(jobs)} single-threaded worker processes each "
-                       f"stopping after {budget / len(jobs):.2f} s; {busy:.1f} s of CPU work in {wall:.1f} s wall")
+                       f"routed loss + gradient, {used} single-threaded worker processes each stopping "
+                       f"after {budget:.2f} s ({busy:.1f} s of CPU work in {wall:.1f} s wall); then "
+                       f"{done1} rows on one core in {wall1:.1f} s",
+                cpu_model=model, host_cpus=host_cpus, affinity_cpus=affinity,
+                single_core_value=single,
+                full_config_rows=n_full,
+                full_config_oracle_s=n_full / value, full_config_oracle_s_single_core=n_full / single)
 
 
 def _noop(x):
@@ -143,9 +203,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--eps", type=float, default=0.2)
     ap.add_argument("--rows", type=int, default=None, help="override the row count (debug)")
-    ap.add_argument("--cpu-sample", type=int, default=256,
-                    help="rows offered to the CPU oracle (it stops after about 20 s of CPU work)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="time only the headline configuration (no other radii, verify or stream keys)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one 1 GiB device copy before timing (counter calibration)")
     ap.add_argument("--metadata", choices=("full", "objective"), default="objective",
@@ -204,23 +264,8 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    def step():
-        saki.saki_couple(s, t, args.eps, seed, 0, out, route, ws)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    stream = torch.cuda.current_stream()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    t_wall = time.perf_counter()
-    ev[0].record(stream)
-    for i in range(args.steps):
-        step()
-        ev[i + 1].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t_wall
-    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
-    ms = sum(per) / len(per)
+    ms, per, wall = time_calls(lambda: saki.saki_couple(s, t, args.eps, seed, 0, out, route, ws),
+                               args.steps, args.warmup)
     print(f"# per-step ms: {[round(x, 3) for x in per]} (wall {wall:.3f} s)", file=sys.stderr, flush=True)
 
     bytes_per_row = 2 * V * 2 + V * 4  # s + t read once (bf16), fp32 gradient written once
@@ -237,8 +282,35 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        workers = max(1, min(16, os.cpu_count() or 1))
-        cpu = cpu_baseline(s, t, args.eps, seed, args.cpu_sample, workers)
+        cpu = cpu_baseline(s, t, args.eps, seed, n_full=n)
+        print(f"# cpu baseline: {cpu}", file=sys.stderr, flush=True)
+
+    # the rest of the metric's configurations, in the same run: the large
+    # workload at the sweep's other radii, speculative verification and the
+    # long-rollout stress workload
+    others = {}
+    if not args.headline_only and n == cfg["rows"]:
+        steps_o = max(1, min(args.steps, 10))
+        for eps_o in cfg["eps"]:
+            if eps_o == args.eps:
+                continue
+            ms_o, per_o, _ = time_calls(lambda: saki.saki_couple(s, t, eps_o, seed, 0, out, route, ws),
+                                        steps_o, 1)
+            ach_o = n * bytes_per_row / (ms_o * 1e-3) / 1e9
+            others[f"large_eps{eps_o}"] = dict(
+                workload=f"large at eps {eps_o}: 65,536 rows, V=151,936 bf16, coupling + routed loss + fp32 grad",
+                value=n / (ms_o * 1e-3), unit="positions/s", ms_per_step=ms_o, steps=steps_o,
+                roofline=dict(bound="hbm", achieved=ach_o, peak=HBM_PEAK_GBS, unit="GB/s", frac=ach_o / HBM_PEAK_GBS),
+                stats=dict(correction_rate=float(out["corrected"].float().mean()),
+                           mean_tv=float(out["tv"].mean()), mean_lambda=float(out["lambda"].mean())))
+            print(f"# large eps {eps_o}: {ms_o:.3f} ms", file=sys.stderr, flush=True)
+        del out, route, ws
+        # the verify workload in the same (n, V) buffers
+        others["verify"] = verify_suite(saki, workloads, dev, s, t, steps_o, 1)
+        print(f"# verify: {others['verify']['ms_per_step']:.3f} ms", file=sys.stderr, flush=True)
+        # the long-rollout workload in the first 4,096 rows of the buffers
+        others["stream"] = stream_suite(saki, workloads, dev, s, t, grad, 1)
+        print(f"# stream: {others['stream']['ms_per_step']:.2f} ms", file=sys.stderr, flush=True)
 
     line = {
         "metric": "coupled+routed positions/sec at V=151,936 bf16; % of MI355X peak HBM GB/s",
@@ -262,8 +334,93 @@ def main():
                      "traffic": measured_traffic_bytes() if n == cfg["rows"] and args.eps == 0.2 else None},
         "cpu_baseline": cpu,
         "stats": {"correction_rate": corr_rate, "mean_tv": mean_tv, "mean_lambda": mean_lam},
+        "other_configs": others,
     }
     print(json.dumps(line), flush=True)
+
+
+def time_calls(call, steps, warmup):
+    """Times `call` (library calls enqueued on torch's current stream) with HIP
+    events: `warmup` untimed calls, then `steps` timed ones; returns the mean
+    ms, the per-call ms and the wall time of the timed calls."""
+    import torch
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    t_wall = time.perf_counter()
+    ev[0].record(stream)
+    for i in range(steps):
+        call()
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+    return sum(per) / len(per), per, wall
+
+
+def verify_suite(saki, workloads, dev, s, t, steps, warmup):
+    """The verify workload (8,192 blocks of k = 8, V = 151,936 bf16, eps 0.2,
+    accepted lengths and corrections only) generated into the buffers s, t."""
+    import torch
+    cfg = workloads.CONFIGS["verify"]
+    k, V = cfg["k"], cfg["V"]
+    n = s.shape[0] - s.shape[0] % k
+    nb = n // k
+    workloads.fill("verify", s[:n], t[:n])
+    draft = workloads.drafts(s[:n])
+    seed = workloads.coupling_seed("verify")
+    acc = torch.empty(nb, dtype=torch.int32, device=dev)
+    corr = torch.empty(nb, dtype=torch.int32, device=dev)
+    ws = torch.empty(max(saki.workspace_bytes(saki.SAKI_OP_VERIFY, n, V), 8), dtype=torch.uint8, device=dev)
+    ms, per, _ = time_calls(lambda: saki.saki_spec_verify(s[:n], t[:n], k, draft, 0.2, seed, 0, -1, acc, corr,
+                                                          None, ws), steps, warmup)
+    al = acc.cpu().numpy()
+    evaluated = int(np.minimum(al + 1, k).sum())  # positions each block reads before it stops
+    achieved = evaluated * 2 * V * 2 / (ms * 1e-3) / 1e9
+    return dict(workload="verify: 256 seq x 32 blocks x k=8 = 65,536 rows, V=151,936 bf16, rho~U(0.2,0.99) "
+                         "per block, drafts z~softmax(s), eps 0.2, accepted lengths and corrections",
+                value=nb / (ms * 1e-3), unit="blocks/s", ms_per_step=ms, steps=steps,
+                mean_accepted_length=float(al.mean()), positions_evaluated=evaluated,
+                roofline=dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
+                              frac=achieved / HBM_PEAK_GBS, traffic=measured_traffic_bytes("verify")))
+
+
+def stream_suite(saki, workloads, dev, s_buf, t_buf, grad_buf, warmup):
+    """The long-rollout stress workload: 262,144 rows of V = 151,936 bf16 in 64
+    chunks of 4,096 (row_offset = 4,096 x chunk, grad_scale = 1 / 262,144),
+    eps 0.02, coupling + routed loss + fp32 gradient; each chunk generated into
+    the first 4,096 rows of the buffers before its call; only the calls are
+    timed (HIP events), and summed."""
+    import torch
+    cfg = workloads.CONFIGS["stream"]
+    V, chunk, n_total = cfg["V"], cfg["chunk"], cfg["rows"]
+    s, t, grad = s_buf[:chunk], t_buf[:chunk], grad_buf[:chunk]
+    eps, seed = 0.02, workloads.coupling_seed("stream")
+    out = saki.alloc_couple_out(chunk, dev)
+    route = dict(valid_mask=None, grad_scale=1.0 / n_total,
+                 row_loss=torch.empty(chunk, dtype=torch.float32, device=dev),
+                 loss_sum=torch.empty(1, dtype=torch.float64, device=dev), grad=grad)
+    ws = torch.empty(max(saki.workspace_bytes(saki.SAKI_OP_COUPLE, chunk, V), 8), dtype=torch.uint8, device=dev)
+    total_ms, corr, tv = 0.0, 0.0, 0.0
+    for c in range(n_total // chunk):
+        lo = c * chunk
+        workloads.fill("stream", s, t, lo=lo)
+        torch.cuda.synchronize()
+        call = lambda: saki.saki_couple(s, t, eps, seed, lo, out, route, ws)  # noqa: E731
+        ms, _, _ = time_calls(call, 1, warmup if c == 0 else 0)
+        total_ms += ms
+        corr += float(out["corrected"].float().sum())
+        tv += float(out["tv"].double().sum())
+    achieved = n_total * (2 * V * 2 + V * 4) / (total_ms * 1e-3) / 1e9
+    return dict(workload="stream: 32 seq x 8192 pos = 262,144 rows in 64 chunks of 4,096, V=151,936 bf16, "
+                         "peaked rows, eps 0.02, coupling + routed loss + fp32 grad",
+                value=n_total / (total_ms * 1e-3), unit="positions/s", ms_per_step=total_ms,
+                chunks=n_total // chunk,
+                roofline=dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
+                              frac=achieved / HBM_PEAK_GBS),
+                stats=dict(correction_rate=corr / n_total, mean_tv=tv / n_total))
 
 
 def _oracle_blocks(args):
@@ -327,21 +484,20 @@ def bench_verify(args, saki, workloads, dev):
     attainable = attainable_read_gbs(dev)
     cpu = None
     if not args.no_cpu_baseline:
-        n_sample = max(1, args.cpu_sample // k)
+        n_sample = 32
         blocks = np.linspace(0, nb - 1, n_sample).astype(np.int64)
         idx = torch.as_tensor(np.concatenate([np.arange(b * k, (b + 1) * k) for b in blocks]), device=dev)
         S = s[idx].float().cpu().numpy().astype(np.float64)
         T = t[idx].float().cpu().numpy().astype(np.float64)
         D = draft[idx].cpu().numpy()
-        workers = max(1, min(16, os.cpu_count() or 1))
+        workers = cpu_workers()
         budget = 20.0
         parts = [np.arange(w, n_sample, workers) for w in range(workers)]
         jobs = [(np.concatenate([S[b * k:(b + 1) * k] for b in p]), np.concatenate([T[b * k:(b + 1) * k] for b in p]),
                  np.concatenate([D[b * k:(b + 1) * k] for b in p]), k, args.eps, seed, blocks[p] * k,
                  budget / workers)
                 for p in parts if len(p)]
-        ctx = mp.get_context("spawn")
-        with ctx.Pool(len(jobs)) as pool:
+        with single_threaded_pool(len(jobs)) as pool:
             pool.map(_noop, range(len(jobs)))
             t0 = time.perf_counter()
             res = pool.map(_oracle_blocks, jobs)
@@ -571,7 +727,7 @@ def bench_rollout(args, saki, workloads, dev):
     if not args.no_cpu_baseline:
         # the oracle on a bounded sample of the same workload: 2 sequences x 8 tokens
         job = (2, k, 8, V, eps, R["seed"], R["model_seed"])
-        with mp.get_context("spawn").Pool(1) as pool:
+        with single_threaded_pool(1) as pool:
             pool.map(_noop, range(1))
             t0 = time.perf_counter()
             busy, ntok = pool.map(_oracle_rollout, [job])[0]

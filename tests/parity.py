@@ -247,16 +247,28 @@ def _verify_job(args):
     return compare_verify(gpu, s, t, k, draft, eps, seed, row_offset, blocks, eos_id)
 
 
+THREAD_VARS = ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS")
+
+
 def _pool_map(fn, jobs):
     if len(jobs) == 1:
         return [fn(jobs[0])]
-    # spawned workers: the parent has a GPU context, which must not be forked
-    with mp.get_context("spawn").Pool(len(jobs), initializer=_single_thread) as pool:
+    # spawned workers (the parent has a GPU context, which must not be
+    # forked), whose numerical libraries start single-threaded: the variables
+    # are set before the workers import numpy
+    saved = {k: os.environ.get(k) for k in THREAD_VARS}
+    for k in THREAD_VARS:
+        os.environ[k] = "1"
+    try:
+        pool = mp.get_context("spawn").Pool(len(jobs))
+    finally:
+        for k, v in saved.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+    with pool:
         return pool.map(fn, jobs)
-
-
-def _single_thread():
-    os.environ["OMP_NUM_THREADS"] = "1"
 
 
 def compare_couple_pool(gpu, s, t, eps, seed, row_offset, rows, grad=None, valid=None,
