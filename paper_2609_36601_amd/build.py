@@ -14,6 +14,12 @@ HIPCC_FLAGS = [
     "-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-shared",
     # no packed FP32 instructions (v_pk_*_f32) in any kernel
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # no machine-level hoisting of loop invariants: in the persistent kernels it
+    # lifts the double constants of the per-row serial math (log / exp
+    # coefficients) out of the row loop, where they stay live across the
+    # sweeps and are spilled to scratch, then reloaded at memory latency in the
+    # serial steps of every row
+    "-mllvm", "-disable-machine-licm",
 ]
 
 

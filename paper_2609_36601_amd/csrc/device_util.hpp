@@ -20,6 +20,20 @@ constexpr double LN2_D = 0.6931471805599453094;
 __device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float flog2(float x) { return __builtin_amdgcn_logf(x); }
 __device__ __forceinline__ float finf() { return __builtin_huge_valf(); }
+// Three-input maximum / minimum (v_max3_f32 / v_min3_f32) applied to the
+// operands as they are: fmaxf on values unpacked from bf16 bits first quiets
+// each operand (one more instruction per entry), which a row statistic does
+// not need (a NaN entry makes the row non-finite either way).
+__device__ __forceinline__ float max3_raw(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+__device__ __forceinline__ float min3_raw(float a, float b, float c) {
+  float r;
+  asm("v_min3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
 
 // ---------------------------------------------------------------------------
 // Row element layout inside a chunk.  Lane l of the wave that owns chunk c

@@ -20,7 +20,19 @@
 
 namespace saki {
 
-constexpr int RED_MAX = 12;  // widest block reduction (doubles per thread)
+constexpr int RED_MAX = 16;  // widest block reduction (doubles per thread)
+
+// The stats sweep also evaluates A and its first two derivatives at a middle
+// lambda (the weights p^(1 - lam) pi^lam), so that the start of the lambda
+// search interpolates A between lambda = 0, that node and 1 instead of
+// extrapolating from the ends.  The node sits near where lambda* falls for the
+// radius (lambda* ~ sqrt(2 eps / Var_p[d]), Var_p[d] of a few units).
+__host__ __device__ inline float mid_lambda(double eps) {
+  const double l = 0.5 * sqrt(eps > 0.0 ? eps : 0.0);
+  return static_cast<float>(l < 0.05 ? 0.05 : l > 0.5 ? 0.5 : l);
+}
+
+
 
 // Row-uniform results of the stats sweep.
 struct RowStats {
@@ -40,6 +52,8 @@ struct RowStats {
   int vstar;           // argmax t, lowest index on ties
   float t_smax;        // t at an entry holding max s (the dominant entry of p)
   double pmax;         // max_v p_v = exp(ms - lse_s)
+  float lam_mid;       // the middle node (mid_lambda)
+  double mid_A, mid_A1, mid_A2;  // A, A', A'' there
   bool finite;
 };
 
@@ -373,14 +387,17 @@ struct StatsAcc {
   double Ss, St;                // per-lane sums of 2^(s log2 e - MsL), 2^(t log2 e - MtL)
   float S1, S2, S3, S4;         // per-lane p-weighted powers of d (relative to Ms)
   float T1, T2;                 // per-lane pi-weighted sums of d, d^2 (relative to Mt)
+  double Sm;                    // per-lane sum of 2^((1 - lm) as + lm at), lm the middle node
+  float Q1, Q2;                 // per-lane d, d^2 under those weights
   int tidx;                     // wave-uniform lowest index of the running max of t
   float t_smax;                 // wave-uniform: t at an entry holding the running max of s
   float dmin, dmax;             // per-lane range of d
   __device__ void init() {
     Ms = -finf(); Mt = -finf();
     MsL = -finf(); MtL = -finf();
-    Ss = St = 0.0;
+    Ss = St = Sm = 0.0;
     S1 = S2 = S3 = S4 = T1 = T2 = 0.f;
+    Q1 = Q2 = 0.f;
     tidx = 0x7fffffff;
     t_smax = 0.f;
     dmin = finf(); dmax = -finf();
@@ -398,17 +415,32 @@ struct StatsAcc {
 // (MsL, sum_c 2^(s log2 e - MsL)), i.e. ln W_c = MsL ln 2 + ln(sum).
 template <bool TAIL, typename SH>
 __device__ __forceinline__ void stats_math(const float* s, const float* t, uint32_t vm, int c,
-                                           int lane, bool keep_chunks, bool keep_teacher, SH& sh,
+                                           int lane, bool keep_chunks, bool keep_teacher, float lm, SH& sh,
                                            StatsAcc& a) {
-  float ls = -finf(), lt = -finf(), lmin = finf(), lmax = -finf();
+  // this lane's maxima and range of d over the chunk: chains of three-input
+  // max / min (EPL - 1 entries after the first, two per instruction)
+  float ls, lt, lmin, lmax;
+  {
+    float ms[EPL], mt[EPL], dn[EPL], dx[EPL];
 #pragma unroll
-  for (int e = 0; e < EPL; ++e) {
-    if (SAKI_VALID(e)) {
+    for (int e = 0; e < EPL; ++e) {
+      const bool ok = SAKI_VALID(e);
       const float d = t[e] - s[e];
-      ls = fmaxf(ls, s[e]);
-      lt = fmaxf(lt, t[e]);
-      lmin = fminf(lmin, d);
-      lmax = fmaxf(lmax, d);
+      ms[e] = ok ? s[e] : -finf();
+      mt[e] = ok ? t[e] : -finf();
+      dn[e] = ok ? d : finf();
+      dx[e] = ok ? d : -finf();
+    }
+    static_assert(EPL % 2 == 0, "pairs of entries per max3");
+    ls = ms[0]; lt = mt[0]; lmin = dn[0]; lmax = dx[0];
+    // entry 0 twice in the first step keeps the chain at EPL / 2 instructions
+#pragma unroll
+    for (int e = 1; e < EPL; e += 2) {
+      const int f = e + 1 < EPL ? e + 1 : e;
+      ls = max3_raw(ls, ms[e], ms[f]);
+      lt = max3_raw(lt, mt[e], mt[f]);
+      lmin = min3_raw(lmin, dn[e], dn[f]);
+      lmax = max3_raw(lmax, dx[e], dx[f]);
     }
   }
   a.dmin = fminf(a.dmin, lmin);
@@ -416,17 +448,21 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
   if (wave_any(ls > a.Ms)) {
     const float cms = wave_max(ls);
     // a new running maximum of s: the largest t among the entries holding it
-    float lt = -finf();
+    float lt2 = -finf();
 #pragma unroll
     for (int e = 0; e < EPL; ++e)
-      if (SAKI_VALID(e) && s[e] == cms) lt = fmaxf(lt, t[e]);
-    a.t_smax = wave_max(lt);
+      if (SAKI_VALID(e) && s[e] == cms) lt2 = fmaxf(lt2, t[e]);
+    a.t_smax = wave_max(lt2);
     // rounded product and difference, never contracted into one fma: the sums
     // so far are relative to exactly the MsL the later terms use
     const float cmsL = __fmul_rn(cms, LOG2E);
-    const float f = fexp2(__fsub_rn(a.MsL, cmsL));
+    const float dsl = __fsub_rn(a.MsL, cmsL);
+    const float f = fexp2(dsl);
     a.Ss *= static_cast<double>(f);
     a.S1 *= f; a.S2 *= f; a.S3 *= f; a.S4 *= f;
+    const float fm = fexp2((1.0f - lm) * dsl);
+    a.Sm *= static_cast<double>(fm);
+    a.Q1 *= fm; a.Q2 *= fm;
     a.Ms = cms;
     a.MsL = cmsL;
   }
@@ -439,40 +475,53 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
       if (SAKI_VALID(e) && t[e] == cmt) li = c * CHUNK + elem_offset(lane, e);
     a.tidx = wave_min(li);
     const float cmtL = __fmul_rn(cmt, LOG2E);
-    const float f = fexp2(__fsub_rn(a.MtL, cmtL));
+    const float dtl = __fsub_rn(a.MtL, cmtL);
+    const float f = fexp2(dtl);
     a.St *= static_cast<double>(f);
     a.T1 *= f;
     a.T2 *= f;
+    const float fm = fexp2(lm * dtl);
+    a.Sm *= static_cast<double>(fm);
+    a.Q1 *= fm; a.Q2 *= fm;
     a.Mt = cmt;
     a.MtL = cmtL;
   }
-  // normalisers: float sums of four entries (within three roundings each),
-  // then double
-  double ps = 0.0, pt = 0.0;
-  float gs = 0.f, gt = 0.f, p1 = 0.f, p2 = 0.f, p3 = 0.f, p4 = 0.f, t1 = 0.f, t2 = 0.f;
+  // normalisers: float sums of eight entries (within seven roundings each),
+  // then double; moments in float
+  double ps = 0.0, pt = 0.0, pm = 0.0;
+  float gs = 0.f, gt = 0.f, gm = 0.f, p1 = 0.f, p2 = 0.f, p3 = 0.f, p4 = 0.f, t1 = 0.f, t2 = 0.f;
+  float q1 = 0.f, q2 = 0.f;
 #pragma unroll
   for (int e = 0; e < EPL; ++e) {
-    float es = fexp2(fmaf(s[e], LOG2E, -a.MsL));
-    float et = fexp2(fmaf(t[e], LOG2E, -a.MtL));
-    if (TAIL && !SAKI_VALID(e)) { es = 0.f; et = 0.f; }
+    const float as = fmaf(s[e], LOG2E, -a.MsL);
+    const float at = fmaf(t[e], LOG2E, -a.MtL);
+    float es = fexp2(as);
+    float et = fexp2(at);
+    // the middle node's weight p~^(1 - lm) pi~^lm: its exponent is at most 0
+    // (as, at <= 0), so it cannot overflow
+    float em = fexp2(fmaf(lm, at - as, as));
+    if (TAIL && !SAKI_VALID(e)) { es = 0.f; et = 0.f; em = 0.f; }
     const float d = t[e] - s[e];
-    const float ed = es * d;
-    const float ed2 = ed * d;
-    const float ed3 = ed2 * d;
-    p1 += ed;
-    p2 += ed2;
-    p3 += ed3;
-    p4 = fmaf(ed3, d, p4);
-    const float etd = et * d;
-    t1 += etd;
-    t2 = fmaf(etd, d, t2);
+    const float d2 = d * d;
+    p1 = fmaf(es, d, p1);
+    p2 = fmaf(es, d2, p2);
+    const float ed2 = es * d2;
+    p3 = fmaf(ed2, d, p3);
+    p4 = fmaf(ed2, d2, p4);
+    t1 = fmaf(et, d, t1);
+    t2 = fmaf(et, d2, t2);
+    q1 = fmaf(em, d, q1);
+    q2 = fmaf(em, d2, q2);
     gs += es;
     gt += et;
-    if ((e & 3) == 3) {
+    gm += em;
+    if ((e & 7) == 7) {
       ps += static_cast<double>(gs);
       pt += static_cast<double>(gt);
+      pm += static_cast<double>(gm);
       gs = 0.f;
       gt = 0.f;
+      gm = 0.f;
     }
   }
   if (keep_chunks) {
@@ -497,12 +546,17 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
   a.St += pt;
   a.T1 += t1;
   a.T2 += t2;
+  a.Sm += pm;
+  a.Q1 += q1;
+  a.Q2 += q2;
 }
 
 // The block's maxima, rescaled sums, argmax and range of d.
 struct StatsBlock {
   float ms, mt;
   double Ss, S1, S2, S3, S4, St, T1, T2;
+  double Sm, Q1, Q2;  // middle-node sums (relative to the row's maxima)
+  float lm;           // the middle node
   float tbest;
   int tidx;
   float t_smax;
@@ -510,15 +564,15 @@ struct StatsBlock {
 };
 
 // One exchange through LDS: each wave posts its sums (relative to its own
-// running maxima), maxima, argmax and range of d; every thread then combines
-// the waves in the same fixed order, so all threads hold the same bits.
+// running maxima), maxima, argmax and range of d (stats_post); after a
+// barrier one thread combines the waves in a fixed order (stats_combine).
 template <int NT, typename SH>
-__device__ StatsBlock stats_combine_block(Block<NT, SH>& B, StatsAcc& a) {
-  constexpr int NW = NT / WAVE;
-  double v[8] = {a.Ss, static_cast<double>(a.S1), static_cast<double>(a.S2), static_cast<double>(a.S3),
-                 static_cast<double>(a.S4), a.St, static_cast<double>(a.T1), static_cast<double>(a.T2)};
+__device__ void stats_post(Block<NT, SH>& B, StatsAcc& a) {
+  double v[11] = {a.Ss, static_cast<double>(a.S1), static_cast<double>(a.S2), static_cast<double>(a.S3),
+                  static_cast<double>(a.S4), a.St, static_cast<double>(a.T1), static_cast<double>(a.T2),
+                  a.Sm, static_cast<double>(a.Q1), static_cast<double>(a.Q2)};
 #pragma unroll
-  for (int i = 0; i < 8; ++i) v[i] = wave_sum(v[i]);
+  for (int i = 0; i < 11; ++i) v[i] = wave_sum(v[i]);
   const float wdmin = -wave_max(-a.dmin);
   const float wdmax = wave_max(a.dmax);
   if (B.lane == 0) {
@@ -532,8 +586,14 @@ __device__ StatsBlock stats_combine_block(Block<NT, SH>& B, StatsAcc& a) {
     B.sh.red_f[B.wave][3] = wdmax;
     B.sh.red_i[B.wave][0] = a.tidx;
     B.sh.red_d[B.wave][10] = static_cast<double>(a.t_smax);
+#pragma unroll
+    for (int i = 0; i < 3; ++i) B.sh.red_d[B.wave][11 + i] = v[8 + i];
   }
-  __syncthreads();
+}
+
+template <int NT, typename SH>
+__device__ StatsBlock stats_combine(Block<NT, SH>& B, float lm) {
+  constexpr int NW = NT / WAVE;
   StatsBlock O;
   O.ms = -finf();
   O.mt = -finf();
@@ -545,7 +605,7 @@ __device__ StatsBlock stats_combine_block(Block<NT, SH>& B, StatsAcc& a) {
     O.dmin = fminf(O.dmin, B.sh.red_f[w][2]);
     O.dmax = fmaxf(O.dmax, B.sh.red_f[w][3]);
   }
-  double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  double acc[11] = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
   float tb = -finf();
   int ti = 0x7fffffff;
   float st = -finf();
@@ -562,11 +622,16 @@ __device__ StatsBlock stats_combine_block(Block<NT, SH>& B, StatsAcc& a) {
     for (int i = 0; i < 5; ++i) acc[i] += B.sh.red_d[w][i] * gs;
 #pragma unroll
     for (int i = 5; i < 8; ++i) acc[i] += B.sh.red_d[w][i] * gt;
+    // the middle node's sums are relative to 2^((1 - lm) wMsL + lm wMtL)
+    const double gm = (wMs == -finf() || wMt == -finf()) ? 0.0 :
+        exp2(static_cast<double>(1.0f - lm) * (static_cast<double>(wMsL) - static_cast<double>(msL)) +
+             static_cast<double>(lm) * (static_cast<double>(wMtL) - static_cast<double>(mtL)));
+#pragma unroll
+    for (int i = 0; i < 3; ++i) acc[8 + i] += B.sh.red_d[w][11 + i] * gm;
     const int wi = B.sh.red_i[w][0];
     if (wMt > tb || (wMt == tb && wi < ti)) { tb = wMt; ti = wi; }
     if (wMs == O.ms) st = fmaxf(st, static_cast<float>(B.sh.red_d[w][10]));
   }
-  __syncthreads();
   const double cs = shift_correction(O.ms, msL), ct = shift_correction(O.mt, mtL);
   // The maximum's own term went into the sums as 2^d0 rounded to float (d0 =
   // the rounding of the shift, ~1e-6: a rounding of ~6e-8 next to 1); after
@@ -576,6 +641,10 @@ __device__ StatsBlock stats_combine_block(Block<NT, SH>& B, StatsAcc& a) {
   const double dom_t = 1.0 - static_cast<double>(fexp2(fmaf(O.mt, LOG2E, -mtL))) * ct;
   O.Ss = acc[0] * cs + dom_s; O.S1 = acc[1] * cs; O.S2 = acc[2] * cs; O.S3 = acc[3] * cs; O.S4 = acc[4] * cs;
   O.St = acc[5] * ct + dom_t; O.T1 = acc[6] * ct; O.T2 = acc[7] * ct;
+  // the middle node's weights carry cs^(1 - lm) ct^lm likewise
+  const double cm = exp2(static_cast<double>(1.0f - lm) * log2(cs) + static_cast<double>(lm) * log2(ct));
+  O.Sm = acc[8] * cm; O.Q1 = acc[9] * cm; O.Q2 = acc[10] * cm;
+  O.lm = lm;
   O.tbest = tb;
   O.tidx = ti;
   O.t_smax = st;
@@ -607,6 +676,18 @@ __device__ inline RowStats row_stats_from(const StatsBlock& O) {
   R.c = static_cast<float>(Ed);
   if (!isfinite(R.c)) R.c = 0.0f;
   R.cL = R.c * LOG2E;
+  // A at the middle node lm: sum_v p_v e^{lm x_v} = e^{lm (mt - ms - c)}
+  // sum_m / sum_s, with sum_m = sum e^{(1 - lm)(s - ms) + lm (t - mt)}; its
+  // derivatives are the mean and variance of x under the tilted weights
+  {
+    const double lm = static_cast<double>(O.lm);
+    const double M1 = O.Q1 / O.Sm, M2 = O.Q2 / O.Sm;
+    R.lam_mid = O.lm;
+    R.mid_A = lm * (static_cast<double>(R.mt) - static_cast<double>(R.ms) - static_cast<double>(R.c)) +
+              log(O.Sm) - log(O.Ss);
+    R.mid_A1 = M1 - static_cast<double>(R.c);
+    R.mid_A2 = fmax(M2 - M1 * M1, 0.0);
+  }
   R.finite = isfinite(R.lse_s) && isfinite(R.lse_t) && isfinite(R.dmin) && isfinite(R.dmax) &&
              isfinite(R.ms) && isfinite(R.mt);
   return R;
@@ -617,18 +698,19 @@ __device__ inline RowStats row_stats_from(const StatsBlock& O) {
 // caller reads its fields there where it needs them rather than holding the
 // whole record in registers across the later sweeps.
 template <typename T, int NT, typename SH>
-__device__ const RowStats& stats_sweep(Block<NT, SH>& B, const T* srow, const T* trow, int V, bool keep_chunks,
-                                       bool keep_teacher = false) {
+__device__ const RowStats& stats_sweep(Block<NT, SH>& B, const T* srow, const T* trow, int V, float lm,
+                                       bool keep_chunks, bool keep_teacher = false) {
   constexpr int NW = NT / WAVE;
   StatsAcc a;
   a.init();
   for_chunks<T, NW, false, fill_mode<T, SH>()>(srow, trow, V, B.wave, B.lane,
                     [&](auto tail, const float* s, const float* t, uint32_t vm, int c) {
                       constexpr bool TAIL = decltype(tail)::value;
-                      stats_math<TAIL>(s, t, vm, c, B.lane, keep_chunks, keep_teacher, B.sh, a);
+                      stats_math<TAIL>(s, t, vm, c, B.lane, keep_chunks, keep_teacher, lm, B.sh, a);
                     }, row_cache<T>(B.sh));
-  const StatsBlock O = stats_combine_block(B, a);
-  if (B.tid == 0) B.sh.rs.r = row_stats_from(O);
+  stats_post(B, a);
+  __syncthreads();
+  if (B.tid == 0) B.sh.rs.r = row_stats_from(stats_combine(B, lm));
   __syncthreads();
   return B.sh.rs.r;
 }
@@ -678,6 +760,10 @@ __device__ __forceinline__ float expm1_sel(float y, float e) {
 // A(lam) and its derivatives (natural units), and KL = lam A' - A.
 struct LamEval {
   double lam, A, A1, A2, A3, A4, KL;
+  // a root of the node's Taylor model is accepted only within this relative
+  // distance of the node (a node whose A4 is a bound rather than a sum
+  // limits it)
+  double reach;
 };
 
 
@@ -757,6 +843,7 @@ __device__ inline LamEval lam_finish(const double (&v)[5], double b0, float lam,
   E.A3 = c3 * l2 * l1;
   E.A4 = c4 * l2 * l2;
   E.KL = fmax(E.lam * E.A1 - E.A, 0.0);  // non-negative; rounding can give -1e-16 when p ~ pi
+  E.reach = __builtin_huge_val();
   return E;
 }
 
@@ -842,6 +929,7 @@ struct LamResult {
   float cL;    // c log2(e) as used in X = fma(d, log2 e, -cL)
   bool qp;     // q = p exactly (eps = 0, or t - s constant): the sweeps use lambda 0
   bool acc;    // A and KL come from a sweep in the expm1 form
+  int sweeps;  // lambda sweeps the search ran
   // x of one entry exactly as the sweeps see it: X ln 2, X = fma(d, log2 e, -cL)
   __device__ double x_of(float s, float t) const {
     return (static_cast<double>(LOG2E) * (static_cast<double>(t) - static_cast<double>(s)) -
@@ -916,13 +1004,116 @@ __device__ inline double two_ended_start(const RowStats& R, double eps) {
     return v * l;
   };
   if (!(kl(1.0) > eps)) return -1.0;
-  // 2^-24 resolution: far below the error of the model itself (~1e-3)
+  // 2^-14 resolution: below the error of the model itself (~1e-3)
   double lo = 0.0, hi = 1.0;
-  for (int it = 0; it < 24; ++it) {
+  for (int it = 0; it < 14; ++it) {
     const double m = 0.5 * (lo + hi);
     if (kl(m) <= eps) lo = m; else hi = m;
   }
   return lo;
+}
+
+// Interpolating start: the polynomial of degree 10 that matches A and its
+// first four derivatives at lambda = 0 (the cumulants of x under p), A, A',
+// A'' at the middle node, and A, A', A'' at lambda = 1 (the teacher end), in
+// Newton form over the confluent nodes.  On rows whose A is smooth on [0, 1] it places
+// lambda* to ~1e-6 or better, where the ends alone (two_ended_start) leave
+// ~1e-3; on spiky rows it can be far off, which the caller detects.
+struct HermiteA {
+  static constexpr int N = 11;
+  double z[N], c[N];
+  __device__ explicit HermiteA(const RowStats& R) {
+    const double lm = static_cast<double>(R.lam_mid);
+    const double f0[5] = {0.0, R.mean_p - R.c, R.var, R.k3, R.k4};
+    const double fm[3] = {R.mid_A, R.mid_A1, R.mid_A2};
+    const double f1[3] = {R.lse_t - R.lse_s - R.c, R.mean_pi - R.c, R.var_pi};
+    const double inv_fact[5] = {1.0, 1.0, 0.5, 1.0 / 6.0, 1.0 / 24.0};
+    auto deriv = [&](int i, int j) { return i < 5 ? f0[j] : i < 8 ? fm[j] : f1[j]; };
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      z[i] = i < 5 ? 0.0 : i < 8 ? lm : 1.0;
+      c[i] = deriv(i, 0);
+    }
+    // divided differences in place: after step j, c[i] = f[z_{i-j} .. z_i]
+    // (a repeated node takes the derivative / j! there); the spans z_i - z_{i-j}
+    // are lm, 1 - lm or 1, so three reciprocals serve every step
+    const double r_lm = 1.0 / lm, r_rest = 1.0 / (1.0 - lm);
+    // fully unrolled: constant indices keep the tables in registers
+#pragma unroll
+    for (int j = 1; j < N; ++j)
+#pragma unroll
+      for (int i = N - 1; i >= j; --i) {
+        const double span = z[i] - z[i - j];
+        const double rs = span == 1.0 ? 1.0 : span == lm ? r_lm : r_rest;
+        c[i] = (span == 0.0) ? deriv(i, j) * inv_fact[j] : (c[i] - c[i - 1]) * rs;
+      }
+  }
+  // the polynomial and its first two derivatives at l
+  __device__ void eval(double l, double& p, double& p1, double& p2) const {
+    p = c[N - 1];
+    p1 = 0.0;
+    p2 = 0.0;
+#pragma unroll
+    for (int k = N - 2; k >= 0; --k) {
+      const double dz = l - z[k];
+      p2 = p2 * dz + 2.0 * p1;
+      p1 = p1 * dz + p;
+      p = p * dz + c[k];
+    }
+  }
+
+};
+
+// Where lambda* starts, and A there.
+struct StartPoint {
+  double lam;  // the first node
+  double A;    // A(lam) predicted by the interpolant (herm only)
+  bool herm;   // lam solves KL = eps on the interpolant, within 30% of the end starts
+};
+
+constexpr double LAM_MAX = 1.0 - 1e-6;
+
+__device__ inline StartPoint start_point(const RowStats& R, double eps) {
+  const double l_cum = cumulant_start(R, eps);
+  const double l_two = two_ended_start(R, eps);
+  double l0 = (l_two > 0.0 && fabs(l_two - l_cum) <= 0.3 * l_cum) ? l_two : l_cum;
+  l0 = fmin(fmax(l0, 1e-7), LAM_MAX);
+  StartPoint S;
+  S.lam = l0;
+  S.A = 0.0;
+  S.herm = false;
+  const HermiteA H(R);
+  double p, p1, p2;
+  H.eval(1.0, p, p1, p2);
+  if (!(p1 - p > eps)) return S;  // the interpolant puts lambda* at 1
+  // safeguarded Newton on KL(l) = l A'(l) - A(l) = eps (KL' = l A''),
+  // keeping the bracket KL(lo) <= eps < KL(hi)
+  // (converged once the step is below 1e-10 of lambda: the interpolant's own
+  // rounding, ~1e-12 of lambda near the root, would otherwise send a
+  // tighter test into the bisection branch)
+  double lo = 0.0, hi = 1.0, l = l0;
+  bool conv = false;
+  for (int it = 0; it < 10; ++it) {
+    H.eval(l, p, p1, p2);
+    const double f = l * p1 - p - eps;
+    if (f <= 0.0) lo = l; else hi = l;
+    const double fp = l * p2;
+    const double step = (fp > 0.0) ? -f / fp : __builtin_huge_val();
+    if (fabs(step) <= 1e-10 * l || hi - lo <= 1e-8 * l) {
+      conv = true;
+      break;
+    }
+    double nl = l + step;
+    if (!(nl > lo && nl < hi)) nl = 0.5 * (lo + hi);
+    l = nl;
+  }
+  if (!conv || !(fabs(l - l0) <= 0.3 * l0) || !(l < LAM_MAX)) return S;
+  H.eval(l, p, p1, p2);
+  if (!(p2 > 0.0) || !isfinite(p)) return S;
+  S.lam = l;
+  S.A = p;
+  S.herm = true;
+  return S;
 }
 
 // Largest lambda in [0, 1] with KL(q_lambda || p) <= eps (Eq. trust_region).
@@ -934,12 +1125,19 @@ __device__ inline double two_ended_start(const RowStats& R, double eps) {
 // otherwise the next node is that root (or the edge of the trust interval).
 // sweep1(lam, acc) evaluates one node over the whole row.
 // force_acc: every sweep in the expm1 form; lam_hint > 0: the first node (a
-// lambda* found before, resolved again in the accurate form).
+// lambda* found before, resolved again in the accurate form); first: the
+// first node already evaluated (by the fused sweep, at first->lam; in the
+// expm1 form if first_acc), used in place of the first sweep.  out.sweeps
+// counts the sweeps run here.
+// no_sweep: stop where a sweep would be needed (out.sweeps = -1), so that one
+// wave can settle the common case of an accepted first node alone.
 template <typename Sweep1>
 __device__ LamResult lambda_search_with(const RowStats& R, double eps, Sweep1&& sweep1, bool force_acc = false,
-                                        float lam_hint = 0.0f) {
+                                        float lam_hint = 0.0f, const LamEval* first = nullptr,
+                                        bool first_acc = false, bool no_sweep = false) {
   LamResult out;
   out.acc = true;
+  out.sweeps = 0;
   if (R.dmin == R.dmax) {
     // t - s constant: p = pi, KL = 0 for every lambda, lambda* = 1, q = p
     out.lam = 1.0f; out.A = 0.0; out.KL = 0.0; out.c = R.dmin; out.cL = R.dmin * LOG2E; out.qp = true;
@@ -955,22 +1153,23 @@ __device__ LamResult lambda_search_with(const RowStats& R, double eps, Sweep1&& 
   // A KL below KL_ACCURATE is resolved with the expm1 form of the sweep: the
   // plain form carries ~2^-24 absolute error per weight, too much next to a
   // KL of that size.
-  bool acc = force_acc || eps < KL_ACCURATE;
+  bool acc = force_acc || eps < KL_ACCURATE || (first != nullptr && first_acc);
   out.acc = acc;
   constexpr double TAYLOR_TOL = 1e-7;
   constexpr double TRUST = 0.3;
-  constexpr double LMAX = 1.0 - 1e-6;
+  constexpr double LMAX = LAM_MAX;
   double lo = 0.0, hi = 1.0;  // KL(lo) <= eps < KL(hi) (hi = 1 until a node above is seen)
   LamEval feas;               // the largest evaluated lambda that is feasible (lambda = 0 is)
   feas.lam = 0.0; feas.A = 0.0; feas.KL = 0.0;
-  const double l_cum = cumulant_start(R, eps);
-  const double l_two = two_ended_start(R, eps);
-  double lg = (l_two > 0.0 && fabs(l_two - l_cum) <= 0.3 * l_cum) ? l_two : l_cum;
-  lg = fmin(fmax(lg, 1e-7), LMAX);
+  double lg = (first == nullptr && !(lam_hint > 0.0f)) ? start_point(R, eps).lam : 0.0;
   bool try_one = R.kl1_est <= 1.05 * eps + 1e-5;
   if (lam_hint > 0.0f) {
     lg = lam_hint;
     try_one = lam_hint == 1.0f;
+  }
+  if (first != nullptr) {
+    lg = first->lam;
+    try_one = false;
   }
   // The first TRUST_SWEEPS sweeps step within TRUST of the node.  A row still
   // unresolved after them (a KL that rises steeply, e.g. a few entries with
@@ -982,7 +1181,13 @@ __device__ LamResult lambda_search_with(const RowStats& R, double eps, Sweep1&& 
   double step1 = 2.0, step2 = 2.0;  // the last two node steps (safeguard)
   for (int sweep = 0; sweep < MAX_SWEEPS; ++sweep) {
     const float lf = try_one ? 1.0f : static_cast<float>(lg);
-    const LamEval E = sweep1(lf, acc);
+    const bool given = sweep == 0 && first != nullptr;
+    if (!given && no_sweep) {
+      out.sweeps = -1;
+      return out;
+    }
+    const LamEval E = given ? *first : sweep1(lf, acc);
+    if (!given) ++out.sweeps;
     if (lf == 1.0f && E.KL <= eps) {
       if (!acc && E.KL < KL_ACCURATE) {
         acc = true;  // resolve a small endpoint KL with the accurate form
@@ -1010,8 +1215,12 @@ __device__ LamResult lambda_search_with(const RowStats& R, double eps, Sweep1&& 
       lg = 0.5 * (lo + hi);
       continue;
     }
-    const double a = trust ? fmax(lo, E.lam * (1.0 - TRUST)) : lo;
-    const double b = trust ? fmin(hi, E.lam * (1.0 + TRUST)) : hi;
+    // a node whose A''' and A'''' are estimates (reach-limited) takes a
+    // trust interval of ten times its reach: far from it the estimates can
+    // bend the model's KL back
+    const double tr = fmin(TRUST, 10.0 * E.reach);
+    const double a = trust ? fmax(lo, E.lam * (1.0 - tr)) : lo;
+    const double b = trust ? fmin(hi, E.lam * (1.0 + tr)) : hi;
     const double fa = M.kl(a) - eps, fb = M.kl(b) - eps;
     if (fa <= 0.0 && fb > 0.0) {
       // safeguarded Newton on the model inside [a, b]
@@ -1032,7 +1241,7 @@ __device__ LamResult lambda_search_with(const RowStats& R, double eps, Sweep1&& 
       }
       const double d = l - E.lam;
       const double err = 5.0 * fabs(E.A4) * d * d * d * d / 24.0;
-      if (err <= TAYLOR_TOL * eps) {
+      if (err <= TAYLOR_TOL * eps && fabs(d) <= E.reach * E.lam) {
         const float lr = static_cast<float>(l);
         double A, Ap;
         M.eval(static_cast<double>(lr), A, Ap);
@@ -1217,6 +1426,246 @@ __device__ double final_sweep_any(Block<NT, SH>& B, const T* srow, const T* trow
   return final_sweep<T, G, NT, GRAD, FIN_FAST>(B, srow, trow, grow, V, F, keep_res, coef, hot, s_hot);
 }
 
+// ---------------------------------------------------------------------------
+// Fused sweep: one pass that evaluates the lambda node and, speculatively,
+// what the final sweep needs.  Where the interpolating start places lambda*
+// close to its node lam_g, with A(lam_g) predicted as AL (log2 units), each
+// entry takes y = lam_g X - AL, e = 2^y (q/p at the node, up to the small
+// error of AL) and r = p~ (e - 1):
+//   node  : W = sum r, S_k = sum p~ e X^k (k = 1..3): A(lam_g) = AL ln 2 +
+//           log1p(W / sum p~), A', A'' and A''' (the model's step is
+//           accepted only within FUSED_REACH lam_g of the node, against a
+//           bound on A'''');
+//   final : over P = {y > 0}: T0 = sum r, U0 = sum p~ e, U1 = sum p~ e X, and
+//           the mass Bd = sum p~ e over the band |y| < FUSED_BAND; per chunk
+//           (keep_res) the masses sum_P r and sum_P p~ e;
+//   grad  : coef p_v under the accept decision taken at the start point.
+// At lambda* (node and model) each exponent moves by h = dl X - dA (dl, dA
+// the changes of lambda and of A log2 e), so
+//   sum [q - p]_+ (unnormalised) = T0 + ln 2 (dl U1 - dA U0) + O(h^2 U0)
+// plus the entries whose sign of y changes, all inside the band when the
+// threshold moves less than FUSED_BAND (fused_tv bounds both).  A row whose
+// lambda*, accept decision or bounds do not hold takes the final sweep after
+// all (its gradient is then rewritten).
+// ---------------------------------------------------------------------------
+constexpr float FUSED_BAND = 1.0f / 1024.0f;
+constexpr double FUSED_REACH = 1e-3;
+// largest bound on TV's error accepted from the fused sums (relative; the
+// bound is a worst case, the error itself is far below it)
+constexpr double FUSED_TV_TOL = 3e-6;
+
+struct FusedConst {
+  float msL, cL;  // as in the final sweep
+  float lam;      // the node lam_g
+  float AL;       // predicted A(lam_g) log2 e: the exponents are y = lam X - AL
+  float gsc;      // coef / sum p~ (with the shift's rounding): grad_v = gsc p~_v
+};
+
+struct FusedSums {
+  double v[4];   // W, S1, S2, S3 (log2 units, relative to 2^AL)
+  double T0, U0, U1, Bd;
+};
+
+template <typename T, typename G, int NT, bool GRAD, int MODE, typename SH>
+__device__ __forceinline__ FusedSums fused_sweep(Block<NT, SH>& B, const T* srow, const T* trow, G* grow, int V,
+                                                 const FusedConst C, bool keep_res, float coef, float invS,
+                                                 int hot, float s_hot) {
+  constexpr int NW = NT / WAVE;
+  double acc[5] = {0, 0, 0, 0, 0};  // W, S1, S2, S3, T0
+  float U0 = 0.f, U1 = 0.f, Bd = 0.f;
+  for_chunks<T, NW, true, use_mode<T, SH>()>(srow, trow, V, B.wave, B.lane,
+                    [&](auto tail, const float* s, const float* t, uint32_t vm, int c) {
+                      constexpr bool TAIL = decltype(tail)::value;
+                      float w = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f, t0 = 0.f, u0 = 0.f, u1 = 0.f, bd = 0.f;
+                      float g[EPL];
+#pragma unroll
+                      for (int e = 0; e < EPL; ++e) {
+                        const float a = fmaf(s[e], LOG2E, -C.msL);
+                        const float pt = fexp2(a);
+                        const float X = fmaf(t[e] - s[e], LOG2E, -C.cL);
+                        const float y = fmaf(C.lam, X, -C.AL);
+                        const float ee = fexp2(y);
+                        const float em1 = (MODE == FIN_ACC) ? expm1_sel(y * LN2, ee) : (ee - 1.0f);
+                        float r = pt * em1;
+                        float pe = pt + r;
+                        if (TAIL && !SAKI_VALID(e)) { r = 0.f; pe = 0.f; }
+                        w += r;
+                        const float X2 = X * X;
+                        s1 = fmaf(pe, X, s1);
+                        s2 = fmaf(pe, X2, s2);
+                        s3 = fmaf(pe * X2, X, s3);
+                        const bool pos = r > 0.0f;
+                        t0 += pos ? r : 0.0f;
+                        const float pp = pos ? pe : 0.0f;
+                        u0 += pp;
+                        u1 = fmaf(pp, X, u1);
+                        bd += (fabsf(y) < FUSED_BAND) ? pe : 0.0f;
+                        if (GRAD) g[e] = C.gsc * pt;
+                      }
+                      if (keep_res) {
+                        const float m = wave_sum(t0);
+                        const float q = wave_sum(u0);
+                        if (B.lane == 0) {
+                          B.sh.chunk_a[c] = m;
+                          B.sh.chunk_b[c] = q;
+                        }
+                      }
+                      acc[0] += static_cast<double>(w);
+                      acc[1] += static_cast<double>(s1);
+                      acc[2] += static_cast<double>(s2);
+                      acc[3] += static_cast<double>(s3);
+                      acc[4] += static_cast<double>(t0);
+                      U0 += u0;
+                      U1 += u1;
+                      Bd += bd;
+                      if (GRAD) store_lane<G, TAIL>(grow, c, B.lane, V, g);
+                    }, row_cache<T>(B.sh));
+  if (GRAD && hot >= 0 && hot < V && B.tid == entry_owner<NT>(hot)) {
+    const float p = fexp2(fmaf(s_hot, LOG2E, -C.msL)) * invS;
+    Storer<G>::store1(grow + hot, coef * (p - 1.0f));
+  }
+  double v[8] = {acc[0], acc[1], acc[2], acc[3], acc[4], static_cast<double>(U0), static_cast<double>(U1),
+                 static_cast<double>(Bd)};
+  B.sum(v);
+  FusedSums S;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) S.v[i] = v[i];
+  S.T0 = v[4];
+  S.U0 = v[5];
+  S.U1 = v[6];
+  S.Bd = v[7];
+  return S;
+}
+
+template <typename T, typename G, int NT, bool GRAD, typename SH>
+__device__ FusedSums fused_sweep_any(Block<NT, SH>& B, const T* srow, const T* trow, G* grow, int V,
+                                     const FusedConst& C, bool acc, bool keep_res, float coef, float invS, int hot,
+                                     float s_hot) {
+  if (acc) return fused_sweep<T, G, NT, GRAD, FIN_ACC>(B, srow, trow, grow, V, C, keep_res, coef, invS, hot, s_hot);
+  return fused_sweep<T, G, NT, GRAD, FIN_FAST>(B, srow, trow, grow, V, C, keep_res, coef, invS, hot, s_hot);
+}
+
+// The lambda node of the fused sums: sum_v p~ 2^{lam X} = 2^AL (sum p~ + W).
+// A'''' is not summed: A4 holds the bound max_v (x_v - A')^2 A'' on its size
+// (a fourth central moment is at most the squared range times the variance),
+// which the model's acceptance test needs and whose term in the model itself
+// is negligible within the node's reach (FUSED_REACH; none at the teacher end,
+// whose node only settles lambda* = 1).
+__device__ inline LamEval fused_node(const RowStats& R, const FusedSums& S, const FusedConst& C, bool end_first) {
+  const float msL = R.ms * LOG2E;
+  const double corr = shift_correction(R.ms, msL);
+  double v[5] = {S.v[0] * corr, S.v[1] * corr, S.v[2] * corr, S.v[3] * corr, 0.0};
+  LamEval E = lam_finish(v, R.sum_s, C.lam, 0.0f, false);
+  E.A += static_cast<double>(C.AL) * LN2_D;
+  E.KL = fmax(E.lam * E.A1 - E.A, 0.0);
+  const double xr = fmax(fabs(static_cast<double>(R.dmax) - R.c - E.A1), fabs(static_cast<double>(R.dmin) - R.c - E.A1));
+  E.A4 = xr * xr * E.A2;
+  E.reach = end_first ? 0.0 : FUSED_REACH;
+  return E;
+}
+
+// What the fused sums give at lambda* (L, F): TV, with the bounds that make it
+// usable.  hmax bounds |h| over the row; flip bounds the unnormalised mass of
+// the entries whose sign of y changes.  false: take the final sweep.
+struct FusedFinal {
+  bool ok;
+  double TV;
+  double hmax, flip;
+  int why;  // 0: ok; 1: lambda* or the form not from the node; 2: lambda moved too far; 3: TV bound
+};
+
+__device__ inline FusedFinal fused_tv(const RowStats& R, const LamResult& L, const FinalConst& F,
+                                      const FusedConst& C, const FusedSums& S, bool fused_acc) {
+  FusedFinal out;
+  out.ok = false;
+  out.TV = 0.0;
+  out.hmax = out.flip = 0.0;
+  out.why = 1;
+  if (L.sweeps != 0 || L.qp || F.wide || (F.acc && !fused_acc) || F.cL != C.cL || F.msL != C.msL) return out;
+  out.why = 2;
+  const double dl = static_cast<double>(F.lam) - static_cast<double>(C.lam);
+  const double dA = static_cast<double>(F.AL) - static_cast<double>(C.AL);
+  const double lg = static_cast<double>(C.lam);
+  // |X| over the row (X = d log2 e - cL), with a margin for its rounding
+  const double xa = fmax(fabs(static_cast<double>(R.dmax) * LOG2E - C.cL),
+                         fabs(static_cast<double>(R.dmin) * LOG2E - C.cL)) * (1.0 + 1e-6) + 1e-6;
+  const double hmax = fabs(dl) * xa + fabs(dA);
+  // an entry's exponent moves by h = rho y + H0 (X = (y + AL) / lam_g): its
+  // sign changes only where |y| <= |H0| / (1 - |rho|)
+  const double rho = dl / lg;
+  const double H0 = dl * static_cast<double>(C.AL) / lg - dA;
+  if (!(fabs(rho) < 0.5)) return out;
+  const double Hf = fabs(H0) / (1.0 - fabs(rho)) + 1e-9;
+  if (!(Hf < static_cast<double>(FUSED_BAND)) || !(hmax < 0.01)) return out;
+  out.why = 3;
+  // such an entry's residual at lambda* is below p~ e (2^Hf - 1) on either side
+  const double flip = S.Bd * Hf * LN2_D * 1.02;
+  const double tvu = S.T0 + LN2_D * (dl * S.U1 - dA * S.U0);
+  // the rest of 2^h - 1 after its linear term, at most (h ln 2)^2 / 2 (1 + h
+  // ln 2): summed over P with (dl X - dA)^2 <= 2 dl^2 X^2 + 2 dA^2 and
+  // sum_P p~ e X^2 <= S2 (every entry)
+  const double h2 = hmax * LN2_D;
+  const double sq = 2.0 * (dl * dl * fabs(S.v[2]) + dA * dA * S.U0);
+  const double err = flip + 0.5 * LN2_D * LN2_D * sq * (1.0 + h2) + 1e-7 * (S.T0 + S.U0 * h2);
+  if (!(tvu > 0.0) || !(err <= FUSED_TV_TOL * tvu)) return out;
+  out.ok = true;
+  out.why = 0;
+  out.TV = tvu * shift_correction(R.ms, C.msL) / R.sum_s;
+  out.hmax = hmax;
+  out.flip = flip;
+  return out;
+}
+
+// What wave 0 settles for a row between sweeps, read by every thread after a
+// barrier (the other waves skip the serial arithmetic).
+struct RowPlan {
+  StartPoint S0;
+  LamResult L;
+  FinalConst F;
+  FusedFinal FF;
+  int fused;   // the row takes the fused sweep
+  int state;   // after it: 1 settled, 0 final sweep after all, -1 the search needs sweeps
+  int C;       // the accept decision at lambda* (state >= 0)
+};
+
+// The chunk level of the residual race from masses known within bounds
+// (mass_bound(c, m, b): |true mass - m| <= b, m >= 0): the winner by the
+// masses m, or -1 when a chunk could still beat it within the bounds (the
+// caller then takes the final sweep).  Keys and ties as in chunk_race.
+template <int NT, typename SH, typename F>
+__device__ int chunk_race_certain(Block<NT, SH>& B, int nchunks, uint64_t seed, uint32_t stream, uint64_t g,
+                                  F mass_bound) {
+  double best = __builtin_huge_val();
+  int bi = 0x7fffffff;
+  // ln E of this thread's first chunk, kept for the second pass
+  auto ln_e = [&](int c) {
+    return log(-log(static_cast<double>(philox_uniform(seed, stream, g, static_cast<uint32_t>(c)))));
+  };
+  const double le0 = B.tid < nchunks ? ln_e(B.tid) : 0.0;
+  for (int c = B.tid; c < nchunks; c += NT) {
+    double m, b;
+    mass_bound(c, m, b);
+    if (m > 0.0) {
+      const double key = (c == B.tid ? le0 : ln_e(c)) - log(m);
+      if (key < best) { best = key; bi = c; }
+    }
+  }
+  B.argmin(best, bi);
+  if (bi >= nchunks) return -1;
+  double mw, bw;
+  mass_bound(bi, mw, bw);
+  if (!(mw - bw > 0.0)) return -1;
+  const double key_hi = ln_e(bi) - log(mw - bw);
+  float amb = 0.0f;
+  for (int c = B.tid; c < nchunks; c += NT) {
+    if (c == bi) continue;
+    double m, b;
+    mass_bound(c, m, b);
+    if (m + b > 0.0 && (c == B.tid ? le0 : ln_e(c)) - log(m + b) <= key_hi) amb = 1.0f;
+  }
+  return B.max(amb) > 0.0f ? -1 : bi;
+}
+
 // Standalone routed loss, first sweep: the log-sum-exp of one array, with the
 // next chunk's loads in flight.  Exponents are taken against the wave's
 // running maximum as one fma, fma(s, log2 e, -MsL) with MsL = Ms log2(e)
@@ -1257,7 +1706,7 @@ __device__ double lse_sweep(Block<NT, SH>& B, const T* srow, int V, float* msL_o
   B.sum(v);
   *msL_out = msL;
   // the maximum's own term exactly: 2^d0 (d0 = ms log2 e - msL, exact in
-  // double) instead of its float rounding (see stats_combine_block)
+  // double) instead of its float rounding (see stats_combine)
   if (isfinite(ms)) {
     const double d0 = static_cast<double>(LOG2E) * static_cast<double>(ms) - static_cast<double>(msL);
     v[0] += exp2(d0) - static_cast<double>(fexp2(fmaf(ms, LOG2E, -msL)));

@@ -79,6 +79,7 @@ __device__ __forceinline__ unsigned int take_next(unsigned int* counter, unsigne
 template <typename T, typename G, bool ROUTE, bool GRAD, int KC>
 __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
   __shared__ RowSharedK<KC> sh;
+  __shared__ RowPlan plan;
   Block<NT, RowSharedK<KC>> B(sh);
   const int V = P.V;
   const int nch = (V + CHUNK - 1) / CHUNK;
@@ -104,7 +105,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
     const float M = (ROUTE && P.valid) ? (P.valid[r] ? 1.0f : 0.0f) : 1.0f;
 
     const bool sample_target = ROUTE && P.target_mode == SAKI_TARGET_SAMPLE;
-    const RowStats& R = stats_sweep<T, NT>(B, srow, trow, V, true, sample_target);
+    const RowStats& R = stats_sweep<T, NT>(B, srow, trow, V, mid_lambda(P.eps), true, sample_target);
     if (!R.finite) {
       if (GRAD) fill_row<G, NT>(B.wave, B.lane, grow, V, M != 0.0f ? nanf_() : 0.0f);
       if (B.tid == 0) {
@@ -133,9 +134,8 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
     }
 
     // z ~ p by the two-level race (chunk masses from the stats sweep): the
-    // chunk race now; the winning chunk's entries are loaded before the lambda
-    // search, which hides their latency, and raced after it.  The logit of the
-    // teacher mode (the loss and gradient at a correction) is loaded early too.
+    // chunk race, then the entry race in the winning chunk.  The logit of the
+    // teacher mode (the loss and gradient at a correction) is loaded early.
     const int c0 = chunk_race<NT>(B, nch, P.seed, PROP_CHUNK, g, [&](int c) {
       return static_cast<double>(sh.chunk_a[c]) * LN2_D + log(static_cast<double>(sh.chunk_b[c]));
     });
@@ -143,7 +143,31 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
     const ElemFetch<T> fz = elem_fetch<T, NT>(srow, trow, cz, V, B.tid);
     const float s_vstar = Loader<T>::load1(srow + R.vstar);
 
-    const LamResult L = lambda_search<T, NT>(B, srow, trow, V, R, P.eps, force_acc);
+    // Rows the interpolating start places well take the fused sweep (the
+    // lambda node and a speculative final sweep in one pass), and so do rows
+    // whose teacher end may be feasible (the node lambda = 1, where A is known
+    // exactly); the others, and fused rows whose checks fail, the lambda
+    // search and the final sweep.
+    // The serial steps between sweeps run on wave 0 alone, which leaves the
+    // other waves' issue slots to the other workgroup of the CU; the results
+    // go through LDS (plan).
+    const bool end_first = R.kl1_est <= 1.05 * P.eps + 1e-5;
+    if (B.wave == 0) {
+      bool fu = !force_acc && P.eps > 0.0 && R.dmin != R.dmax;
+      StartPoint S0;
+      S0.lam = 1.0; S0.A = R.lse_t - R.lse_s - static_cast<double>(R.c); S0.herm = true;
+      if (fu) {
+        if (!end_first) S0 = start_point(R, P.eps);
+        const double top = S0.lam * (static_cast<double>(R.dmax) - static_cast<double>(R.c));
+        fu = S0.herm && top <= 56.0 && (top - S0.A) * static_cast<double>(LOG2E) <= 56.0;
+      }
+      if (B.lane == 0) {
+        plan.S0 = S0;
+        plan.fused = fu ? 1 : 0;
+      }
+    }
+    __syncthreads();
+    const bool fused = plan.fused != 0;
 
     float sz, tz;
     int z = elem_pick<NT>(B, fz, cz, V, P.seed, PROP_ELEM, g,
@@ -153,22 +177,22 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
       sz = s_vstar;
       tz = Loader<T>::load1(trow + z);
     }
-
-    // accept test, Eq. accept in the log form exp(min(0, log q(z) - log p(z)))
-    const double alpha = exp(fmin(0.0, L.log_ratio(sz, tz)));
     const double u = static_cast<double>(philox_uniform(P.seed, ACCEPT, g, 0));
-    const bool C = !(u < alpha);
-
     const double logp_z = static_cast<double>(sz) - R.lse_s;
     const double logt_z = static_cast<double>(tz) - R.lse_t;
     const double adv = logt_z - logp_z;
-    const float coef = ROUTE ? static_cast<float>(static_cast<double>(P.grad_scale) * M * (C ? 1.0 : adv)) : 0.0f;
-    // the gradient's indicator: the proposal when accepted; at a correction
-    // the teacher mode, or a draw from pi by the same two-level race on its
-    // own streams (teacher chunk masses from the stats sweep)
-    int hot = C ? R.vstar : z;
-    float s_hot = C ? s_vstar : sz;
-    if (sample_target && C) {
+    auto coef_of = [&](bool corr) {
+      return ROUTE ? static_cast<float>(static_cast<double>(P.grad_scale) * M * (corr ? 1.0 : adv)) : 0.0f;
+    };
+    // the gradient's indicator at a correction: the teacher mode, or a draw
+    // from pi by the same two-level race on its own streams (teacher chunk
+    // masses from the stats sweep); it does not depend on lambda
+    int hot_c = R.vstar;
+    float s_hot_c = s_vstar;
+    bool have_hot_c = !sample_target;
+    auto correction_target = [&]() {
+      if (have_hot_c) return;
+      have_hot_c = true;
       const int ct = chunk_race<NT>(B, nch, P.seed, TS_CHUNK, g, [&](int c) {
         return static_cast<double>(sh.chunk_c[c]) * LN2_D + log(static_cast<double>(sh.chunk_d[c]));
       });
@@ -178,13 +202,114 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
       const int vt = elem_pick<NT>(B, ft, cc, V, P.seed, TS_ELEM, g,
                                    [&](float, float tl, int) { return tl; }, &sv, &tv);
       if (vt < V) {
-        hot = vt;
-        s_hot = sv;
+        hot_c = vt;
+        s_hot_c = sv;
       }
+    };
+    auto sweep1 = [&](float lam, bool acc) { return lam_sweep<T, NT>(B, srow, trow, V, R, lam, acc); };
+
+    LamResult L;
+    FinalConst F;
+    bool C;
+    double TV = 0.0;
+    bool settled = false;  // TV, the residual chunk and the gradient row come from the fused sweep
+    int res_chunk = nch;
+    if (fused) {
+      // accept decision at the start point: it sets the gradient the fused
+      // sweep writes, and must agree with the one at lambda*
+      const double xz = (static_cast<double>(LOG2E) * (static_cast<double>(tz) - static_cast<double>(sz)) -
+                         static_cast<double>(R.cL)) * LN2_D;
+      const bool Cg = !(u < exp(fmin(0.0, plan.S0.lam * xz - plan.S0.A)));
+      if (Cg) correction_target();
+      const float coef_g = coef_of(Cg);
+      FusedConst FC;
+      FC.msL = R.ms * LOG2E;
+      FC.cL = R.cL;
+      FC.lam = static_cast<float>(plan.S0.lam);
+      FC.AL = static_cast<float>(plan.S0.A * static_cast<double>(LOG2E));
+      const float invS = static_cast<float>(shift_correction(R.ms, FC.msL) / R.sum_s);
+      FC.gsc = coef_g * invS;
+      // the expm1 form where the lambda sweep or the final sweep would take
+      // it (KL* = eps below lambda = 1, KL(pi || p) at it)
+      const bool facc = (end_first ? R.kl1_est < 1.01 * TV_ACCURATE : P.eps < TV_ACCURATE) || R.pmax > P_PEAKED;
+      const FusedSums FS = fused_sweep_any<T, G, NT, GRAD>(B, srow, trow, grow, V, FC, facc, Cg, coef_g, invS,
+                                                          Cg ? hot_c : z, Cg ? s_hot_c : sz);
+      // wave 0: lambda* from the node's model when it needs no sweep, the
+      // accept decision there and TV from the fused sums
+      if (B.wave == 0) {
+        const LamEval E0 = fused_node(R, FS, FC, end_first);
+        const LamResult L0 = lambda_search_with(R, P.eps, [](float, bool) { LamEval e{}; return e; }, false, 0.0f,
+                                                &E0, facc, true);
+        int state = -1, C0 = 0;
+        FinalConst F0{};
+        FusedFinal FF0{};
+        if (L0.sweeps == 0) {
+          F0 = final_const(R, L0, false);
+          C0 = !(u < exp(fmin(0.0, L0.log_ratio(sz, tz)))) ? 1 : 0;
+          FF0 = fused_tv(R, L0, F0, FC, FS, facc);
+          state = (FF0.ok && (C0 != 0) == Cg) ? 1 : 0;
+        }
+        if (B.lane == 0) {
+          plan.L = L0;
+          plan.F = F0;
+          plan.FF = FF0;
+          plan.state = state;
+          plan.C = C0;
+        }
+      }
+      __syncthreads();
+      if (plan.state < 0) {
+        // the node's model did not settle lambda*: the search goes on with
+        // lambda sweeps from that node
+        const LamEval E0 = fused_node(R, FS, FC, end_first);
+        L = lambda_search_with(R, P.eps, sweep1, false, 0.0f, &E0, facc);
+        F = final_const(R, L, false);
+        C = !(u < exp(fmin(0.0, L.log_ratio(sz, tz))));
+      } else {
+        L = plan.L;
+        F = plan.F;
+        C = plan.C != 0;
+        if (plan.state == 1) {
+          TV = plan.FF.TV;
+          settled = true;
+          if (C) {
+            // the residual chunk from the masses at the node, each within
+            // (2^hmax - 1) of its positive mass plus the sign-change bound
+            const double hb = expm1(plan.FF.hmax * LN2_D) * 1.02 + 2e-6;
+            const double flip = plan.FF.flip;
+            res_chunk = chunk_race_certain<NT>(B, nch, P.seed, RES_CHUNK, g, [&](int c, double& m, double& b) {
+              m = fmax(static_cast<double>(sh.chunk_a[c]), 0.0);
+              b = hb * static_cast<double>(sh.chunk_b[c]) + flip;
+            });
+            if (res_chunk < 0) {
+              settled = false;
+              res_chunk = nch;
+            }
+          }
+        }
+      }
+    } else {
+      L = lambda_search<T, NT>(B, srow, trow, V, R, P.eps, force_acc);
+      F = final_const(R, L, force_acc);
+      C = !(u < exp(fmin(0.0, L.log_ratio(sz, tz))));
     }
 
-    const FinalConst F = final_const(R, L, force_acc);
-    const double TV = final_sweep_any<T, G, NT, GRAD>(B, srow, trow, grow, V, F, C, coef, hot, s_hot);
+    // accept test, Eq. accept in the log form exp(min(0, log q(z) - log p(z)))
+    const double alpha = exp(fmin(0.0, L.log_ratio(sz, tz)));
+    if (C) correction_target();
+    const float coef = coef_of(C);
+    const int hot = C ? hot_c : z;
+    const float s_hot = C ? s_hot_c : sz;
+
+    if (!settled) {
+      TV = final_sweep_any<T, G, NT, GRAD>(B, srow, trow, grow, V, F, C, coef, hot, s_hot);
+      if (C) {
+        res_chunk = chunk_race<NT>(B, nch, P.seed, RES_CHUNK, g, [&](int c) {
+          const float m = sh.chunk_a[c];
+          return m > 0.0f ? log(static_cast<double>(m)) : -__builtin_huge_val();
+        });
+      }
+    }
     if (!force_acc && redo_accurate(R, L, F.acc, TV)) {
       // listed for the second launch, which rewrites the row's gradient and
       // writes its outputs
@@ -195,12 +320,9 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
     int y = z;
     float sy = sz, ty = tz;
     if (C) {
-      const int c1 = chunk_race<NT>(B, nch, P.seed, RES_CHUNK, g, [&](int c) {
-        const float m = sh.chunk_a[c];
-        return m > 0.0f ? log(static_cast<double>(m)) : -__builtin_huge_val();
-      });
       // a residual that rounds to zero everywhere in float (lambda* x within
       // rounding of A*) leaves no chunk with mass; the proposal is kept then
+      const int c1 = res_chunk;
       if (c1 < nch) {
         const ElemFetch<T> fr = elem_fetch<T, NT>(srow, trow, c1, V, B.tid);
         float sw, tw;
@@ -340,7 +462,7 @@ __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyP
         next_unwritten = j + 1;
         break;
       }
-      const RowStats& R = stats_sweep<T, VNT>(B, srow, trow, V, false);
+      const RowStats& R = stats_sweep<T, VNT>(B, srow, trow, V, mid_lambda(P.eps), false);
       if (!R.finite) {
         if (P.has_pp && B.tid == 0) write_skipped(o, r, z, SAKI_ROW_NONFINITE);
         n = j;
