@@ -413,7 +413,9 @@ struct StatsAcc {
 // is one factor for every term sharing it, removed exactly once the row's
 // maxima are known (shift_correction).  The proposal mass of chunk c is kept as
 // (MsL, sum_c 2^(s log2 e - MsL)), i.e. ln W_c = MsL ln 2 + ln(sum).
-template <bool TAIL, typename SH>
+// MID: also the middle node's sums (else the row carries no middle node and
+// the lambda search starts from the ends alone).
+template <bool TAIL, bool MID, typename SH>
 __device__ __forceinline__ void stats_math(const float* s, const float* t, uint32_t vm, int c,
                                            int lane, bool keep_chunks, bool keep_teacher, float lm, SH& sh,
                                            StatsAcc& a) {
@@ -499,7 +501,7 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
     float et = fexp2(at);
     // the middle node's weight p~^(1 - lm) pi~^lm: its exponent is at most 0
     // (as, at <= 0), so it cannot overflow
-    float em = fexp2(fmaf(lm, at - as, as));
+    float em = MID ? fexp2(fmaf(lm, at - as, as)) : 0.0f;
     if (TAIL && !SAKI_VALID(e)) { es = 0.f; et = 0.f; em = 0.f; }
     const float d = t[e] - s[e];
     const float d2 = d * d;
@@ -510,11 +512,13 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
     p4 = fmaf(ed2, d2, p4);
     t1 = fmaf(et, d, t1);
     t2 = fmaf(et, d2, t2);
-    q1 = fmaf(em, d, q1);
-    q2 = fmaf(em, d2, q2);
+    if (MID) {
+      q1 = fmaf(em, d, q1);
+      q2 = fmaf(em, d2, q2);
+      gm += em;
+    }
     gs += es;
     gt += et;
-    gm += em;
     if ((e & 7) == 7) {
       ps += static_cast<double>(gs);
       pt += static_cast<double>(gt);
@@ -682,7 +686,7 @@ __device__ inline RowStats row_stats_from(const StatsBlock& O) {
   {
     const double lm = static_cast<double>(O.lm);
     const double M1 = O.Q1 / O.Sm, M2 = O.Q2 / O.Sm;
-    R.lam_mid = O.lm;
+    R.lam_mid = O.Sm > 0.0 ? O.lm : 0.0f;
     R.mid_A = lm * (static_cast<double>(R.mt) - static_cast<double>(R.ms) - static_cast<double>(R.c)) +
               log(O.Sm) - log(O.Ss);
     R.mid_A1 = M1 - static_cast<double>(R.c);
@@ -697,7 +701,7 @@ __device__ inline RowStats row_stats_from(const StatsBlock& O) {
 // The statistics are kept in the workgroup's LDS (thread 0 writes them): the
 // caller reads its fields there where it needs them rather than holding the
 // whole record in registers across the later sweeps.
-template <typename T, int NT, typename SH>
+template <typename T, int NT, bool MID = true, typename SH>
 __device__ const RowStats& stats_sweep(Block<NT, SH>& B, const T* srow, const T* trow, int V, float lm,
                                        bool keep_chunks, bool keep_teacher = false) {
   constexpr int NW = NT / WAVE;
@@ -706,11 +710,11 @@ __device__ const RowStats& stats_sweep(Block<NT, SH>& B, const T* srow, const T*
   for_chunks<T, NW, false, fill_mode<T, SH>()>(srow, trow, V, B.wave, B.lane,
                     [&](auto tail, const float* s, const float* t, uint32_t vm, int c) {
                       constexpr bool TAIL = decltype(tail)::value;
-                      stats_math<TAIL>(s, t, vm, c, B.lane, keep_chunks, keep_teacher, lm, B.sh, a);
+                      stats_math<TAIL, MID>(s, t, vm, c, B.lane, keep_chunks, keep_teacher, lm, B.sh, a);
                     }, row_cache<T>(B.sh));
   stats_post(B, a);
   __syncthreads();
-  if (B.tid == 0) B.sh.rs.r = row_stats_from(stats_combine(B, lm));
+  if (B.tid == 0) B.sh.rs.r = row_stats_from(stats_combine(B, MID ? lm : 0.0f));
   __syncthreads();
   return B.sh.rs.r;
 }
@@ -1082,6 +1086,7 @@ __device__ inline StartPoint start_point(const RowStats& R, double eps) {
   S.lam = l0;
   S.A = 0.0;
   S.herm = false;
+  if (!(R.lam_mid > 0.0f)) return S;
   const HermiteA H(R);
   double p, p1, p2;
   H.eval(1.0, p, p1, p2);

@@ -427,6 +427,7 @@ template <typename T, int KC, int VNT>
 __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyParams P) {
   using SH = RowShared<VNT, (KC > 0 ? CACHED_MAXC : MAX_CHUNKS), KC>;
   __shared__ SH sh;
+  __shared__ RowPlan plan;
   Block<VNT, SH> B(sh);
   const int V = P.V;
   const int nch = (V + CHUNK - 1) / CHUNK;
@@ -471,13 +472,27 @@ __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyP
       }
       const float sz = Loader<T>::load1(srow + z), tz = Loader<T>::load1(trow + z);
       const double u = static_cast<double>(philox_uniform(P.seed, ACCEPT, g, 0));
-      // lam x_z - A(lam) is concave in lam and 0 at lam = 0, so on [0, 1] it lies
-      // above lam (x_z - A(1)) >= min(0, log pi(z) - log p(z)): a draft with u
-      // below that bound is accepted whatever lambda* is, and when no output
-      // needs lambda* its search is skipped
+      // g(lam) = lam x_z - A(lam) = log q(z) - log p(z) is concave in lam with
+      // g(0) = 0, so on a bracket [la, lb] of lambda* it lies above min(g(la),
+      // g(lb)): a draft with u below exp of that is accepted whatever lambda*
+      // is, and when no output needs lambda* its search is skipped.  The
+      // bracket is [0, 1] (g(1) = log pi(z) - log p(z)), or split at the
+      // middle node by the sign of KL(lm) - eps; the middle node's values come
+      // from float sums, so that bound keeps a margin of 2e-6.
       if (!need_lam) {
         const double lr1 = (static_cast<double>(tz) - R.lse_t) - (static_cast<double>(sz) - R.lse_s);
-        if (u < exp(fmin(0.0, lr1))) {
+        double gmin = fmin(0.0, lr1);
+        if (R.lam_mid > 0.0f) {
+          const double lm = static_cast<double>(R.lam_mid);
+          const double xz = static_cast<double>(tz) - static_cast<double>(sz) - static_cast<double>(R.c);
+          const double gm = lm * xz - R.mid_A;
+          const double klm = lm * R.mid_A1 - R.mid_A;
+          const double lo_side = fmin(0.0, gm), hi_side = fmin(gm, lr1);
+          const double gb = (klm < P.eps * (1.0 - 1e-3)) ? hi_side : (klm > P.eps * (1.0 + 1e-3)) ? lo_side
+                                                                     : fmin(lo_side, hi_side);
+          gmin = fmax(gmin, gb - 2e-6);
+        }
+        if (u < exp(gmin)) {
           if (P.has_pp && B.tid == 0) {
             if (o.logp_token) o.logp_token[r] = static_cast<float>(static_cast<double>(sz) - R.lse_s);
             if (o.logt_token) o.logt_token[r] = static_cast<float>(static_cast<double>(tz) - R.lse_t);
@@ -496,27 +511,123 @@ __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyP
           continue;
         }
       }
-      const LamResult L = lambda_search<T, VNT>(B, srow, trow, V, R, P.eps, force_acc);
+      // Positions the interpolating start places well take the fused sweep
+      // (the lambda node, and the residual chunk masses where the start
+      // predicts a rejection); the others the lambda search and, when
+      // rejected or when TV is asked for, the final sweep.
+      const bool end_first = R.kl1_est <= 1.05 * P.eps + 1e-5;
+      if (B.wave == 0) {
+        bool fu = !force_acc && P.eps > 0.0 && R.dmin != R.dmax;
+        StartPoint S0;
+        S0.lam = 1.0; S0.A = R.lse_t - R.lse_s - static_cast<double>(R.c); S0.herm = true;
+        if (fu) {
+          if (!end_first) S0 = start_point(R, P.eps);
+          const double top = S0.lam * (static_cast<double>(R.dmax) - static_cast<double>(R.c));
+          fu = S0.herm && top <= 56.0 && (top - S0.A) * static_cast<double>(LOG2E) <= 56.0;
+        }
+        if (B.lane == 0) {
+          plan.S0 = S0;
+          plan.fused = fu ? 1 : 0;
+        }
+      }
+      __syncthreads();
+      LamResult L;
+      FinalConst F;
+      double TV = __builtin_nan("");
+      bool settled = false;  // lambda*, the decision, TV (if valid) and the residual chunk from the fused sweep
+      bool tv_ok = false;
+      int res_chunk = nch;
+      auto sweep1 = [&](float lam, bool acc) { return lam_sweep<T, VNT>(B, srow, trow, V, R, lam, acc); };
+      if (plan.fused != 0) {
+        const double xz = (static_cast<double>(LOG2E) * (static_cast<double>(tz) - static_cast<double>(sz)) -
+                           static_cast<double>(R.cL)) * LN2_D;
+        const bool reject_g = !(u < exp(fmin(0.0, plan.S0.lam * xz - plan.S0.A)));
+        FusedConst FC;
+        FC.msL = R.ms * LOG2E;
+        FC.cL = R.cL;
+        FC.lam = static_cast<float>(plan.S0.lam);
+        FC.AL = static_cast<float>(plan.S0.A * static_cast<double>(LOG2E));
+        FC.gsc = 0.0f;
+        const bool facc = (end_first ? R.kl1_est < 1.01 * TV_ACCURATE : P.eps < TV_ACCURATE) || R.pmax > P_PEAKED;
+        const FusedSums FS = fused_sweep_any<T, float, VNT, false>(B, srow, trow, nullptr, V, FC, facc, reject_g,
+                                                                  0.0f, 0.0f, -1, 0.0f);
+        if (B.wave == 0) {
+          const LamEval E0 = fused_node(R, FS, FC, end_first);
+          const LamResult L0 = lambda_search_with(R, P.eps, [](float, bool) { LamEval e{}; return e; }, false, 0.0f,
+                                                  &E0, facc, true);
+          int state = -1, C0 = 0;
+          FinalConst F0{};
+          FusedFinal FF0{};
+          if (L0.sweeps == 0) {
+            F0 = final_const(R, L0, false);
+            C0 = !(u < exp(fmin(0.0, L0.log_ratio(sz, tz)))) ? 1 : 0;
+            FF0 = fused_tv(R, L0, F0, FC, FS, facc);
+            // settled unless the decision or TV needs the final sweep: a
+            // rejection needs valid residual masses (kept only where the
+            // start predicted it), TV a valid correction
+            const bool need_final = (C0 != 0) ? !(FF0.ok && reject_g) : (need_tv && !FF0.ok);
+            state = need_final ? 0 : 1;
+          }
+          if (B.lane == 0) {
+            plan.L = L0;
+            plan.F = F0;
+            plan.FF = FF0;
+            plan.state = state;
+            plan.C = C0;
+          }
+        }
+        __syncthreads();
+        if (plan.state < 0) {
+          const LamEval E0 = fused_node(R, FS, FC, end_first);
+          L = lambda_search_with(R, P.eps, sweep1, false, 0.0f, &E0, facc);
+          F = final_const(R, L, false);
+        } else {
+          L = plan.L;
+          F = plan.F;
+          if (plan.state == 1) {
+            settled = true;
+            tv_ok = plan.FF.ok;
+            if (tv_ok) TV = plan.FF.TV;
+            if (plan.C != 0) {
+              const double hb = expm1(plan.FF.hmax * LN2_D) * 1.02 + 2e-6;
+              const double flip = plan.FF.flip;
+              res_chunk = chunk_race_certain<VNT>(B, nch, P.seed, RES_CHUNK, g, [&](int c, double& m, double& bb) {
+                m = fmax(static_cast<double>(sh.chunk_a[c]), 0.0);
+                bb = hb * static_cast<double>(sh.chunk_b[c]) + flip;
+              });
+              if (res_chunk < 0) {
+                settled = false;
+                res_chunk = nch;
+              }
+            }
+          }
+        }
+      } else {
+        L = lambda_search<T, VNT>(B, srow, trow, V, R, P.eps, force_acc);
+        F = final_const(R, L, force_acc);
+      }
       const double alpha = exp(fmin(0.0, L.log_ratio(sz, tz)));
       const bool accept = u < alpha;
-      double TV = __builtin_nan("");
-      const FinalConst F = final_const(R, L, force_acc);
-      if (need_tv || !accept) {
+      if (!settled && (need_tv || !accept)) {
         TV = final_sweep_any<T, float, VNT, false>(B, srow, trow, nullptr, V, F, !accept, 0.0f, -1, 0.0f);
-        if (!force_acc && redo_accurate(R, L, F.acc, TV)) {
-          force_acc = true;
-          --j;
-          continue;
+        tv_ok = true;
+        if (!accept) {
+          res_chunk = chunk_race<VNT>(B, nch, P.seed, RES_CHUNK, g, [&](int c) {
+            const float m = sh.chunk_a[c];
+            return m > 0.0f ? log(static_cast<double>(m)) : -__builtin_huge_val();
+          });
         }
+      }
+      if ((need_tv || !accept) && tv_ok && !force_acc && redo_accurate(R, L, F.acc, TV)) {
+        force_acc = true;
+        --j;
+        continue;
       }
       force_acc = false;
       int y = z;
       float sy = sz, ty = tz;
       if (!accept) {
-        const int c1 = chunk_race<VNT>(B, nch, P.seed, RES_CHUNK, g, [&](int c) {
-          const float m = sh.chunk_a[c];
-          return m > 0.0f ? log(static_cast<double>(m)) : -__builtin_huge_val();
-        });
+        const int c1 = res_chunk;
         if (c1 < nch) {
           const ElemFetch<T> fr = elem_fetch<T, VNT>(srow, trow, c1, V, B.tid);
           float sw, tw;
