@@ -1220,10 +1220,9 @@ __device__ LamResult lambda_search_with(const RowStats& R, double eps, Sweep1&& 
       lg = 0.5 * (lo + hi);
       continue;
     }
-    // a node whose A''' and A'''' are estimates (reach-limited) takes a
-    // trust interval of ten times its reach: far from it the estimates can
-    // bend the model's KL back
-    const double tr = fmin(TRUST, 10.0 * E.reach);
+    // a node whose A'''' is a bound (reach-limited) takes a trust interval of
+    // twice its reach: far from the node that term would bend the model's KL
+    const double tr = fmin(TRUST, 2.0 * E.reach);
     const double a = trust ? fmax(lo, E.lam * (1.0 - tr)) : lo;
     const double b = trust ? fmin(hi, E.lam * (1.0 + tr)) : hi;
     const double fa = M.kl(a) - eps, fb = M.kl(b) - eps;
@@ -1454,7 +1453,7 @@ __device__ double final_sweep_any(Block<NT, SH>& B, const T* srow, const T* trow
 // all (its gradient is then rewritten).
 // ---------------------------------------------------------------------------
 constexpr float FUSED_BAND = 1.0f / 1024.0f;
-constexpr double FUSED_REACH = 1e-3;
+constexpr double FUSED_REACH = 0.02;
 // largest bound on TV's error accepted from the fused sums (relative; the
 // bound is a worst case, the error itself is far below it)
 constexpr double FUSED_TV_TOL = 3e-6;
@@ -1550,16 +1549,32 @@ __device__ FusedSums fused_sweep_any(Block<NT, SH>& B, const T* srow, const T* t
   return fused_sweep<T, G, NT, GRAD, FIN_FAST>(B, srow, trow, grow, V, C, keep_res, coef, invS, hot, s_hot);
 }
 
+// The dominant entry's term of the fused sweep's W in the plain form: its
+// float value as the sweep computes it and its value in double (as
+// dominant_fix does for the lambda sweep); the difference corrects W.
+__device__ inline double dominant_fix_fused(float s, float t, const FusedConst& C) {
+  const float a = fmaf(s, LOG2E, -C.msL);
+  const float X = fmaf(t - s, LOG2E, -C.cL);
+  const float y = fmaf(C.lam, X, -C.AL);
+  const float rf = fexp2(a) * (fexp2(y) - 1.0f);
+  const double yd = (static_cast<double>(C.lam) * static_cast<double>(X) - static_cast<double>(C.AL)) * LN2_D;
+  return exp2(static_cast<double>(a)) * expm1(yd) - static_cast<double>(rf);
+}
+
 // The lambda node of the fused sums: sum_v p~ 2^{lam X} = 2^AL (sum p~ + W).
 // A'''' is not summed: A4 holds the bound max_v (x_v - A')^2 A'' on its size
 // (a fourth central moment is at most the squared range times the variance),
 // which the model's acceptance test needs and whose term in the model itself
 // is negligible within the node's reach (FUSED_REACH; none at the teacher end,
 // whose node only settles lambda* = 1).
-__device__ inline LamEval fused_node(const RowStats& R, const FusedSums& S, const FusedConst& C, bool end_first) {
+// acc: the sweep took the expm1 form (else the dominant entry's term of W is
+// taken exactly).
+__device__ inline LamEval fused_node(const RowStats& R, const FusedSums& S, const FusedConst& C, bool end_first,
+                                     bool acc) {
   const float msL = R.ms * LOG2E;
   const double corr = shift_correction(R.ms, msL);
-  double v[5] = {S.v[0] * corr, S.v[1] * corr, S.v[2] * corr, S.v[3] * corr, 0.0};
+  const double w = S.v[0] + (acc ? 0.0 : dominant_fix_fused(R.ms, R.t_smax, C));
+  double v[5] = {w * corr, S.v[1] * corr, S.v[2] * corr, S.v[3] * corr, 0.0};
   LamEval E = lam_finish(v, R.sum_s, C.lam, 0.0f, false);
   E.A += static_cast<double>(C.AL) * LN2_D;
   E.KL = fmax(E.lam * E.A1 - E.A, 0.0);
@@ -1580,13 +1595,13 @@ struct FusedFinal {
 };
 
 __device__ inline FusedFinal fused_tv(const RowStats& R, const LamResult& L, const FinalConst& F,
-                                      const FusedConst& C, const FusedSums& S, bool fused_acc) {
+                                      const FusedConst& C, const FusedSums& S) {
   FusedFinal out;
   out.ok = false;
   out.TV = 0.0;
   out.hmax = out.flip = 0.0;
   out.why = 1;
-  if (L.sweeps != 0 || L.qp || F.wide || (F.acc && !fused_acc) || F.cL != C.cL || F.msL != C.msL) return out;
+  if (L.sweeps != 0 || L.qp || F.wide || F.cL != C.cL || F.msL != C.msL) return out;
   out.why = 2;
   const double dl = static_cast<double>(F.lam) - static_cast<double>(C.lam);
   const double dA = static_cast<double>(F.AL) - static_cast<double>(C.AL);

@@ -212,6 +212,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
     FinalConst F;
     bool C;
     double TV = 0.0;
+    bool tv_acc = false;   // the fused sweep's form (the final sweep's is F.acc)
     bool settled = false;  // TV, the residual chunk and the gradient row come from the fused sweep
     int res_chunk = nch;
     if (fused) {
@@ -229,15 +230,19 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
       FC.AL = static_cast<float>(plan.S0.A * static_cast<double>(LOG2E));
       const float invS = static_cast<float>(shift_correction(R.ms, FC.msL) / R.sum_s);
       FC.gsc = coef_g * invS;
-      // the expm1 form where the lambda sweep or the final sweep would take
-      // it (KL* = eps below lambda = 1, KL(pi || p) at it)
-      const bool facc = (end_first ? R.kl1_est < 1.01 * TV_ACCURATE : P.eps < TV_ACCURATE) || R.pmax > P_PEAKED;
+      // the expm1 form where the lambda sweep would take it (KL below
+      // KL_ACCURATE: the radius, or KL(pi || p) at the teacher end) and on
+      // peaked rows, whose TV the plain form would often leave too imprecise;
+      // elsewhere a row whose TV turns out too small for the plain form is
+      // listed for the accurate second launch (redo_accurate)
+      const bool facc = (end_first ? R.kl1_est < 1.01 * KL_ACCURATE : P.eps < KL_ACCURATE) || R.pmax > P_PEAKED;
+      tv_acc = facc;
       const FusedSums FS = fused_sweep_any<T, G, NT, GRAD>(B, srow, trow, grow, V, FC, facc, Cg, coef_g, invS,
                                                           Cg ? hot_c : z, Cg ? s_hot_c : sz);
       // wave 0: lambda* from the node's model when it needs no sweep, the
       // accept decision there and TV from the fused sums
       if (B.wave == 0) {
-        const LamEval E0 = fused_node(R, FS, FC, end_first);
+        const LamEval E0 = fused_node(R, FS, FC, end_first, facc);
         const LamResult L0 = lambda_search_with(R, P.eps, [](float, bool) { LamEval e{}; return e; }, false, 0.0f,
                                                 &E0, facc, true);
         int state = -1, C0 = 0;
@@ -246,7 +251,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
         if (L0.sweeps == 0) {
           F0 = final_const(R, L0, false);
           C0 = !(u < exp(fmin(0.0, L0.log_ratio(sz, tz)))) ? 1 : 0;
-          FF0 = fused_tv(R, L0, F0, FC, FS, facc);
+          FF0 = fused_tv(R, L0, F0, FC, FS);
           state = (FF0.ok && (C0 != 0) == Cg) ? 1 : 0;
         }
         if (B.lane == 0) {
@@ -261,7 +266,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
       if (plan.state < 0) {
         // the node's model did not settle lambda*: the search goes on with
         // lambda sweeps from that node
-        const LamEval E0 = fused_node(R, FS, FC, end_first);
+        const LamEval E0 = fused_node(R, FS, FC, end_first, facc);
         L = lambda_search_with(R, P.eps, sweep1, false, 0.0f, &E0, facc);
         F = final_const(R, L, false);
         C = !(u < exp(fmin(0.0, L.log_ratio(sz, tz))));
@@ -310,7 +315,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
         });
       }
     }
-    if (!force_acc && redo_accurate(R, L, F.acc, TV)) {
+    if (!force_acc && redo_accurate(R, L, settled ? tv_acc : F.acc, TV)) {
       // listed for the second launch, which rewrites the row's gradient and
       // writes its outputs
       if (B.tid == 0) P.redo_list[atomicAdd(P.redo_count, 1u)] = static_cast<unsigned int>(r);
@@ -536,6 +541,7 @@ __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyP
       double TV = __builtin_nan("");
       bool settled = false;  // lambda*, the decision, TV (if valid) and the residual chunk from the fused sweep
       bool tv_ok = false;
+      bool tv_acc = false;   // the fused sweep's form (the final sweep's is F.acc)
       int res_chunk = nch;
       auto sweep1 = [&](float lam, bool acc) { return lam_sweep<T, VNT>(B, srow, trow, V, R, lam, acc); };
       if (plan.fused != 0) {
@@ -548,11 +554,12 @@ __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyP
         FC.lam = static_cast<float>(plan.S0.lam);
         FC.AL = static_cast<float>(plan.S0.A * static_cast<double>(LOG2E));
         FC.gsc = 0.0f;
-        const bool facc = (end_first ? R.kl1_est < 1.01 * TV_ACCURATE : P.eps < TV_ACCURATE) || R.pmax > P_PEAKED;
+        const bool facc = (end_first ? R.kl1_est < 1.01 * KL_ACCURATE : P.eps < KL_ACCURATE) || R.pmax > P_PEAKED;
+        tv_acc = facc;
         const FusedSums FS = fused_sweep_any<T, float, VNT, false>(B, srow, trow, nullptr, V, FC, facc, reject_g,
                                                                   0.0f, 0.0f, -1, 0.0f);
         if (B.wave == 0) {
-          const LamEval E0 = fused_node(R, FS, FC, end_first);
+          const LamEval E0 = fused_node(R, FS, FC, end_first, facc);
           const LamResult L0 = lambda_search_with(R, P.eps, [](float, bool) { LamEval e{}; return e; }, false, 0.0f,
                                                   &E0, facc, true);
           int state = -1, C0 = 0;
@@ -561,7 +568,7 @@ __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyP
           if (L0.sweeps == 0) {
             F0 = final_const(R, L0, false);
             C0 = !(u < exp(fmin(0.0, L0.log_ratio(sz, tz)))) ? 1 : 0;
-            FF0 = fused_tv(R, L0, F0, FC, FS, facc);
+            FF0 = fused_tv(R, L0, F0, FC, FS);
             // settled unless the decision or TV needs the final sweep: a
             // rejection needs valid residual masses (kept only where the
             // start predicted it), TV a valid correction
@@ -578,7 +585,7 @@ __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyP
         }
         __syncthreads();
         if (plan.state < 0) {
-          const LamEval E0 = fused_node(R, FS, FC, end_first);
+          const LamEval E0 = fused_node(R, FS, FC, end_first, facc);
           L = lambda_search_with(R, P.eps, sweep1, false, 0.0f, &E0, facc);
           F = final_const(R, L, false);
         } else {
@@ -618,7 +625,7 @@ __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyP
           });
         }
       }
-      if ((need_tv || !accept) && tv_ok && !force_acc && redo_accurate(R, L, F.acc, TV)) {
+      if ((need_tv || !accept) && tv_ok && !force_acc && redo_accurate(R, L, settled ? tv_acc : F.acc, TV)) {
         force_acc = true;
         --j;
         continue;
