@@ -27,6 +27,15 @@ constexpr int RED_MAX = 16;  // widest block reduction (doubles per thread)
 // search interpolates A between lambda = 0, that node and 1 instead of
 // extrapolating from the ends.  The node sits near where lambda* falls for the
 // radius (lambda* ~ sqrt(2 eps / Var_p[d]), Var_p[d] of a few units).
+// The stats sweep sums the p-moments of d through d^4 (K34: the third and
+// fourth cumulants feed the starts) or through d^2 only.  They pay where
+// lambda* is small, close to the node lambda = 0 they describe: radii below
+// K34_EPS (lambda* ~ sqrt(2 eps / Var_p[d])); elsewhere the middle and end
+// nodes place lambda* as well without them, and in float the higher moments
+// of d (not centred) carry more noise than they add.
+constexpr double K34_EPS = 0.03;
+__host__ __device__ inline bool use_k34(double eps) { return eps < K34_EPS; }
+
 __host__ __device__ inline float mid_lambda(double eps) {
   const double l = 0.5 * sqrt(eps > 0.0 ? eps : 0.0);
   return static_cast<float>(l < 0.05 ? 0.05 : l > 0.5 ? 0.5 : l);
@@ -53,6 +62,7 @@ struct RowStats {
   float t_smax;        // t at an entry holding max s (the dominant entry of p)
   double pmax;         // max_v p_v = exp(ms - lse_s)
   float lam_mid;       // the middle node (mid_lambda)
+  bool k34;            // k3, k4 were summed (else 0)
   double mid_A, mid_A1, mid_A2;  // A, A', A'' there
   bool finite;
 };
@@ -414,8 +424,9 @@ struct StatsAcc {
 // maxima are known (shift_correction).  The proposal mass of chunk c is kept as
 // (MsL, sum_c 2^(s log2 e - MsL)), i.e. ln W_c = MsL ln 2 + ln(sum).
 // MID: also the middle node's sums (else the row carries no middle node and
-// the lambda search starts from the ends alone).
-template <bool TAIL, bool MID, typename SH>
+// the lambda search starts from the ends alone); K34: the third and fourth
+// p-moments of d.
+template <bool TAIL, bool MID, bool K34, typename SH>
 __device__ __forceinline__ void stats_math(const float* s, const float* t, uint32_t vm, int c,
                                            int lane, bool keep_chunks, bool keep_teacher, float lm, SH& sh,
                                            StatsAcc& a) {
@@ -507,9 +518,11 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
     const float d2 = d * d;
     p1 = fmaf(es, d, p1);
     p2 = fmaf(es, d2, p2);
-    const float ed2 = es * d2;
-    p3 = fmaf(ed2, d, p3);
-    p4 = fmaf(ed2, d2, p4);
+    if (K34) {
+      const float ed2 = es * d2;
+      p3 = fmaf(ed2, d, p3);
+      p4 = fmaf(ed2, d2, p4);
+    }
     t1 = fmaf(et, d, t1);
     t2 = fmaf(et, d2, t2);
     if (MID) {
@@ -528,15 +541,16 @@ __device__ __forceinline__ void stats_math(const float* s, const float* t, uint3
       gm = 0.f;
     }
   }
+  // chunk masses (stored as float) by a float reduction
   if (keep_chunks) {
-    const float csum = static_cast<float>(wave_sum(ps));
+    const float csum = wave_sum(static_cast<float>(ps));
     if (lane == 0) {
       sh.chunk_a[c] = a.MsL;
       sh.chunk_b[c] = csum;
     }
   }
   if (keep_teacher) {
-    const float csum = static_cast<float>(wave_sum(pt));
+    const float csum = wave_sum(static_cast<float>(pt));
     if (lane == 0) {
       sh.chunk_c[c] = a.MtL;
       sh.chunk_d[c] = csum;
@@ -656,7 +670,7 @@ __device__ StatsBlock stats_combine(Block<NT, SH>& B, float lm) {
 }
 
 // Row statistics from the (combined) block statistics.
-__device__ inline RowStats row_stats_from(const StatsBlock& O) {
+__device__ inline RowStats row_stats_from(const StatsBlock& O, bool k34) {
   RowStats R;
   R.ms = O.ms;
   R.mt = O.mt;
@@ -670,8 +684,9 @@ __device__ inline RowStats row_stats_from(const StatsBlock& O) {
   R.lse_t = static_cast<double>(R.mt) + log(O.St);
   const double Ed = O.S1 / O.Ss, E2 = O.S2 / O.Ss, E3 = O.S3 / O.Ss, E4 = O.S4 / O.Ss;
   R.var = fmax(E2 - Ed * Ed, 0.0);
-  R.k3 = E3 - 3.0 * Ed * E2 + 2.0 * Ed * Ed * Ed;
-  R.k4 = (E4 - 4.0 * Ed * E3 + 6.0 * Ed * Ed * E2 - 3.0 * Ed * Ed * Ed * Ed) - 3.0 * R.var * R.var;
+  R.k34 = k34;
+  R.k3 = k34 ? E3 - 3.0 * Ed * E2 + 2.0 * Ed * Ed * Ed : 0.0;
+  R.k4 = k34 ? (E4 - 4.0 * Ed * E3 + 6.0 * Ed * Ed * E2 - 3.0 * Ed * Ed * Ed * Ed) - 3.0 * R.var * R.var : 0.0;
   R.mean_p = Ed;
   R.mean_pi = O.T1 / O.St;
   R.var_pi = fmax(O.T2 / O.St - R.mean_pi * R.mean_pi, 0.0);
@@ -701,7 +716,7 @@ __device__ inline RowStats row_stats_from(const StatsBlock& O) {
 // The statistics are kept in the workgroup's LDS (thread 0 writes them): the
 // caller reads its fields there where it needs them rather than holding the
 // whole record in registers across the later sweeps.
-template <typename T, int NT, bool MID = true, typename SH>
+template <typename T, int NT, bool MID = true, bool K34 = true, typename SH>
 __device__ const RowStats& stats_sweep(Block<NT, SH>& B, const T* srow, const T* trow, int V, float lm,
                                        bool keep_chunks, bool keep_teacher = false) {
   constexpr int NW = NT / WAVE;
@@ -710,11 +725,11 @@ __device__ const RowStats& stats_sweep(Block<NT, SH>& B, const T* srow, const T*
   for_chunks<T, NW, false, fill_mode<T, SH>()>(srow, trow, V, B.wave, B.lane,
                     [&](auto tail, const float* s, const float* t, uint32_t vm, int c) {
                       constexpr bool TAIL = decltype(tail)::value;
-                      stats_math<TAIL, MID>(s, t, vm, c, B.lane, keep_chunks, keep_teacher, lm, B.sh, a);
+                      stats_math<TAIL, MID, K34>(s, t, vm, c, B.lane, keep_chunks, keep_teacher, lm, B.sh, a);
                     }, row_cache<T>(B.sh));
   stats_post(B, a);
   __syncthreads();
-  if (B.tid == 0) B.sh.rs.r = row_stats_from(stats_combine(B, MID ? lm : 0.0f));
+  if (B.tid == 0) B.sh.rs.r = row_stats_from(stats_combine(B, MID ? lm : 0.0f), K34);
   __syncthreads();
   return B.sh.rs.r;
 }
@@ -1017,14 +1032,15 @@ __device__ inline double two_ended_start(const RowStats& R, double eps) {
   return lo;
 }
 
-// Interpolating start: the polynomial of degree 10 that matches A and its
-// first four derivatives at lambda = 0 (the cumulants of x under p), A, A',
-// A'' at the middle node, and A, A', A'' at lambda = 1 (the teacher end), in
-// Newton form over the confluent nodes.  On rows whose A is smooth on [0, 1] it places
+// Interpolating start: the polynomial of degree N0 + 5 that matches A and its
+// first N0 - 1 derivatives at lambda = 0 (the cumulants of x under p: four
+// with k3, k4, else two), A, A', A'' at the middle node, and A, A', A'' at
+// lambda = 1 (the teacher end), in Newton form over the confluent nodes.  On rows whose A is smooth on [0, 1] it places
 // lambda* to ~1e-6 or better, where the ends alone (two_ended_start) leave
 // ~1e-3; on spiky rows it can be far off, which the caller detects.
+template <int N0>  // conditions at lambda = 0: 5 with k3, k4, else 3
 struct HermiteA {
-  static constexpr int N = 11;
+  static constexpr int N = N0 + 6;
   double z[N], c[N];
   __device__ explicit HermiteA(const RowStats& R) {
     const double lm = static_cast<double>(R.lam_mid);
@@ -1032,10 +1048,10 @@ struct HermiteA {
     const double fm[3] = {R.mid_A, R.mid_A1, R.mid_A2};
     const double f1[3] = {R.lse_t - R.lse_s - R.c, R.mean_pi - R.c, R.var_pi};
     const double inv_fact[5] = {1.0, 1.0, 0.5, 1.0 / 6.0, 1.0 / 24.0};
-    auto deriv = [&](int i, int j) { return i < 5 ? f0[j] : i < 8 ? fm[j] : f1[j]; };
+    auto deriv = [&](int i, int j) { return i < N0 ? f0[j] : i < N0 + 3 ? fm[j - 0] : f1[j]; };
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      z[i] = i < 5 ? 0.0 : i < 8 ? lm : 1.0;
+      z[i] = i < N0 ? 0.0 : i < N0 + 3 ? lm : 1.0;
       c[i] = deriv(i, 0);
     }
     // divided differences in place: after step j, c[i] = f[z_{i-j} .. z_i]
@@ -1077,20 +1093,14 @@ struct StartPoint {
 
 constexpr double LAM_MAX = 1.0 - 1e-6;
 
-__device__ inline StartPoint start_point(const RowStats& R, double eps) {
-  const double l_cum = cumulant_start(R, eps);
-  const double l_two = two_ended_start(R, eps);
-  double l0 = (l_two > 0.0 && fabs(l_two - l_cum) <= 0.3 * l_cum) ? l_two : l_cum;
-  l0 = fmin(fmax(l0, 1e-7), LAM_MAX);
-  StartPoint S;
-  S.lam = l0;
-  S.A = 0.0;
-  S.herm = false;
-  if (!(R.lam_mid > 0.0f)) return S;
-  const HermiteA H(R);
+// The interpolant's root of KL = eps near l0 (S unchanged when it is not
+// found, lies more than 30% from l0, or the interpolant is not convex there).
+template <int N0>
+__device__ inline void hermite_refine(const RowStats& R, double eps, double l0, StartPoint& S) {
+  const HermiteA<N0> H(R);
   double p, p1, p2;
   H.eval(1.0, p, p1, p2);
-  if (!(p1 - p > eps)) return S;  // the interpolant puts lambda* at 1
+  if (!(p1 - p > eps)) return;  // the interpolant puts lambda* at 1
   // safeguarded Newton on KL(l) = l A'(l) - A(l) = eps (KL' = l A''),
   // keeping the bracket KL(lo) <= eps < KL(hi)
   // (converged once the step is below 1e-10 of lambda: the interpolant's own
@@ -1112,12 +1122,28 @@ __device__ inline StartPoint start_point(const RowStats& R, double eps) {
     if (!(nl > lo && nl < hi)) nl = 0.5 * (lo + hi);
     l = nl;
   }
-  if (!conv || !(fabs(l - l0) <= 0.3 * l0) || !(l < LAM_MAX)) return S;
+  if (!conv || !(fabs(l - l0) <= 0.3 * l0) || !(l < LAM_MAX)) return;
   H.eval(l, p, p1, p2);
-  if (!(p2 > 0.0) || !isfinite(p)) return S;
+  if (!(p2 > 0.0) || !isfinite(p)) return;
   S.lam = l;
   S.A = p;
   S.herm = true;
+}
+
+__device__ inline StartPoint start_point(const RowStats& R, double eps) {
+  const double l_cum = cumulant_start(R, eps);
+  const double l_two = two_ended_start(R, eps);
+  double l0 = (l_two > 0.0 && fabs(l_two - l_cum) <= 0.3 * l_cum) ? l_two : l_cum;
+  l0 = fmin(fmax(l0, 1e-7), LAM_MAX);
+  StartPoint S;
+  S.lam = l0;
+  S.A = 0.0;
+  S.herm = false;
+  if (!(R.lam_mid > 0.0f)) return S;
+  if (R.k34)
+    hermite_refine<5>(R, eps, l0, S);
+  else
+    hermite_refine<3>(R, eps, l0, S);
   return S;
 }
 
@@ -1436,17 +1462,19 @@ __device__ double final_sweep_any(Block<NT, SH>& B, const T* srow, const T* trow
 // close to its node lam_g, with A(lam_g) predicted as AL (log2 units), each
 // entry takes y = lam_g X - AL, e = 2^y (q/p at the node, up to the small
 // error of AL) and r = p~ (e - 1):
-//   node  : W = sum r, S_k = sum p~ e X^k (k = 1..3): A(lam_g) = AL ln 2 +
-//           log1p(W / sum p~), A', A'' and A''' (the model's step is
-//           accepted only within FUSED_REACH lam_g of the node, against a
-//           bound on A'''');
-//   final : over P = {y > 0}: T0 = sum r, U0 = sum p~ e, U1 = sum p~ e X, and
+//   node  : W = sum r, S_k = sum p~ e y^k (k = 1..3): A(lam_g) = AL ln 2 +
+//           log1p(W / sum p~), and from the moments of y = lam_g X - AL
+//           those of X, i.e. A', A'' and A''' (the model's step is accepted
+//           only within FUSED_REACH lam_g of the node, against a bound on
+//           A'''');
+//   final : over P = {y > 0}: T0 = sum r, U0 = sum p~ e, U1 = sum p~ e y, and
 //           the mass Bd = sum p~ e over the band |y| < FUSED_BAND; per chunk
 //           (keep_res) the masses sum_P r and sum_P p~ e;
 //   grad  : coef p_v under the accept decision taken at the start point.
-// At lambda* (node and model) each exponent moves by h = dl X - dA (dl, dA
-// the changes of lambda and of A log2 e), so
-//   sum [q - p]_+ (unnormalised) = T0 + ln 2 (dl U1 - dA U0) + O(h^2 U0)
+// At lambda* (node and model) each exponent moves by h = dl X - dA = rho y +
+// H0 (dl, dA the changes of lambda and of A log2 e; rho = dl / lam_g,
+// H0 = rho AL - dA), so
+//   sum [q - p]_+ (unnormalised) = T0 + ln 2 (rho U1 + H0 U0) + O(h^2 U0)
 // plus the entries whose sign of y changes, all inside the band when the
 // threshold moves less than FUSED_BAND (fused_tv bounds both).  A row whose
 // lambda*, accept decision or bounds do not hold takes the final sweep after
@@ -1463,10 +1491,21 @@ struct FusedConst {
   float lam;      // the node lam_g
   float AL;       // predicted A(lam_g) log2 e: the exponents are y = lam X - AL
   float gsc;      // coef / sum p~ (with the shift's rounding): grad_v = gsc p~_v
+  float kL, K;    // y = fma(t - s, kL, -K): kL = lam log2 e, K = lam cL + AL
+  // the node and centring these float constants give exactly: with
+  // X = (t - s) log2 e - cL, y = lam_e X - AL_e (the roundings of kL and K
+  // are shared by every entry, so they are taken out here, not bounded)
+  double lam_e, AL_e;
+  __device__ void set_y() {
+    kL = lam * LOG2E;
+    K = fmaf(lam, cL, AL);
+    lam_e = static_cast<double>(kL) / static_cast<double>(LOG2E);
+    AL_e = static_cast<double>(K) - lam_e * static_cast<double>(cL);
+  }
 };
 
 struct FusedSums {
-  double v[4];   // W, S1, S2, S3 (log2 units, relative to 2^AL)
+  double v[4];   // W, S1, S2, S3 (moments of y, relative to 2^AL)
   double T0, U0, U1, Bd;
 };
 
@@ -1486,23 +1525,22 @@ __device__ __forceinline__ FusedSums fused_sweep(Block<NT, SH>& B, const T* srow
                       for (int e = 0; e < EPL; ++e) {
                         const float a = fmaf(s[e], LOG2E, -C.msL);
                         const float pt = fexp2(a);
-                        const float X = fmaf(t[e] - s[e], LOG2E, -C.cL);
-                        const float y = fmaf(C.lam, X, -C.AL);
+                        const float y = fmaf(t[e] - s[e], C.kL, -C.K);
                         const float ee = fexp2(y);
-                        const float em1 = (MODE == FIN_ACC) ? expm1_sel(y * LN2, ee) : (ee - 1.0f);
-                        float r = pt * em1;
+                        // r = p~ (e - 1), rounded once in either form
+                        float r = (MODE == FIN_ACC) ? pt * expm1_sel(y * LN2, ee) : fmaf(pt, ee, -pt);
                         float pe = pt + r;
                         if (TAIL && !SAKI_VALID(e)) { r = 0.f; pe = 0.f; }
                         w += r;
-                        const float X2 = X * X;
-                        s1 = fmaf(pe, X, s1);
-                        s2 = fmaf(pe, X2, s2);
-                        s3 = fmaf(pe * X2, X, s3);
+                        const float y2 = y * y;
+                        s1 = fmaf(pe, y, s1);
+                        s2 = fmaf(pe, y2, s2);
+                        s3 = fmaf(pe * y2, y, s3);
                         const bool pos = r > 0.0f;
                         t0 += pos ? r : 0.0f;
                         const float pp = pos ? pe : 0.0f;
                         u0 += pp;
-                        u1 = fmaf(pp, X, u1);
+                        u1 = fmaf(pp, y, u1);
                         bd += (fabsf(y) < FUSED_BAND) ? pe : 0.0f;
                         if (GRAD) g[e] = C.gsc * pt;
                       }
@@ -1554,10 +1592,11 @@ __device__ FusedSums fused_sweep_any(Block<NT, SH>& B, const T* srow, const T* t
 // dominant_fix does for the lambda sweep); the difference corrects W.
 __device__ inline double dominant_fix_fused(float s, float t, const FusedConst& C) {
   const float a = fmaf(s, LOG2E, -C.msL);
-  const float X = fmaf(t - s, LOG2E, -C.cL);
-  const float y = fmaf(C.lam, X, -C.AL);
-  const float rf = fexp2(a) * (fexp2(y) - 1.0f);
-  const double yd = (static_cast<double>(C.lam) * static_cast<double>(X) - static_cast<double>(C.AL)) * LN2_D;
+  const float y = fmaf(t - s, C.kL, -C.K);
+  const float pt = fexp2(a);
+  const float rf = fmaf(pt, fexp2(y), -pt);
+  const double yd = (static_cast<double>(C.kL) * (static_cast<double>(t) - static_cast<double>(s)) -
+                     static_cast<double>(C.K)) * LN2_D;
   return exp2(static_cast<double>(a)) * expm1(yd) - static_cast<double>(rf);
 }
 
@@ -1573,11 +1612,22 @@ __device__ inline LamEval fused_node(const RowStats& R, const FusedSums& S, cons
                                      bool acc) {
   const float msL = R.ms * LOG2E;
   const double corr = shift_correction(R.ms, msL);
-  const double w = S.v[0] + (acc ? 0.0 : dominant_fix_fused(R.ms, R.t_smax, C));
-  double v[5] = {w * corr, S.v[1] * corr, S.v[2] * corr, S.v[3] * corr, 0.0};
-  LamEval E = lam_finish(v, R.sum_s, C.lam, 0.0f, false);
-  E.A += static_cast<double>(C.AL) * LN2_D;
-  E.KL = fmax(E.lam * E.A1 - E.A, 0.0);
+  const double w = (S.v[0] + (acc ? 0.0 : dominant_fix_fused(R.ms, R.t_smax, C))) * corr;
+  const double S0 = R.sum_s + w;
+  // moments of y under q_lam, then those of X = (y + AL) / lam; x = X ln 2
+  const double m1 = S.v[1] * corr / S0, m2 = S.v[2] * corr / S0, m3 = S.v[3] * corr / S0;
+  const double c2 = fmax(m2 - m1 * m1, 0.0);
+  const double c3 = m3 - 3.0 * m1 * m2 + 2.0 * m1 * m1 * m1;
+  const double lam = C.lam_e, il = LN2_D / lam;
+  LamEval E;
+  E.lam = lam;
+  const double lw = log1p(w / R.sum_s);
+  E.A = C.AL_e * LN2_D + lw;
+  E.A1 = (m1 + C.AL_e) * il;
+  E.A2 = c2 * il * il;
+  E.A3 = c3 * il * il * il;
+  // KL = lam A' - A = ln 2 m1 - log1p(W / sum p~): no cancellation against AL
+  E.KL = fmax(LN2_D * m1 - lw, 0.0);
   const double xr = fmax(fabs(static_cast<double>(R.dmax) - R.c - E.A1), fabs(static_cast<double>(R.dmin) - R.c - E.A1));
   E.A4 = xr * xr * E.A2;
   E.reach = end_first ? 0.0 : FUSED_REACH;
@@ -1594,8 +1644,11 @@ struct FusedFinal {
   int why;  // 0: ok; 1: lambda* or the form not from the node; 2: lambda moved too far; 3: TV bound
 };
 
+// acc: the sweep took the expm1 form, where each r carries ~1e-7 of itself as
+// rounding; in the plain form each carries ~6e-8 of p~ e instead, which over
+// P sums to as much as 1e-7 U0.
 __device__ inline FusedFinal fused_tv(const RowStats& R, const LamResult& L, const FinalConst& F,
-                                      const FusedConst& C, const FusedSums& S) {
+                                      const FusedConst& C, const FusedSums& S, bool acc) {
   FusedFinal out;
   out.ok = false;
   out.TV = 0.0;
@@ -1603,30 +1656,30 @@ __device__ inline FusedFinal fused_tv(const RowStats& R, const LamResult& L, con
   out.why = 1;
   if (L.sweeps != 0 || L.qp || F.wide || F.cL != C.cL || F.msL != C.msL) return out;
   out.why = 2;
-  const double dl = static_cast<double>(F.lam) - static_cast<double>(C.lam);
-  const double dA = static_cast<double>(F.AL) - static_cast<double>(C.AL);
-  const double lg = static_cast<double>(C.lam);
+  const double dl = static_cast<double>(F.lam) - C.lam_e;
+  const double dA = static_cast<double>(F.AL) - C.AL_e;
+  const double lg = C.lam_e;
   // |X| over the row (X = d log2 e - cL), with a margin for its rounding
   const double xa = fmax(fabs(static_cast<double>(R.dmax) * LOG2E - C.cL),
                          fabs(static_cast<double>(R.dmin) * LOG2E - C.cL)) * (1.0 + 1e-6) + 1e-6;
   const double hmax = fabs(dl) * xa + fabs(dA);
   // an entry's exponent moves by h = rho y + H0 (X = (y + AL) / lam_g): its
-  // sign changes only where |y| <= |H0| / (1 - |rho|)
+  // sign changes only where |y| <= |H0| / (1 - |rho|) (plus the rounding of y)
   const double rho = dl / lg;
-  const double H0 = dl * static_cast<double>(C.AL) / lg - dA;
+  const double H0 = dl * C.AL_e / lg - dA;
   if (!(fabs(rho) < 0.5)) return out;
-  const double Hf = fabs(H0) / (1.0 - fabs(rho)) + 1e-9;
+  const double Hf = fabs(H0) / (1.0 - fabs(rho)) + 1e-7;
   if (!(Hf < static_cast<double>(FUSED_BAND)) || !(hmax < 0.01)) return out;
   out.why = 3;
   // such an entry's residual at lambda* is below p~ e (2^Hf - 1) on either side
   const double flip = S.Bd * Hf * LN2_D * 1.02;
-  const double tvu = S.T0 + LN2_D * (dl * S.U1 - dA * S.U0);
+  const double tvu = S.T0 + LN2_D * (rho * S.U1 + H0 * S.U0);
   // the rest of 2^h - 1 after its linear term, at most (h ln 2)^2 / 2 (1 + h
-  // ln 2): summed over P with (dl X - dA)^2 <= 2 dl^2 X^2 + 2 dA^2 and
-  // sum_P p~ e X^2 <= S2 (every entry)
+  // ln 2): summed over P with (rho y + H0)^2 <= 2 rho^2 y^2 + 2 H0^2 and
+  // sum_P p~ e y^2 <= S2 (every entry)
   const double h2 = hmax * LN2_D;
-  const double sq = 2.0 * (dl * dl * fabs(S.v[2]) + dA * dA * S.U0);
-  const double err = flip + 0.5 * LN2_D * LN2_D * sq * (1.0 + h2) + 1e-7 * (S.T0 + S.U0 * h2);
+  const double sq = 2.0 * (rho * rho * fabs(S.v[2]) + H0 * H0 * S.U0);
+  const double err = flip + 0.5 * LN2_D * LN2_D * sq * (1.0 + h2) + 1e-7 * ((acc ? S.T0 : S.U0) + S.U0 * h2);
   if (!(tvu > 0.0) || !(err <= FUSED_TV_TOL * tvu)) return out;
   out.ok = true;
   out.why = 0;

@@ -76,7 +76,8 @@ __device__ __forceinline__ unsigned int take_next(unsigned int* counter, unsigne
   return v;
 }
 
-template <typename T, typename G, bool ROUTE, bool GRAD, int KC>
+// K34: the stats sweep sums k3, k4 (radii below K34_EPS).
+template <typename T, typename G, bool ROUTE, bool GRAD, int KC, bool K34>
 __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
   __shared__ RowSharedK<KC> sh;
   __shared__ RowPlan plan;
@@ -105,7 +106,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
     const float M = (ROUTE && P.valid) ? (P.valid[r] ? 1.0f : 0.0f) : 1.0f;
 
     const bool sample_target = ROUTE && P.target_mode == SAKI_TARGET_SAMPLE;
-    const RowStats& R = stats_sweep<T, NT>(B, srow, trow, V, mid_lambda(P.eps), true, sample_target);
+    const RowStats& R = stats_sweep<T, NT, true, K34>(B, srow, trow, V, mid_lambda(P.eps), true, sample_target);
     if (!R.finite) {
       if (GRAD) fill_row<G, NT>(B.wave, B.lane, grow, V, M != 0.0f ? nanf_() : 0.0f);
       if (B.tid == 0) {
@@ -230,6 +231,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
       FC.AL = static_cast<float>(plan.S0.A * static_cast<double>(LOG2E));
       const float invS = static_cast<float>(shift_correction(R.ms, FC.msL) / R.sum_s);
       FC.gsc = coef_g * invS;
+      FC.set_y();
       // the expm1 form where the lambda sweep would take it (KL below
       // KL_ACCURATE: the radius, or KL(pi || p) at the teacher end) and on
       // peaked rows, whose TV the plain form would often leave too imprecise;
@@ -251,7 +253,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
         if (L0.sweeps == 0) {
           F0 = final_const(R, L0, false);
           C0 = !(u < exp(fmin(0.0, L0.log_ratio(sz, tz)))) ? 1 : 0;
-          FF0 = fused_tv(R, L0, F0, FC, FS);
+          FF0 = fused_tv(R, L0, F0, FC, FS, facc);
           state = (FF0.ok && (C0 != 0) == Cg) ? 1 : 0;
         }
         if (B.lane == 0) {
@@ -428,7 +430,7 @@ __device__ void write_skipped(const saki_couple_out& o, int64_t r, int32_t draft
 // VNT threads per workgroup: 256 (two workgroups per CU) for large batches,
 // 512 (one per CU) when a call has no more blocks than CUs, as in rollouts,
 // so that each position's sweeps are spread over eight waves.
-template <typename T, int KC, int VNT>
+template <typename T, int KC, int VNT, bool K34>
 __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyParams P) {
   using SH = RowShared<VNT, (KC > 0 ? CACHED_MAXC : MAX_CHUNKS), KC>;
   __shared__ SH sh;
@@ -468,7 +470,7 @@ __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyP
         next_unwritten = j + 1;
         break;
       }
-      const RowStats& R = stats_sweep<T, VNT>(B, srow, trow, V, mid_lambda(P.eps), false);
+      const RowStats& R = stats_sweep<T, VNT, true, K34>(B, srow, trow, V, mid_lambda(P.eps), false);
       if (!R.finite) {
         if (P.has_pp && B.tid == 0) write_skipped(o, r, z, SAKI_ROW_NONFINITE);
         n = j;
@@ -554,6 +556,7 @@ __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyP
         FC.lam = static_cast<float>(plan.S0.lam);
         FC.AL = static_cast<float>(plan.S0.A * static_cast<double>(LOG2E));
         FC.gsc = 0.0f;
+        FC.set_y();
         const bool facc = (end_first ? R.kl1_est < 1.01 * KL_ACCURATE : P.eps < KL_ACCURATE) || R.pmax > P_PEAKED;
         tv_acc = facc;
         const FusedSums FS = fused_sweep_any<T, float, VNT, false>(B, srow, trow, nullptr, V, FC, facc, reject_g,
@@ -568,7 +571,7 @@ __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyP
           if (L0.sweeps == 0) {
             F0 = final_const(R, L0, false);
             C0 = !(u < exp(fmin(0.0, L0.log_ratio(sz, tz)))) ? 1 : 0;
-            FF0 = fused_tv(R, L0, F0, FC, FS);
+            FF0 = fused_tv(R, L0, F0, FC, FS, facc);
             // settled unless the decision or TV needs the final sweep: a
             // rejection needs valid residual masses (kept only where the
             // start predicted it), TV a valid correction
@@ -1011,16 +1014,43 @@ saki_status launched(const char* what) {
   return SAKI_OK;
 }
 
-template <typename T, typename G, bool ROUTE, bool GRAD>
-saki_status launch_couple(const saki::CoupleParams& P, int grid, hipStream_t st) {
+template <bool K34>
+void launch_verify(const saki::VerifyParams& P, int cus, int grid, bool cached, bool bf16, hipStream_t hs) {
+  if (P.n_blocks <= cus) {
+    // no more blocks than CUs: one 512-thread workgroup per block
+    const dim3 g1(static_cast<unsigned>(P.n_blocks)), b1(512);
+    if (cached)
+      hipLaunchKernelGGL((saki::verify_kernel<uint16_t, saki::CACHE_KC, 512, K34>), g1, b1, 0, hs, P);
+    else if (bf16)
+      hipLaunchKernelGGL((saki::verify_kernel<uint16_t, 0, 512, K34>), g1, b1, 0, hs, P);
+    else
+      hipLaunchKernelGGL((saki::verify_kernel<float, 0, 512, K34>), g1, b1, 0, hs, P);
+  } else if (cached) {
+    hipLaunchKernelGGL((saki::verify_kernel<uint16_t, saki::CACHE_KC, 256, K34>), dim3(grid), dim3(256), 0, hs, P);
+  } else if (bf16) {
+    hipLaunchKernelGGL((saki::verify_kernel<uint16_t, 0, 256, K34>), dim3(grid), dim3(256), 0, hs, P);
+  } else {
+    hipLaunchKernelGGL((saki::verify_kernel<float, 0, 256, K34>), dim3(grid), dim3(256), 0, hs, P);
+  }
+}
+
+template <typename T, typename G, bool ROUTE, bool GRAD, bool K34>
+saki_status launch_couple_k(const saki::CoupleParams& P, int grid, hipStream_t st) {
   if constexpr (sizeof(T) == 2) {
     if ((P.V + saki::CHUNK - 1) / saki::CHUNK <= saki::CACHED_MAXC) {
-      hipLaunchKernelGGL((saki::couple_kernel<T, G, ROUTE, GRAD, saki::CACHE_KC>), dim3(grid), dim3(saki::NT), 0, st, P);
+      hipLaunchKernelGGL((saki::couple_kernel<T, G, ROUTE, GRAD, saki::CACHE_KC, K34>), dim3(grid), dim3(saki::NT), 0,
+                         st, P);
       return launched("couple_kernel");
     }
   }
-  hipLaunchKernelGGL((saki::couple_kernel<T, G, ROUTE, GRAD, 0>), dim3(grid), dim3(saki::NT), 0, st, P);
+  hipLaunchKernelGGL((saki::couple_kernel<T, G, ROUTE, GRAD, 0, K34>), dim3(grid), dim3(saki::NT), 0, st, P);
   return launched("couple_kernel");
+}
+
+template <typename T, typename G, bool ROUTE, bool GRAD>
+saki_status launch_couple(const saki::CoupleParams& P, int grid, hipStream_t st) {
+  return saki::use_k34(P.eps) ? launch_couple_k<T, G, ROUTE, GRAD, true>(P, grid, st)
+                              : launch_couple_k<T, G, ROUTE, GRAD, false>(P, grid, st);
 }
 
 template <typename T>
@@ -1315,22 +1345,10 @@ saki_status saki_spec_verify(const saki_rows* in, int32_t k, const int32_t* draf
   st = launched("clear_counter_kernel");
   if (st != SAKI_OK) return st;
   const bool cached = in->dtype == SAKI_BF16 && (P.V + saki::CHUNK - 1) / saki::CHUNK <= saki::CACHED_MAXC;
-  if (P.n_blocks <= cus) {
-    // no more blocks than CUs: one 512-thread workgroup per block
-    const dim3 g1(static_cast<unsigned>(P.n_blocks)), b1(512);
-    if (cached)
-      hipLaunchKernelGGL((saki::verify_kernel<uint16_t, saki::CACHE_KC, 512>), g1, b1, 0, hs, P);
-    else if (in->dtype == SAKI_BF16)
-      hipLaunchKernelGGL((saki::verify_kernel<uint16_t, 0, 512>), g1, b1, 0, hs, P);
-    else
-      hipLaunchKernelGGL((saki::verify_kernel<float, 0, 512>), g1, b1, 0, hs, P);
-  } else if (cached) {
-    hipLaunchKernelGGL((saki::verify_kernel<uint16_t, saki::CACHE_KC, 256>), dim3(grid), dim3(256), 0, hs, P);
-  } else if (in->dtype == SAKI_BF16) {
-    hipLaunchKernelGGL((saki::verify_kernel<uint16_t, 0, 256>), dim3(grid), dim3(256), 0, hs, P);
-  } else {
-    hipLaunchKernelGGL((saki::verify_kernel<float, 0, 256>), dim3(grid), dim3(256), 0, hs, P);
-  }
+  if (saki::use_k34(P.eps))
+    launch_verify<true>(P, cus, grid, cached, in->dtype == SAKI_BF16, hs);
+  else
+    launch_verify<false>(P, cus, grid, cached, in->dtype == SAKI_BF16, hs);
   st = launched("verify_kernel");
   if (st != SAKI_OK) return st;
   return ok();
