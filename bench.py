@@ -24,25 +24,30 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
 # header of their own, which these kernels do not use).
 _CORE_SOURCES = ["include/saki.h", "paper_2609_36601_amd/csrc/saki.hip", "paper_2609_36601_amd/csrc/row_engine.hpp",
                  "paper_2609_36601_amd/csrc/device_util.hpp"]
-KERNEL_SOURCES = {"couple": _CORE_SOURCES, "route": _CORE_SOURCES, "verify": _CORE_SOURCES,
+KERNEL_SOURCES = {"couple": _CORE_SOURCES, "route": _CORE_SOURCES, "verify": _CORE_SOURCES, "stream": _CORE_SOURCES,
                   "probe": _CORE_SOURCES + ["paper_2609_36601_amd/csrc/probe.hpp"]}
 
-# HBM traffic of one launch of the dominant kernel, from two rocprofv3 --pmc
-# runs (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch): the couple kernel on the
-# large workload at eps 0.2 (profiles/couple_kernel_large.md), the route kernel
-# on the same rows (profiles/route_kernel_large.md) and the probe kernel on
-# 4,096 of them (profiles/probe_kernel_large.md).  A plain 1 GiB device copy
-# reads FETCH_SIZE = 524,309 KiB and WRITE_SIZE = 1,048,576 KiB on the same
-# box, so FETCH_SIZE is scaled by 2.0 and WRITE_SIZE by 1.0.  Keyed by the
-# SHA-256 of the kernel's sources: a changed kernel reports traffic = null
-# until re-measured.
+# HBM traffic of one step of the dominant kernel, from two rocprofv3 --pmc runs
+# (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch): the couple kernel on the large
+# workload at eps 0.2 (its main launch and the short launch that redoes flagged
+# rows, profiles/couple_kernel_large.md), the verify kernel on the verification
+# workload (profiles/verify_kernel.md), the couple kernel on one 4,096-row chunk
+# of the long-rollout workload (mean of five chunks, profiles/couple_kernel_stream.md),
+# the route kernel on the large workload's coupled rows
+# (profiles/route_kernel_large.md) and the probe kernel on 4,096 of them
+# (profiles/probe_kernel_large.md).  A plain 1 GiB device copy in the same runs
+# reads FETCH_SIZE = 524,300-524,320 KiB and WRITE_SIZE = 1,048,576 KiB, so
+# FETCH_SIZE is scaled by 2.0 and WRITE_SIZE by 1.0.  Keyed by the SHA-256 of
+# the kernel's sources: a changed kernel reports traffic = null until re-measured.
+_CORE_HASH = "73d82721b8cf89b8d65bd67c83a60484906e5cdf5b30982c62d31f4be5d87cba"
 MEASURED_TRAFFIC = {
-    "couple": {"a734d2e29a9c6b0c8263f3415efcfe7a5a2f371b6b7dea7f896a98ceeef8676c":
-               dict(fetch_kib=55341600.8, write_kib=41626396.8, fetch_scale=2.0, write_scale=1.0)},
-    "route": {"a734d2e29a9c6b0c8263f3415efcfe7a5a2f371b6b7dea7f896a98ceeef8676c":
-              dict(fetch_kib=17096839.0, write_kib=42813865.5, fetch_scale=2.0, write_scale=1.0)},
-    "probe": {"12ef1ba31790647def0782c558292ca4ac9c1c1157150bd79a38e1349be3ebc8":
-              dict(fetch_kib=1284865.6, write_kib=939.2, fetch_scale=2.0, write_scale=1.0)},
+    "couple": {_CORE_HASH: dict(fetch_kib=39329667.9 + 53.4, write_kib=42114071.1 + 10768.0,
+                                fetch_scale=2.0, write_scale=1.0)},
+    "verify": {_CORE_HASH: dict(fetch_kib=13633056.1, write_kib=105962.0, fetch_scale=2.0, write_scale=1.0)},
+    "stream": {_CORE_HASH: dict(fetch_kib=2726036.8, write_kib=2861585.1, fetch_scale=2.0, write_scale=1.0)},
+    "route": {_CORE_HASH: dict(fetch_kib=17097121.4, write_kib=41992042.7, fetch_scale=2.0, write_scale=1.0)},
+    "probe": {"8797beda64966ea6e87c9238c8236c0c938d0aeb0a5eadebc3278b79a7f749f7":
+              dict(fetch_kib=1284928.5, write_kib=961.9, fetch_scale=2.0, write_scale=1.0)},
 }
 
 
@@ -60,6 +65,15 @@ def measured_traffic_bytes(workload="couple"):
     if m is None:
         return None
     return (m["fetch_kib"] * m["fetch_scale"] + m["write_kib"] * m["write_scale"]) * 1024.0
+
+
+def stream_traffic_bytes(n_chunks, rows):
+    """HBM bytes of the whole long-rollout step: the measured mean of one
+    4,096-row launch times the launches, for the full 262,144 rows only."""
+    per = measured_traffic_bytes("stream")
+    if per is None or rows != 262144 or n_chunks != 64:
+        return None
+    return per * n_chunks
 
 
 def _oracle_rows(args):
@@ -256,13 +270,7 @@ def main():
                      device=dev)
     torch.cuda.synchronize()
     if args.calibrate_copy:
-        # a plain copy of known size: its FETCH_SIZE / WRITE_SIZE per byte moved
-        # scales the counters read for the coupling kernel
-        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+        calibration_copy(dev)
 
     ms, per, wall = time_calls(lambda: saki.saki_couple(s, t, args.eps, seed, 0, out, route, ws),
                                args.steps, args.warmup)
@@ -337,6 +345,18 @@ def main():
         "other_configs": others,
     }
     print(json.dumps(line), flush=True)
+
+
+def calibration_copy(dev):
+    """One plain 1 GiB device-to-device copy: its FETCH_SIZE / WRITE_SIZE per
+    byte moved scales the counters read for the measured kernel in the same run."""
+    import torch
+    src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+    torch.cuda.empty_cache()
 
 
 def time_calls(call, steps, warmup):
@@ -419,7 +439,8 @@ def stream_suite(saki, workloads, dev, s_buf, t_buf, grad_buf, warmup):
                 value=n_total / (total_ms * 1e-3), unit="positions/s", ms_per_step=total_ms,
                 chunks=n_total // chunk,
                 roofline=dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
-                              frac=achieved / HBM_PEAK_GBS),
+                              frac=achieved / HBM_PEAK_GBS,
+                              traffic=stream_traffic_bytes(n_total // chunk, n_total)),
                 stats=dict(correction_rate=corr / n_total, mean_tv=tv / n_total))
 
 
@@ -460,6 +481,8 @@ def bench_verify(args, saki, workloads, dev):
     corr = torch.empty(nb, dtype=torch.int32, device=dev)
     ws = torch.empty(max(saki.workspace_bytes(saki.SAKI_OP_VERIFY, n, V), 8), dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
+    if args.calibrate_copy:
+        calibration_copy(dev)
 
     def step():
         saki.saki_spec_verify(s, t, k, draft, args.eps, seed, 0, -1, acc, corr, None, ws)
@@ -526,7 +549,8 @@ def bench_verify(args, saki, workloads, dev):
                    "mean_accepted_length": float(al.mean()), "positions_evaluated": evaluated},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "attainable_read": attainable,
-                     "frac_attainable": achieved / attainable, "traffic": None},
+                     "frac_attainable": achieved / attainable,
+                     "traffic": measured_traffic_bytes("verify") if n == cfg["rows"] and args.eps == 0.2 else None},
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
@@ -557,6 +581,8 @@ def bench_route(args, saki, workloads, dev):
     loss_sum = torch.empty(1, dtype=torch.float64, device=dev)
     ws = torch.empty(max(saki.workspace_bytes(saki.SAKI_OP_ROUTE, n, V), 8), dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
+    if args.calibrate_copy:
+        calibration_copy(dev)
 
     def step():
         saki.saki_route_loss(s, out["token"], out["corrected"], out["teacher_argmax"], adv,
@@ -619,6 +645,8 @@ def bench_probe(args, saki, workloads, dev):
                topk=torch.empty(n, k, dtype=torch.int32, device=dev),
                row_status=torch.empty(n, dtype=torch.uint8, device=dev))
     torch.cuda.synchronize()
+    if args.calibrate_copy:
+        calibration_copy(dev)
 
     def step():
         saki.saki_probe_metrics(s, t, k, **out)
@@ -785,6 +813,8 @@ def bench_stream(args, saki, workloads, dev):
     ws = torch.empty(max(saki.workspace_bytes(saki.SAKI_OP_COUPLE, chunk, V), 8), dtype=torch.uint8,
                      device=dev)
     total_ms, rows, corr, tv = 0.0, 0, 0.0, 0.0
+    if args.calibrate_copy:
+        calibration_copy(dev)
     for c in range(n_chunks):
         lo = c * chunk
         n = min(chunk, n_total - lo)
@@ -826,7 +856,7 @@ def bench_stream(args, saki, workloads, dev):
                    "rows": rows, "vocab": V, "eps": eps, "chunks": n_chunks},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "attainable_read": attainable,
-                     "frac_attainable": achieved / attainable, "traffic": None},
+                     "frac_attainable": achieved / attainable, "traffic": stream_traffic_bytes(n_chunks, rows)},
         "cpu_baseline": None,
         "stats": {"correction_rate": corr / rows, "mean_tv": tv / rows},
     }

@@ -1088,27 +1088,40 @@ struct HermiteA {
 struct StartPoint {
   double lam;  // the first node
   double A;    // A(lam) predicted by the interpolant (herm only)
-  bool herm;   // lam solves KL = eps on the interpolant, within 30% of the end starts
+  bool herm;   // lam solves KL = eps on the interpolant, on the middle node's side
 };
 
 constexpr double LAM_MAX = 1.0 - 1e-6;
 
-// The interpolant's root of KL = eps near l0 (S unchanged when it is not
-// found, lies more than 30% from l0, or the interpolant is not convex there).
+// The interpolant's root of KL = eps from l0 (S unchanged when it is not
+// found, lies on the wrong side of the middle node, or the interpolant is not
+// convex there).
 template <int N0>
 __device__ inline void hermite_refine(const RowStats& R, double eps, double l0, StartPoint& S) {
   const HermiteA<N0> H(R);
   double p, p1, p2;
   H.eval(1.0, p, p1, p2);
   if (!(p1 - p > eps)) return;  // the interpolant puts lambda* at 1
+  // KL increases with lambda, so KL at the middle node (known from the stats
+  // sweep, which the interpolant matches there) tells on which side of it
+  // lambda* lies: the search keeps to that side.  The ends' starts can be far
+  // off on rows whose largest d dominate q_lambda, where the interpolant is
+  // still close, so l0 only seeds the search.
+  const double lm = static_cast<double>(R.lam_mid);
+  const bool above = lm * R.mid_A1 - R.mid_A <= eps;
+  const double blo = above ? lm : 0.0, bhi = above ? 1.0 : lm;
   // safeguarded Newton on KL(l) = l A'(l) - A(l) = eps (KL' = l A''),
   // keeping the bracket KL(lo) <= eps < KL(hi)
   // (converged once the step is below 1e-10 of lambda: the interpolant's own
   // rounding, ~1e-12 of lambda near the root, would otherwise send a
   // tighter test into the bisection branch)
-  double lo = 0.0, hi = 1.0, l = l0;
+  double lo = blo, hi = bhi;
+  // the search starts from l0, moved inside the bracket when outside it (to
+  // its nearer end, so that Newton does not start among the interpolant's
+  // other roots far from both)
+  double l = fmin(fmax(l0, blo + 1e-6 * (bhi - blo)), bhi - 1e-6 * (bhi - blo));
   bool conv = false;
-  for (int it = 0; it < 10; ++it) {
+  for (int it = 0; it < 14; ++it) {
     H.eval(l, p, p1, p2);
     const double f = l * p1 - p - eps;
     if (f <= 0.0) lo = l; else hi = l;
@@ -1122,7 +1135,7 @@ __device__ inline void hermite_refine(const RowStats& R, double eps, double l0, 
     if (!(nl > lo && nl < hi)) nl = 0.5 * (lo + hi);
     l = nl;
   }
-  if (!conv || !(fabs(l - l0) <= 0.3 * l0) || !(l < LAM_MAX)) return;
+  if (!conv || !(l > blo && l < bhi) || !(l < LAM_MAX)) return;
   H.eval(l, p, p1, p2);
   if (!(p2 > 0.0) || !isfinite(p)) return;
   S.lam = l;
