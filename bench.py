@@ -279,6 +279,7 @@ def main():
     bytes_per_row = 2 * V * 2 + V * 4  # s + t read once (bf16), fp32 gradient written once
     achieved = n * bytes_per_row / (ms * 1e-3) / 1e9
     corr_rate = float(out["corrected"].float().mean())
+    near_margin = near_margin_rows(out)
     mean_tv = float(out["tv"].mean())
     mean_lam = float(out["lambda"].mean())
     print(f"# correction rate {corr_rate:.4f}, mean TV {mean_tv:.4f}, mean lambda {mean_lam:.4f}",
@@ -310,7 +311,8 @@ def main():
                 value=n / (ms_o * 1e-3), unit="positions/s", ms_per_step=ms_o, steps=steps_o,
                 roofline=dict(bound="hbm", achieved=ach_o, peak=HBM_PEAK_GBS, unit="GB/s", frac=ach_o / HBM_PEAK_GBS),
                 stats=dict(correction_rate=float(out["corrected"].float().mean()),
-                           mean_tv=float(out["tv"].mean()), mean_lambda=float(out["lambda"].mean())))
+                           mean_tv=float(out["tv"].mean()), mean_lambda=float(out["lambda"].mean()),
+                           near_margin_rows=near_margin_rows(out)))
             print(f"# large eps {eps_o}: {ms_o:.3f} ms", file=sys.stderr, flush=True)
         del out, route, ws
         # the verify workload in the same (n, V) buffers
@@ -341,10 +343,17 @@ def main():
                      "attainable_read": attainable, "frac_attainable": achieved / attainable,
                      "traffic": measured_traffic_bytes() if n == cfg["rows"] and args.eps == 0.2 else None},
         "cpu_baseline": cpu,
-        "stats": {"correction_rate": corr_rate, "mean_tv": mean_tv, "mean_lambda": mean_lam},
+        "stats": {"correction_rate": corr_rate, "mean_tv": mean_tv, "mean_lambda": mean_lam,
+                  "near_margin_rows": near_margin},
         "other_configs": others,
     }
     print(json.dumps(line), flush=True)
+
+
+def near_margin_rows(out):
+    """Rows whose accept decision lies within 1e-6 of its threshold (|u - alpha|):
+    the rows a comparison with the oracle may excuse."""
+    return int((out["margin"] < 1e-6).sum())
 
 
 def calibration_copy(dev):
