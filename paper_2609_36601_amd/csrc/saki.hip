@@ -521,10 +521,14 @@ __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyP
       // Positions the interpolating start places well take the fused sweep
       // (the lambda node, and the residual chunk masses where the start
       // predicts a rejection); the others the lambda search and, when
-      // rejected or when TV is asked for, the final sweep.
+      // rejected or when TV is asked for, the final sweep.  With one
+      // workgroup per CU (rollout waves) a position's steps are not hidden
+      // behind another workgroup's, and the fused sweep's serial start and
+      // settling cost more than the lambda sweep they replace: every position
+      // takes the search there.
       const bool end_first = R.kl1_est <= 1.05 * P.eps + 1e-5;
       if (B.wave == 0) {
-        bool fu = !force_acc && P.eps > 0.0 && R.dmin != R.dmax;
+        bool fu = VNT == 256 && !force_acc && P.eps > 0.0 && R.dmin != R.dmax;
         StartPoint S0;
         S0.lam = 1.0; S0.A = R.lse_t - R.lse_s - static_cast<double>(R.c); S0.herm = true;
         if (fu) {
