@@ -494,7 +494,25 @@ __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyP
           const double xz = static_cast<double>(tz) - static_cast<double>(sz) - static_cast<double>(R.c);
           const double gm = lm * xz - R.mid_A;
           const double klm = lm * R.mid_A1 - R.mid_A;
-          const double lo_side = fmin(0.0, gm), hi_side = fmin(gm, lr1);
+          // Above the middle node the bracket ends below 1 where convexity
+          // alone forces KL > eps.  With A and A' known at lm and 1, the
+          // tangent of A at lambda lies below A at lm, so A'(lambda) >=
+          // (A(lambda) - A(lm)) / (lambda - lm), and A(lambda) lies above the
+          // tangent at 1; together KL(lambda) >= (lm T1(lambda) - lambda A(lm))
+          // / (lambda - lm), T1 that tangent, which passes eps at lh below.
+          // On [lm, lh] g lies above lambda x_z minus the chord of A from lm
+          // to 1 (A is convex), a line: its smaller end value bounds g.
+          // Guards keep lh away from cancellations in the float sums.
+          const double A1 = R.lse_t - R.lse_s - static_cast<double>(R.c);
+          const double D1 = R.mean_pi - static_cast<double>(R.c);
+          const double num = R.kl1_est - P.eps, den = lm * D1 - R.mid_A - P.eps;
+          double g_hi = lr1;
+          if (num > 1e-2 * (fabs(R.kl1_est) + P.eps) &&
+              den > 1e-2 * (fabs(lm * D1) + fabs(R.mid_A) + P.eps)) {
+            const double lh = fmax(lm, lm * num / den * (1.0 + 1e-3) + 1e-6);
+            if (lh < 1.0) g_hi = lh * xz - (R.mid_A + (A1 - R.mid_A) * (lh - lm) / (1.0 - lm));
+          }
+          const double lo_side = fmin(0.0, gm), hi_side = fmin(gm, g_hi);
           const double gb = (klm < P.eps * (1.0 - 1e-3)) ? hi_side : (klm > P.eps * (1.0 + 1e-3)) ? lo_side
                                                                      : fmin(lo_side, hi_side);
           gmin = fmax(gmin, gb - 2e-6);
