@@ -51,6 +51,30 @@ MEASURED_TRAFFIC = {
 }
 
 
+# VALU instructions (wave64, SQ_INSTS_VALU) of one launch of the dominant
+# kernel, from the rocprofv3 --pmc run of the same sources (the couple kernel
+# on the large workload at eps 0.2, the verify kernel on the verification
+# workload).  Their issue rate is the bound these kernels meet first: a CU
+# issues at most one wave64 VALU instruction per cycle (four SIMDs of 16 lanes,
+# four cycles each), 256 CUs x 2.4 GHz = 6.14e11 per second.
+VALU_ISSUE_PEAK = 256 * 2.4e9
+MEASURED_VALU = {
+    "couple": {_CORE_HASH: 9.793e9},
+    "verify": {_CORE_HASH: 3.202e9},
+}
+
+
+def valu_issue(workload, ms):
+    """The measured VALU instructions per launch over the launch time, against
+    the issue peak (None when the kernel changed after its counters)."""
+    n = MEASURED_VALU.get(workload, {}).get(kernel_source_hash(workload))
+    if n is None:
+        return None
+    achieved = n / (ms * 1e-3)
+    return {"instructions": n, "achieved": achieved, "peak": VALU_ISSUE_PEAK, "unit": "wave64 instr/s",
+            "frac": achieved / VALU_ISSUE_PEAK}
+
+
 def kernel_source_hash(workload="couple"):
     import hashlib
     h = hashlib.sha256()
@@ -341,7 +365,8 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,
                      "attainable_read": attainable, "frac_attainable": achieved / attainable,
-                     "traffic": measured_traffic_bytes() if n == cfg["rows"] and args.eps == 0.2 else None},
+                     "traffic": measured_traffic_bytes() if n == cfg["rows"] and args.eps == 0.2 else None,
+                     "valu_issue": valu_issue("couple", ms) if n == cfg["rows"] and args.eps == 0.2 else None},
         "cpu_baseline": cpu,
         "stats": {"correction_rate": corr_rate, "mean_tv": mean_tv, "mean_lambda": mean_lam,
                   "near_margin_rows": near_margin},
@@ -413,7 +438,8 @@ def verify_suite(saki, workloads, dev, s, t, steps, warmup):
                 value=nb / (ms * 1e-3), unit="blocks/s", ms_per_step=ms, steps=steps,
                 mean_accepted_length=float(al.mean()), positions_evaluated=evaluated,
                 roofline=dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
-                              frac=achieved / HBM_PEAK_GBS, traffic=measured_traffic_bytes("verify")))
+                              frac=achieved / HBM_PEAK_GBS, traffic=measured_traffic_bytes("verify"),
+                              valu_issue=valu_issue("verify", ms)))
 
 
 def stream_suite(saki, workloads, dev, s_buf, t_buf, grad_buf, warmup):

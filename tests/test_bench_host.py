@@ -40,3 +40,15 @@ def test_traffic_table_is_keyed_by_source_hash():
         assert (t is None) == (h not in bench.MEASURED_TRAFFIC[w])
         if t is not None:
             assert floor[w] < t < 5 * floor[w]
+
+
+def test_valu_issue_is_keyed_by_source_hash():
+    sys.path.insert(0, ROOT)
+    import bench
+    for w in ("couple", "verify"):
+        v = bench.valu_issue(w, 20.0)
+        assert (v is None) == (bench.kernel_source_hash(w) not in bench.MEASURED_VALU[w])
+        if v is not None:
+            # at most one wave64 VALU instruction per CU and cycle
+            assert 0.0 < v["frac"] and v["peak"] == 256 * 2.4e9
+            assert v["achieved"] == v["instructions"] / 20e-3
