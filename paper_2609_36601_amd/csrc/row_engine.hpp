@@ -1712,6 +1712,8 @@ struct RowPlan {
   int fused;   // the row takes the fused sweep
   int state;   // after it: 1 settled, 0 final sweep after all, -1 the search needs sweeps
   int C;       // the accept decision at lambda* (state >= 0)
+  int z;       // the proposal, and its s and t (wave_proposal)
+  float sz, tz;
 };
 
 // The chunk level of the residual race from masses known within bounds
@@ -1982,6 +1984,68 @@ __device__ int elem_pick(Block<NT, SH>& B, const ElemFetch<T>& f, int c, int V, 
     }
   }
   B.argmin_with(best, bi, bs, bt);
+  *s_win = bs;
+  *t_win = bt;
+  return bi;
+}
+
+// The two-level race of chunk_race and elem_race run by one wave alone (same
+// uniforms, keys and ties), so that it can overlap other waves' serial
+// steps: the chunk keys in double, chunks lane, lane + 64, ...; then the
+// entries of the winning chunk, four consecutive ones per load as elem_fetch
+// takes them (a lane covers the four quarter-chunks j = 0..3 of a 256-thread
+// block's layout).  chunk_logw(c) as for chunk_race; logw(s, t, v) as for
+// elem_pick.  Returns the winner (or >= V if no entry has weight) with its s
+// and t, on every lane.
+template <typename T, typename FC, typename FE>
+__device__ int wave_proposal(const T* srow, const T* trow, int nchunks, int V, int lane, uint64_t seed,
+                             uint32_t chunk_stream, uint32_t elem_stream, uint64_t g, FC chunk_logw, FE logw,
+                             float* s_win, float* t_win) {
+  double ck = __builtin_huge_val();
+  int ci = 0x7fffffff;
+  for (int c = lane; c < nchunks; c += WAVE) {
+    const double lw = chunk_logw(c);
+    if (lw > -__builtin_huge_val()) {
+      const double u = static_cast<double>(philox_uniform(seed, chunk_stream, g, static_cast<uint32_t>(c)));
+      const double key = log(-log(u)) - lw;
+      if (key < ck) { ck = key; ci = c; }
+    }
+  }
+  wave_argmin(ck, ci);
+  const int c = ci < nchunks ? ci : 0;
+  const int hi = min(V, c * CHUNK + CHUNK);
+  float best = finf(), bs = 0.0f, bt = 0.0f;
+  int bi = 0x7fffffff;
+#pragma unroll
+  for (int j = 0; j < CHUNK / (4 * WAVE); ++j) {
+    const ElemFetch<T> f = elem_fetch<T, CHUNK / 4>(srow, trow, c, V, lane + WAVE * j);
+    if (f.v0 < hi) {
+      const uint4 w = philox_block(seed, elem_stream, g, static_cast<uint32_t>(f.v0 >> 2));
+      const uint32_t words[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int v = f.v0 + k;
+        if (v < hi) {
+          const float sk = f.s(k), tk = f.t(k);
+          const float lw = logw(sk, tk, v);
+          if (lw > -finf()) {
+            const float u = word_to_uniform(words[k]);
+            const float E = -flog2(u) * LN2;
+            const float key = flog2(E) * LN2 - lw;
+            if (key < best) { best = key; bi = v; bs = sk; bt = tk; }
+          }
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int o = WAVE / 2; o > 0; o >>= 1) {
+    const float k2 = __shfl_xor(best, o, WAVE);
+    const int i2 = __shfl_xor(bi, o, WAVE);
+    const float a2 = __shfl_xor(bs, o, WAVE);
+    const float b2 = __shfl_xor(bt, o, WAVE);
+    if (k2 < best || (k2 == best && i2 < bi)) { best = k2; bi = i2; bs = a2; bt = b2; }
+  }
   *s_win = bs;
   *t_win = bt;
   return bi;

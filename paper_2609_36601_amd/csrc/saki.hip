@@ -134,14 +134,8 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
       continue;
     }
 
-    // z ~ p by the two-level race (chunk masses from the stats sweep): the
-    // chunk race, then the entry race in the winning chunk.  The logit of the
-    // teacher mode (the loss and gradient at a correction) is loaded early.
-    const int c0 = chunk_race<NT>(B, nch, P.seed, PROP_CHUNK, g, [&](int c) {
-      return static_cast<double>(sh.chunk_a[c]) * LN2_D + log(static_cast<double>(sh.chunk_b[c]));
-    });
-    const int cz = c0 < nch ? c0 : 0;
-    const ElemFetch<T> fz = elem_fetch<T, NT>(srow, trow, cz, V, B.tid);
+    // The logit of the teacher mode (the loss and gradient at a correction) is
+    // loaded early.
     const float s_vstar = Loader<T>::load1(srow + R.vstar);
 
     // Rows the interpolating start places well take the fused sweep (the
@@ -149,9 +143,11 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
     // whose teacher end may be feasible (the node lambda = 1, where A is known
     // exactly); the others, and fused rows whose checks fail, the lambda
     // search and the final sweep.
-    // The serial steps between sweeps run on wave 0 alone, which leaves the
-    // other waves' issue slots to the other workgroup of the CU; the results
-    // go through LDS (plan).
+    // The serial steps between sweeps run on one wave at a time: wave 0 the
+    // start point while wave 1 draws the proposal z ~ p (the two-level race on
+    // the stats sweep's chunk masses, then the entry race in the winning
+    // chunk), which leaves the other waves' issue slots to the other
+    // workgroup of the CU; the results go through LDS (plan).
     const bool end_first = R.kl1_est <= 1.05 * P.eps + 1e-5;
     if (B.wave == 0) {
       bool fu = !force_acc && P.eps > 0.0 && R.dmin != R.dmax;
@@ -166,13 +162,25 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void couple_kernel(CoupleParams P) {
         plan.S0 = S0;
         plan.fused = fu ? 1 : 0;
       }
+    } else if (B.wave == 1) {
+      float ws, wt;
+      const int zz = wave_proposal<T>(srow, trow, nch, V, B.lane, P.seed, PROP_CHUNK, PROP_ELEM, g,
+                                      [&](int c) {
+                                        return static_cast<double>(sh.chunk_a[c]) * LN2_D +
+                                               log(static_cast<double>(sh.chunk_b[c]));
+                                      },
+                                      [](float sv, float, int) { return sv; }, &ws, &wt);
+      if (B.lane == 0) {
+        plan.z = zz;
+        plan.sz = ws;
+        plan.tz = wt;
+      }
     }
     __syncthreads();
     const bool fused = plan.fused != 0;
 
-    float sz, tz;
-    int z = elem_pick<NT>(B, fz, cz, V, P.seed, PROP_ELEM, g,
-                          [&](float sv, float, int) { return sv; }, &sz, &tz);
+    float sz = plan.sz, tz = plan.tz;
+    int z = plan.z;
     if (z >= V) {  // unreachable for finite rows: every chunk has a winner
       z = R.vstar;
       sz = s_vstar;
